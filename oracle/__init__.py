@@ -1,0 +1,227 @@
+"""CPU oracle for the WhiFlash target-verification step (fp64, plain loops).
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by the smoke check and by the
+benchmark's CPU-baseline leg, never by the product path.  It shares no code
+with the GPU library (paper_2606_07710_amd).
+
+The arithmetic lives in wfref.c; this module only marshals numpy arrays.
+Storage codes: float32 arrays -> fp32, uint16 arrays -> bf16 bit patterns,
+float64 arrays -> fp64.  Every result is fp64.
+
+Paper: arXiv 2606.07710 (WhiFlash).  What each call computes:
+  verify_attn      -- Sec. 3.2 parallel verification of the drafted block:
+                      block-causal grouped-query softmax attention against
+                      the KV cache.
+  kv_only_prefill  -- Sec. 3.4 "KV-only Prefill": K/V projection, RoPE on K.
+  lmhead_rows      -- Sec. 3.3.1: next-token logits, argmax and the entropy
+                      H = -sum p log p of the softmax distribution.
+  accept           -- greedy acceptance of the longest matching draft prefix
+                      plus the Sec. 3.3.1 entropy routing rule (H > tau -> AR).
+  layer_forward    -- a full single attention layer, used to pin that KV-only
+                      prefill yields the cache a full forward would.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libwfref.so")
+_lib = None
+
+_CODES = {np.dtype(np.float32): 0, np.dtype(np.uint16): 1,
+          np.dtype(np.float64): 2}
+
+_p = ctypes.c_void_p
+_i = ctypes.c_int
+_d = ctypes.c_double
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _b
+        _b.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.wfref_num_threads.restype = _i
+    lib.wfref_verify_attn.argtypes = [_i, _p, _p, _p, _p, _i, _i, _i, _i, _i,
+                                      _i, _d]
+    lib.wfref_verify_attn_rows.argtypes = [_i, _p, _p, _p, _p, _i, _i, _i, _i,
+                                           _i, _i, _d, _i, _p]
+    lib.wfref_kv_only_prefill.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i,
+                                          _i, _i, _d]
+    lib.wfref_lmhead_rows.argtypes = [_i, _p, _p, _p, _i, _i, _i, _p, _p, _p,
+                                      _p]
+    lib.wfref_accept.argtypes = [_p, _p, _p, _i, _d, _p, _p]
+    lib.wfref_rope_inplace.argtypes = [_p, _i, _d, _d]
+    lib.wfref_rope_inplace.restype = None
+    lib.wfref_layer_forward.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i, _i,
+                                        _i, _i, _d, _d, _p, _p, _p, _p, _p]
+    for name in ("wfref_verify_attn", "wfref_verify_attn_rows",
+                 "wfref_kv_only_prefill", "wfref_lmhead_rows", "wfref_accept",
+                 "wfref_layer_forward"):
+        getattr(lib, name).restype = _i
+    _lib = lib
+    return lib
+
+
+def _arr(a):
+    a = np.ascontiguousarray(a)
+    if a.dtype not in _CODES:
+        raise TypeError(f"oracle input dtype {a.dtype} not supported")
+    return a, _CODES[a.dtype]
+
+
+def _ptr(a):
+    return ctypes.c_void_p(a.ctypes.data) if a is not None else None
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise ValueError(f"oracle {what} rejected its arguments (rc={rc})")
+
+
+def num_threads() -> int:
+    return int(_load().wfref_num_threads())
+
+
+def verify_attn(q, k_cache, v_cache, ctx_len, scale=None):
+    """q [gamma][Hq][D]; caches [Hkv][cap][D] (same storage); -> fp64 out."""
+    lib = _load()
+    q, code = _arr(q)
+    k_cache, c2 = _arr(k_cache)
+    v_cache, c3 = _arr(v_cache)
+    if not (code == c2 == c3):
+        raise TypeError("q and caches must share a storage type")
+    gamma, hq, dh = q.shape
+    hkv, cap, dh2 = k_cache.shape
+    if dh2 != dh or v_cache.shape != k_cache.shape:
+        raise ValueError("shape mismatch")
+    if scale is None:
+        scale = 1.0 / np.sqrt(dh)
+    out = np.empty((gamma, hq, dh), np.float64)
+    rc = lib.wfref_verify_attn(code, _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                               _ptr(out), gamma, int(ctx_len), cap, hq, hkv,
+                               dh, float(scale))
+    _check(rc, "verify_attn")
+    return out
+
+
+def verify_attn_rows(q, k_cache, v_cache, ctx_len, rows_heads, scale=None):
+    """Attention output at the listed (block row, q head) pairs only."""
+    lib = _load()
+    q, code = _arr(q)
+    k_cache, _ = _arr(k_cache)
+    v_cache, _ = _arr(v_cache)
+    gamma, hq, dh = q.shape
+    hkv, cap, _ = k_cache.shape
+    rh = np.ascontiguousarray(np.asarray(rows_heads, np.int32).reshape(-1, 2))
+    if scale is None:
+        scale = 1.0 / np.sqrt(dh)
+    out = np.empty((rh.shape[0], dh), np.float64)
+    rc = lib.wfref_verify_attn_rows(code, _ptr(q), _ptr(k_cache),
+                                    _ptr(v_cache), _ptr(out), gamma,
+                                    int(ctx_len), cap, hq, hkv, dh,
+                                    float(scale), rh.shape[0], _ptr(rh))
+    _check(rc, "verify_attn_rows")
+    return out
+
+
+def kv_only_prefill(x, w_k, w_v, start_pos, n_kv_heads, head_dim, rope_base):
+    """x [n][d_in]; w_k, w_v [Hkv*D][d_in] -> (K, V) each [Hkv][n][D] fp64."""
+    lib = _load()
+    x, code = _arr(x)
+    w_k, _ = _arr(w_k)
+    w_v, _ = _arr(w_v)
+    n_tok, d_in = x.shape
+    k = np.empty((n_kv_heads, n_tok, head_dim), np.float64)
+    v = np.empty_like(k)
+    rc = lib.wfref_kv_only_prefill(code, _ptr(x), _ptr(w_k), _ptr(w_v),
+                                   _ptr(k), _ptr(v), n_tok, int(start_pos),
+                                   d_in, n_kv_heads, head_dim,
+                                   float(rope_base))
+    _check(rc, "kv_only_prefill")
+    return k, v
+
+
+def lmhead_rows(h=None, w=None, logits=None, want_logits=False):
+    """Per-row argmax (int32), entropy (nats), top-2 margin, optional logits.
+
+    Either (h [gamma][d], w [vocab][d]) or logits [gamma][vocab] float32.
+    """
+    lib = _load()
+    if logits is not None:
+        logits = np.ascontiguousarray(logits, np.float32)
+        gamma, vocab = logits.shape
+        d, code = 0, 0
+        hp = wp = None
+    else:
+        h, code = _arr(h)
+        w, c2 = _arr(w)
+        if code != c2:
+            raise TypeError("h and w must share a storage type")
+        gamma, d = h.shape
+        vocab = w.shape[0]
+        hp, wp = h, w
+    am = np.empty(gamma, np.int32)
+    ent = np.empty(gamma, np.float64)
+    margin = np.empty(gamma, np.float64)
+    z = np.empty((gamma, vocab), np.float64) if want_logits else None
+    rc = lib.wfref_lmhead_rows(code, _ptr(hp), _ptr(wp), _ptr(logits), gamma,
+                               d, vocab, _ptr(am), _ptr(ent), _ptr(margin),
+                               _ptr(z))
+    _check(rc, "lmhead_rows")
+    if want_logits:
+        return am, ent, margin, z
+    return am, ent, margin
+
+
+def accept(argmax, entropy, draft, tau):
+    """-> (n_accepted, bonus, route, H_t)."""
+    lib = _load()
+    argmax = np.ascontiguousarray(argmax, np.int32)
+    entropy = np.ascontiguousarray(entropy, np.float64)
+    gamma = argmax.shape[0]
+    dr = np.ascontiguousarray(draft, np.int32) if gamma > 1 else None
+    if dr is not None and dr.shape[0] != gamma - 1:
+        raise ValueError("draft must hold gamma-1 tokens")
+    out3 = np.empty(3, np.int32)
+    ht = ctypes.c_double()
+    rc = lib.wfref_accept(_ptr(argmax), _ptr(entropy), _ptr(dr), gamma,
+                          float(tau), _ptr(out3), ctypes.byref(ht))
+    _check(rc, "accept")
+    return int(out3[0]), int(out3[1]), int(out3[2]), float(ht.value)
+
+
+def rope(v, pos, base):
+    """RoPE (rotate-half) of a fp64 vector at position pos."""
+    lib = _load()
+    v = np.array(v, np.float64, copy=True)
+    lib.wfref_rope_inplace(_ptr(v), v.shape[0], float(pos), float(base))
+    return v
+
+
+def layer_forward(x, gain, w_q, w_k, w_v, pos0, n_q_heads, n_kv_heads,
+                  head_dim, rms_eps, rope_base):
+    """Full single-layer forward; returns dict of fp64 arrays."""
+    lib = _load()
+    x, code = _arr(x)
+    gain, _ = _arr(gain)
+    w_q, _ = _arr(w_q)
+    w_k, _ = _arr(w_k)
+    w_v, _ = _arr(w_v)
+    T, d = x.shape
+    xn = np.empty((T, d), np.float64)
+    q = np.empty((T, n_q_heads, head_dim), np.float64)
+    k = np.empty((n_kv_heads, T, head_dim), np.float64)
+    v = np.empty_like(k)
+    out = np.empty_like(q)
+    rc = lib.wfref_layer_forward(code, _ptr(x), _ptr(gain), _ptr(w_q),
+                                 _ptr(w_k), _ptr(w_v), T, int(pos0), d,
+                                 n_q_heads, n_kv_heads, head_dim,
+                                 float(rms_eps), float(rope_base), _ptr(xn),
+                                 _ptr(q), _ptr(k), _ptr(v), _ptr(out))
+    _check(rc, "layer_forward")
+    return {"xn": xn, "q": q, "k": k, "v": v, "out": out}
