@@ -1,0 +1,349 @@
+#!/usr/bin/env python3
+"""Benchmark of the WhiFlash verification step on one MI355X.
+
+One step = the whole hot path over one synthetic batch, issued on one
+stream in model order:
+  n_layers x wf_verify_attn      (block-causal GQA attention vs the cache)
+  n_layers x wf_kv_only_prefill  (catch-up K/V projection + RoPE + append)
+  1 x wf_lmhead_accept_entropy   (LM head -> argmax, entropy, accept, route)
+(the router-heavy workload adds the logits-only LM-head call).  Inputs are
+seeded synthetic tensors already resident in HBM.  The default workload is
+8B shapes at 32K context with a 16-token block (36 layers).
+
+Output: ONE JSON line.  `value` is the verify-step time in microseconds
+(lower is better); the roofline object reports the dominant kernel, the
+per-layer verify attention, against HBM bandwidth using the algorithmic
+bytes of one call; cpu_baseline is the fp64 oracle timed on host cores on a
+bounded sample of the same step, scaled to one step.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3,
+                    help="workload 1..5 (default 3: 8B shapes, ctx 32K, "
+                         "gamma 16, 16 catch-up tokens)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the step as one captured HIP graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-layers", type=int, default=None)
+    ap.add_argument("--copy-probe-mib", type=int, default=1024,
+                    help="size of the plain device copy run after timing "
+                         "(reference for HBM traffic counters); 0 = off")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class Step:
+    """Pre-marshalled C-ABI calls of one verification step."""
+
+    def __init__(self, w, layers, head, outs, lmouts, draft, tau, ws_attn,
+                 ws_lm, wf):
+        self.w, self.layers, self.head = w, layers, head
+        self.outs, self.lmouts, self.draft, self.tau = outs, lmouts, draft, tau
+        self.ws_attn, self.ws_lm, self.wf = ws_attn, ws_lm, wf
+
+    def build(self, stream_ptr):
+        w, wf = self.w, self.wf
+        P = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
+        code = wf.WF_BF16 if w.dtype == "bf16" else wf.WF_F32
+        s = ctypes.c_void_p(stream_ptr)
+        self.attn = []
+        self.pre = []
+        for l, t in enumerate(self.layers):
+            self.attn.append((code, P(t["q"]), P(t["k_cache"]), P(t["v_cache"]),
+                              P(self.outs[l]), w.gamma, w.ctx_len, w.cap,
+                              w.n_q_heads, w.n_kv_heads, w.head_dim,
+                              w.softmax_scale, 0, P(self.ws_attn),
+                              self.ws_attn.numel(), s))
+            if w.n_prefill:
+                kc = t["drafter_k_cache"] if w.separate_drafter_cache else t["k_cache"]
+                vc = t["drafter_v_cache"] if w.separate_drafter_cache else t["v_cache"]
+                self.pre.append((code, P(t["x"]), P(t["w_k"]), P(t["w_v"]), P(kc),
+                                 P(vc), w.n_prefill, w.prefill_start,
+                                 kc.shape[1], w.hidden, w.n_kv_heads,
+                                 w.head_dim, w.rope_base, s))
+        am, ent, acc = self.lmouts[0]
+        self.lm = [(code, P(self.head["h"]), P(self.head["w_lm"]), None,
+                    P(self.draft), w.gamma, w.hidden, w.vocab, self.tau, P(am),
+                    P(ent), P(acc), P(self.ws_lm), self.ws_lm.numel(), s)]
+        if w.router_logits:
+            am2, ent2, acc2 = self.lmouts[1]
+            self.lm.append((code, None, None, P(self.head["router_logits"]),
+                            P(self.draft), w.gamma, 0, w.vocab, self.tau,
+                            P(am2), P(ent2), P(acc2), P(self.ws_lm),
+                            self.ws_lm.numel(), s))
+
+    def run(self, check=False, attn_events=None, phase_events=None):
+        lib = self.wf.lib
+        pe = phase_events
+        if pe:
+            pe[0].record()
+        for l, a in enumerate(self.attn):
+            if attn_events:
+                attn_events[l][0].record()
+            rc = lib.wf_verify_attn(*a)
+            if attn_events:
+                attn_events[l][1].record()
+            if check and rc:
+                raise RuntimeError(f"wf_verify_attn: {self.wf.status_string(rc)}")
+        if pe:
+            pe[1].record()
+        for a in self.pre:
+            rc = lib.wf_kv_only_prefill(*a)
+            if check and rc:
+                raise RuntimeError(f"wf_kv_only_prefill: {self.wf.status_string(rc)}")
+        if pe:
+            pe[2].record()
+        for a in self.lm:
+            rc = lib.wf_lmhead_accept_entropy(*a)
+            if check and rc:
+                raise RuntimeError(f"wf_lmhead_accept_entropy: {self.wf.status_string(rc)}")
+        if pe:
+            pe[3].record()
+
+
+def cpu_baseline(w, layers, head, sample_layers):
+    """The oracle as it stands, on host cores, over a bounded sample of the
+    step: `sample_layers` layers of attention and prefill plus the LM head;
+    scaled to one full step."""
+    import oracle
+    import workloads as W
+    n = w.ctx_len + w.gamma
+    t_attn = t_pre = 0.0
+    for l in range(sample_layers):
+        t = layers[l]
+        q = W.to_oracle(t["q"])
+        k = W.to_oracle(t["k_cache"][:, :n].contiguous())
+        v = W.to_oracle(t["v_cache"][:, :n].contiguous())
+        t0 = time.perf_counter()
+        oracle.verify_attn(q, k, v, w.ctx_len)
+        t_attn += time.perf_counter() - t0
+        if w.n_prefill:
+            x, wk, wv = (W.to_oracle(t[k_]) for k_ in ("x", "w_k", "w_v"))
+            t0 = time.perf_counter()
+            oracle.kv_only_prefill(x, wk, wv, w.prefill_start, w.n_kv_heads,
+                                   w.head_dim, w.rope_base)
+            t_pre += time.perf_counter() - t0
+        log(f"cpu baseline: layer {l} done")
+    h, wl = W.to_oracle(head["h"]), W.to_oracle(head["w_lm"])
+    t0 = time.perf_counter()
+    oracle.lmhead_rows(h, wl)
+    t_lm = time.perf_counter() - t0
+    if w.router_logits:
+        z = head["router_logits"].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.lmhead_rows(logits=z)
+        t_lm += time.perf_counter() - t0
+    per_step_s = (t_attn + t_pre) / sample_layers * w.n_layers + t_lm
+    return {
+        "value": round(per_step_s * 1e6, 1),
+        "unit": "us",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": (f"{sample_layers} of {w.n_layers} layers (attention, all "
+                   f"{w.gamma * w.n_q_heads} rows x heads"
+                   + (", KV-only prefill" if w.n_prefill else "")
+                   + ") + full LM head; scaled to one step"),
+        "measured_s": round(t_attn + t_pre + t_lm, 2),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the verification step is built "
+              "and timed on a single MI355X (no multi-GPU path exists); run "
+              "with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_07710_amd as wf
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    w = W.CONFIGS[args.config]
+    log(f"workload {w.name}: {w.description}")
+
+    t0 = time.perf_counter()
+    layers = [W.generate_layer(w, l, device=dev) for l in range(w.n_layers)]
+    head = W.generate_head(w, device=dev)
+    torch.cuda.synchronize()
+    log(f"inputs generated in {time.perf_counter() - t0:.1f}s")
+
+    outs = [torch.empty_like(t["q"]) for t in layers]
+    ws_attn = wf.alloc_workspace(
+        wf.wf_verify_attn_workspace_bytes(1 if w.dtype == "bf16" else 0,
+                                          w.gamma, w.ctx_len, w.n_q_heads,
+                                          w.n_kv_heads, w.head_dim), dev)
+    ws_lm = wf.alloc_workspace(wf.wf_lmhead_workspace_bytes(w.gamma, w.vocab), dev)
+    lmouts = [(torch.empty(w.gamma, dtype=torch.int32, device=dev),
+               torch.empty(w.gamma, dtype=torch.float32, device=dev),
+               torch.empty(3, dtype=torch.int32, device=dev)) for _ in range(2)]
+
+    # drafts: the workload's accept prefix, built from this GPU's own argmax
+    # (the timed work does not depend on draft content)
+    am, ent, acc = lmouts[0]
+    wf.wf_lmhead_accept_entropy(head["h"], head["w_lm"], None,
+                                torch.zeros(max(w.gamma - 1, 1), dtype=torch.int32,
+                                            device=dev),
+                                0.0, am, ent, acc, workspace=ws_lm)
+    torch.cuda.synchronize()
+    k = W.prefix_len(w, 0)
+    draft = torch.as_tensor(W.make_drafts(am.cpu().numpy(), k, w.vocab, 1),
+                            device=dev)
+    tau = float(np.median(ent.cpu().numpy()))
+
+    step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_lm, wf)
+    stream = torch.cuda.current_stream()
+    step.build(stream.cuda_stream)
+    step.run(check=True)
+    torch.cuda.synchronize()
+    log(f"step ok: accept {tuple(acc.tolist())} (expected n = {k})")
+
+    graph = None
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        with torch.cuda.stream(side):
+            step.build(side.cuda_stream)
+            step.run(check=True)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            step.build(torch.cuda.current_stream().cuda_stream)
+            step.run(check=True)
+        step.build(stream.cuda_stream)
+        torch.cuda.synchronize()
+
+    def one_step():
+        if graph is not None:
+            graph.replay()
+        else:
+            step.run()
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    # ---- timed region 1: the step ------------------------------------------
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        one_step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step "
+        f"(host wall {wall / args.steps * 1e6:.1f} us/step)")
+
+    # ---- timed region 2: per-call events on the dominant kernel ------------
+    n_l = w.n_layers
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    attn_ev = [[[ev(), ev()] for _ in range(n_l)] for _ in range(args.steps)]
+    phase_ev = [[ev() for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for s in range(args.steps):
+        step.run(attn_events=attn_ev[s], phase_events=phase_ev[s])
+    torch.cuda.synchronize()
+    attn_ms = [a.elapsed_time(b) for evs in attn_ev for a, b in evs]
+    phases = np.array([[p[0].elapsed_time(p[1]), p[1].elapsed_time(p[2]),
+                        p[2].elapsed_time(p[3])] for p in phase_ev])
+    attn_avg_ms = float(np.mean(attn_ms))
+    log(f"attention call avg {attn_avg_ms * 1e3:.2f} us, phases (us) "
+        f"attn {phases[:, 0].mean() * 1e3:.1f} prefill "
+        f"{phases[:, 1].mean() * 1e3:.1f} lmhead {phases[:, 2].mean() * 1e3:.1f}")
+
+    by = w.algorithmic_bytes()
+    achieved = by["attn_per_layer"] / (attn_avg_ms * 1e-3) / 1e9
+    step_gbps = by["total"] / (ms_per_step * 1e-3) / 1e9
+
+    # ---- plain copy for the HBM traffic counters (not timed) ---------------
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        sample = args.cpu_sample_layers or (w.n_layers if w.n_layers <= 2 else 4)
+        log(f"cpu baseline on {sample} layers ...")
+        cpu = cpu_baseline(w, layers, head, sample)
+
+    line = {
+        "metric": "verify-step us and achieved HBM GB/s (gamma=16, 32K ctx, "
+                  "8B shapes, 1 GPU)" if w.cfg == 3 else
+                  f"verify-step us and achieved HBM GB/s ({w.name}, 1 GPU)",
+        "value": round(ms_per_step * 1e3, 2),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded; shapes of the paper's Qwen3-8B-class "
+                "targets, random inputs)",
+        "config": {"workload": w.name, "layers": w.n_layers,
+                   "hidden": w.hidden, "q_heads": w.n_q_heads,
+                   "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "ctx_len": w.ctx_len, "gamma": w.gamma,
+                   "catch_up_tokens": w.n_prefill, "vocab": w.vocab,
+                   "graph": bool(graph is not None)},
+        "step_hbm_gbps": round(step_gbps, 1),
+        "step_algorithmic_bytes": by["total"],
+        "breakdown_us": {"attention": round(float(phases[:, 0].mean()) * 1e3, 1),
+                         "prefill": round(float(phases[:, 1].mean()) * 1e3, 1),
+                         "lmhead": round(float(phases[:, 2].mean()) * 1e3, 1)},
+        "roofline": {
+            "kernel": "wf_verify_attn (one layer: split partial + merge)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4),
+            "traffic": None,
+            "bytes_per_launch": by["attn_per_layer"],
+            "avg_launch_us": round(attn_avg_ms * 1e3, 2),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

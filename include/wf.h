@@ -1,0 +1,184 @@
+/*
+ * wf.h -- C ABI of libwf, the MI355X (gfx950) verification-step library for
+ * WhiFlash cross-paradigm speculative decoding (arXiv 2606.07710).
+ *
+ * One speculation round of the paper (Sec. 3.2) drafts a block of tokens,
+ * hands it to the target model for parallel verification, accepts the
+ * longest prefix the target agrees with, and routes the next round by the
+ * entropy of the target's next-token distribution at the final accepted
+ * position (Sec. 3.3.1).  A drafter switch first catches the incoming
+ * drafter's KV cache up on the backlog tokens with a KV-only prefill
+ * (Sec. 3.4).  This library implements the three data-parallel pieces of
+ * that step on one GPU:
+ *
+ *   wf_verify_attn            block-causal grouped-query attention of the
+ *                             gamma verify rows against the KV cache
+ *   wf_kv_only_prefill        K/V projection + RoPE + cache append for
+ *                             catch-up tokens
+ *   wf_lmhead_accept_entropy  LM head reduced to argmax and entropy per row,
+ *                             then greedy acceptance and the entropy route
+ *
+ * Conventions shared by every call
+ *   - Every tensor pointer is DEVICE memory owned by the caller, 16-byte
+ *     aligned, densely packed in the layout stated.  The library never
+ *     allocates, frees or synchronises, and keeps no global state.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream).  Outputs are valid once the stream reaches that point.
+ *   - Arguments are validated on the host before anything is launched; on a
+ *     non-OK status nothing was enqueued.  A failed kernel launch returns
+ *     WF_ERR_HIP.
+ *   - Workspaces are caller-owned scratch of at least the size the matching
+ *     *_workspace_bytes query returns.  Contents need no initialisation and
+ *     are clobbered.  Two calls that overlap in time must not share one.
+ *   - Reductions use a fixed order, so repeated calls on the same inputs and
+ *     the same split count return bit-identical results.
+ *   - Row-major throughout; "[a][b][c]" lists dimensions slowest first.
+ */
+#ifndef WF_H
+#define WF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    WF_OK = 0,
+    WF_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad size or range  */
+    WF_ERR_UNSUPPORTED = 2,   /* valid but not implemented (e.g. head_dim)    */
+    WF_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required   */
+    WF_ERR_HIP = 4            /* the HIP runtime rejected a kernel launch     */
+} wf_status_t;
+
+typedef enum {
+    WF_F32 = 0,               /* IEEE fp32 storage and arithmetic             */
+    WF_BF16 = 1               /* bf16 storage, fp32 accumulation              */
+} wf_dtype_t;
+
+/* Version of this ABI (bumped on any signature or semantic change). */
+int32_t wf_abi_version(void);
+
+/* Static description of a status code; never NULL. */
+const char *wf_status_string(wf_status_t s);
+
+/* ------------------------------------------------------------------------
+ * wf_verify_attn -- target attention over the verify block (Sec. 3.2: the
+ * candidate tokens return to the target for one parallel verification
+ * pass; the round then continues from the last accepted token).
+ *
+ * Block row i (0 <= i < gamma) sits at position ctx_len + i.  Row 0 is the
+ * last committed token, rows 1..gamma-1 are the drafts, whether they came
+ * from an autoregressive chain or a diffusion block.  Verification is causal
+ * inside the block: row i attends to the ctx_len cached keys and to block
+ * keys ctx_len .. ctx_len+i, so row i equals a single-token decode on prefix
+ * ctx_len+i and gamma == 1 is ordinary decoding.  Query head h reads KV head
+ * h / (n_q_heads / n_kv_heads) (consecutive query heads share a KV head).
+ *
+ *   out[i][h][:] = sum_j softmax_j(softmax_scale * <q[i][h], K[g][j]>) V[g][j]
+ *
+ * q        [gamma][n_q_heads][head_dim], RoPE already applied.
+ * k_cache  [n_kv_heads][cap][head_dim], post-RoPE keys.  Rows
+ *          [0, ctx_len+gamma) must be valid: the caller appends the block's
+ *          own K/V at rows ctx_len.. before the call.  Rows beyond are never
+ *          read.
+ * v_cache  [n_kv_heads][cap][head_dim].
+ * out      [gamma][n_q_heads][head_dim], dtype dt (bf16 rounded to nearest
+ *          even once from fp32).
+ * Limits:  1 <= gamma <= 64; ctx_len >= 0; ctx_len + gamma <= cap;
+ *          n_q_heads % n_kv_heads == 0; n_q_heads <= 256;
+ *          head_dim in {64, 128} (else WF_ERR_UNSUPPORTED).
+ * num_splits  0 selects the split of the key range automatically; a
+ *          positive value forces that many key splits per KV head (results
+ *          agree to fp32 rounding for any split count).  At most 1024.
+ * workspace  >= wf_verify_attn_workspace_bytes(...) bytes with the same
+ *          num_splits.
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
+                           const void *v_cache, void *out, int32_t gamma,
+                           int32_t ctx_len, int32_t cap, int32_t n_q_heads,
+                           int32_t n_kv_heads, int32_t head_dim,
+                           float softmax_scale, int32_t num_splits,
+                           void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/* Workspace for wf_verify_attn (0 for invalid arguments). */
+size_t wf_verify_attn_workspace_bytes(wf_dtype_t dt, int32_t gamma,
+                                      int32_t ctx_len, int32_t n_q_heads,
+                                      int32_t n_kv_heads, int32_t head_dim,
+                                      int32_t num_splits);
+
+/* ------------------------------------------------------------------------
+ * wf_kv_only_prefill -- lazy catch-up of a drafter's KV cache (Sec. 3.4).
+ * On a drafter switch, the tokens accepted while that drafter was inactive
+ * (the backlog) are prefilled in one batch, and for them only the attention
+ * layer's K/V are formed: no MLP, no LM head.  Token t is at position
+ * start_pos + t:
+ *
+ *   K[g][start_pos+t][:] = RoPE(W_k[g*D:(g+1)*D][:] x[t], start_pos + t)
+ *   V[g][start_pos+t][:] =      W_v[g*D:(g+1)*D][:] x[t]
+ *
+ * RoPE is the rotate-half form: for i < D/2, theta_i = rope_base^(-2i/D)
+ * and the pair (k_i, k_{i+D/2}) turns by (start_pos+t)*theta_i radians
+ * (angles formed in fp64).
+ *
+ * x         [n_tok][d_in], the layer input after RMSNorm.
+ * w_k, w_v  [n_kv_heads*head_dim][d_in] each (output feature major).
+ * k_cache, v_cache  [n_kv_heads][cap][head_dim]; only rows
+ *           [start_pos, start_pos+n_tok) are written (dtype dt).
+ * Limits:   0 <= n_tok <= 4096 (0 is a no-op); start_pos >= 0;
+ *           start_pos + n_tok <= cap; head_dim in {64, 128};
+ *           d_in >= 1, and d_in % 32 == 0 for WF_BF16.
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
+                               const void *w_v, void *k_cache, void *v_cache,
+                               int32_t n_tok, int32_t start_pos, int32_t cap,
+                               int32_t d_in, int32_t n_kv_heads,
+                               int32_t head_dim, double rope_base,
+                               void *stream);
+
+/* ------------------------------------------------------------------------
+ * wf_lmhead_accept_entropy -- LM head, greedy acceptance and entropy route.
+ *
+ * For every verify row i the target's next-token logits z_i = W h_i are
+ * reduced on the fly (never written out) to
+ *   argmax_out[i]  = lowest index attaining max_v z_i[v]
+ *   entropy_out[i] = -sum_v p_i(v) log p_i(v), p_i = softmax(z_i), in nats
+ * (Sec. 3.3.1: an O(|V|) reduction over the next-token distribution).
+ * Then greedy verification accepts the longest prefix of drafts the target
+ * agrees with, and the entropy at the final accepted position picks the
+ * next drafter (Sec. 3.3.1 rule: autoregressive iff H_t > tau):
+ *   n     = number of j in 0.. with draft[j] == argmax[j] for all earlier j,
+ *           at most gamma-1
+ *   accept_out = { n, bonus token argmax[n], route (1 = AR, 0 = diffusion)
+ *                  = entropy[n] > tau_entropy }
+ *
+ * h         [gamma][d] final-norm hidden states of the verify rows.
+ * w_lm      [vocab][d] LM-head weight (one row per vocabulary entry).
+ * logits    logits-only mode: [gamma][vocab] fp32 given directly, with
+ *           h == w_lm == NULL; dt and d are then ignored.  Otherwise NULL.
+ * draft     [gamma-1] int32: draft[j] is the token at block row j+1, checked
+ *           against the argmax of row j.  May be NULL only when gamma == 1.
+ * argmax_out [gamma] int32, entropy_out [gamma] fp32, accept_out [3] int32.
+ * Limits:   1 <= gamma <= 64; 1 <= vocab <= 2^30; d >= 1, and
+ *           d % 32 == 0 for WF_BF16.
+ * workspace >= wf_lmhead_workspace_bytes(gamma, vocab) bytes.
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_lmhead_accept_entropy(wf_dtype_t dt, const void *h,
+                                     const void *w_lm, const float *logits,
+                                     const int32_t *draft, int32_t gamma,
+                                     int32_t d, int32_t vocab,
+                                     float tau_entropy, int32_t *argmax_out,
+                                     float *entropy_out, int32_t *accept_out,
+                                     void *workspace, size_t workspace_bytes,
+                                     void *stream);
+
+/* Workspace for wf_lmhead_accept_entropy (0 for invalid arguments). */
+size_t wf_lmhead_workspace_bytes(int32_t gamma, int32_t vocab);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WF_H */

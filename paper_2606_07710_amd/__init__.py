@@ -1,0 +1,182 @@
+"""Python binding of libwf, the MI355X verification-step library for WhiFlash
+cross-paradigm speculative decoding (arXiv 2606.07710).
+
+Argument marshalling only: every function passes torch tensors' device
+pointers and the current HIP stream to the C ABI declared in include/wf.h,
+and raises WfError on a non-OK status.  All computation runs in the HIP
+kernels of libwf.so; there is no fallback path.  If the library has not been
+built, importing this package raises ImportError.
+"""
+import ctypes
+import os
+
+import torch  # loaded first so libwf binds to the same HIP runtime as torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libwf.so")
+
+WF_OK, WF_ERR_INVALID_ARG, WF_ERR_UNSUPPORTED, WF_ERR_WORKSPACE, WF_ERR_HIP = range(5)
+WF_F32, WF_BF16 = 0, 1
+
+EXPORTED_SYMBOLS = (
+    "wf_abi_version", "wf_status_string", "wf_verify_attn",
+    "wf_verify_attn_workspace_bytes", "wf_kv_only_prefill",
+    "wf_lmhead_accept_entropy", "wf_lmhead_workspace_bytes",
+)
+
+
+class WfError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with "
+            "`python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(LIB_PATH)
+    p, i32, sz, f32, f64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t,
+                            ctypes.c_float, ctypes.c_double)
+    lib.wf_abi_version.restype = i32
+    lib.wf_status_string.argtypes = [i32]
+    lib.wf_status_string.restype = ctypes.c_char_p
+    lib.wf_verify_attn.argtypes = [i32, p, p, p, p, i32, i32, i32, i32, i32,
+                                   i32, f32, i32, p, sz, p]
+    lib.wf_verify_attn.restype = i32
+    lib.wf_verify_attn_workspace_bytes.argtypes = [i32, i32, i32, i32, i32,
+                                                   i32, i32]
+    lib.wf_verify_attn_workspace_bytes.restype = sz
+    lib.wf_kv_only_prefill.argtypes = [i32, p, p, p, p, p, i32, i32, i32, i32,
+                                       i32, i32, f64, p]
+    lib.wf_kv_only_prefill.restype = i32
+    lib.wf_lmhead_accept_entropy.argtypes = [i32, p, p, p, p, i32, i32, i32,
+                                             f32, p, p, p, p, sz, p]
+    lib.wf_lmhead_accept_entropy.restype = i32
+    lib.wf_lmhead_workspace_bytes.argtypes = [i32, i32]
+    lib.wf_lmhead_workspace_bytes.restype = sz
+    return lib
+
+
+lib = _load()
+
+
+def status_string(status: int) -> str:
+    return lib.wf_status_string(int(status)).decode()
+
+
+def abi_version() -> int:
+    return int(lib.wf_abi_version())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return WF_F32
+    if t.dtype == torch.bfloat16:
+        return WF_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _dev(t, name):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(status, what):
+    if status != WF_OK:
+        raise WfError(status, what)
+
+
+def wf_verify_attn_workspace_bytes(dtype, gamma, ctx_len, n_q_heads,
+                                   n_kv_heads, head_dim, num_splits=0) -> int:
+    code = dtype if isinstance(dtype, int) else (
+        WF_F32 if dtype == torch.float32 else WF_BF16)
+    return int(lib.wf_verify_attn_workspace_bytes(
+        code, gamma, ctx_len, n_q_heads, n_kv_heads, head_dim, num_splits))
+
+
+def wf_lmhead_workspace_bytes(gamma, vocab) -> int:
+    return int(lib.wf_lmhead_workspace_bytes(gamma, vocab))
+
+
+def alloc_workspace(nbytes: int, device) -> torch.Tensor:
+    """Caller-owned scratch for the workspace arguments (16-byte aligned)."""
+    return torch.empty(max(16, (nbytes + 15) // 16 * 16), dtype=torch.uint8,
+                       device=device)
+
+
+def wf_verify_attn(q, k_cache, v_cache, out, ctx_len, softmax_scale=None,
+                   num_splits=0, workspace=None, stream=None):
+    """q [gamma][Hq][D]; k_cache, v_cache [Hkv][cap][D]; out like q."""
+    gamma, hq, dh = q.shape
+    hkv, cap, dh2 = k_cache.shape
+    if dh2 != dh or tuple(v_cache.shape) != tuple(k_cache.shape):
+        raise ValueError("cache shapes do not match q")
+    if tuple(out.shape) != tuple(q.shape) or out.dtype != q.dtype:
+        raise ValueError("out must match q in shape and dtype")
+    code = _dtype_code(q)
+    if softmax_scale is None:
+        softmax_scale = dh ** -0.5
+    need = wf_verify_attn_workspace_bytes(code, gamma, ctx_len, hq, hkv, dh,
+                                          num_splits)
+    if workspace is None:
+        workspace = alloc_workspace(need, q.device)
+    st = lib.wf_verify_attn(code, _dev(q, "q"), _dev(k_cache, "k_cache"),
+                            _dev(v_cache, "v_cache"), _dev(out, "out"), gamma,
+                            int(ctx_len), cap, hq, hkv, dh,
+                            float(softmax_scale), int(num_splits),
+                            _dev(workspace, "workspace"), workspace.numel(),
+                            _stream(stream))
+    _check(st, "wf_verify_attn")
+    return out
+
+
+def wf_kv_only_prefill(x, w_k, w_v, k_cache, v_cache, start_pos, rope_base,
+                       stream=None):
+    """x [n][d_in]; w_k, w_v [Hkv*D][d_in]; caches [Hkv][cap][D]."""
+    n_tok, d_in = x.shape
+    hkv, cap, dh = k_cache.shape
+    code = _dtype_code(x)
+    st = lib.wf_kv_only_prefill(code, _dev(x, "x"), _dev(w_k, "w_k"),
+                                _dev(w_v, "w_v"), _dev(k_cache, "k_cache"),
+                                _dev(v_cache, "v_cache"), n_tok,
+                                int(start_pos), cap, d_in, hkv, dh,
+                                float(rope_base), _stream(stream))
+    _check(st, "wf_kv_only_prefill")
+
+
+def wf_lmhead_accept_entropy(h, w_lm, logits, draft, tau, argmax_out,
+                             entropy_out, accept_out, workspace=None,
+                             stream=None, gamma=None, vocab=None):
+    """Either (h [gamma][d], w_lm [vocab][d]) or logits [gamma][vocab] fp32.
+    draft [gamma-1] int32 (None when gamma == 1); outputs int32 [gamma],
+    fp32 [gamma], int32 [3]."""
+    if logits is not None:
+        gamma, vocab = logits.shape
+        d, code = 0, WF_F32
+    else:
+        gamma, d = h.shape
+        vocab = w_lm.shape[0]
+        code = _dtype_code(h)
+    need = wf_lmhead_workspace_bytes(gamma, vocab)
+    dev = (logits if logits is not None else h).device
+    if workspace is None:
+        workspace = alloc_workspace(need, dev)
+    st = lib.wf_lmhead_accept_entropy(
+        code, _dev(h, "h"), _dev(w_lm, "w_lm"), _dev(logits, "logits"),
+        _dev(draft, "draft"), gamma, d, vocab, float(tau),
+        _dev(argmax_out, "argmax_out"), _dev(entropy_out, "entropy_out"),
+        _dev(accept_out, "accept_out"), _dev(workspace, "workspace"),
+        workspace.numel(), _stream(stream))
+    _check(st, "wf_lmhead_accept_entropy")

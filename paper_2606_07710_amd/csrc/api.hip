@@ -1,0 +1,170 @@
+// api.hip -- the extern "C" boundary of libwf: argument validation on the
+// host, workspace queries and dispatch to the kernel launchers.  Nothing is
+// enqueued unless every check passes.  The library holds no global state.
+#include <cmath>
+
+#include "wf_api_internal.h"
+
+namespace {
+
+constexpr int kMaxGamma = 64;
+constexpr int kMaxQHeads = 256;
+constexpr int kMaxSplits = 1024;
+constexpr int kMaxPrefillTokens = 4096;
+
+inline bool aligned16(const void *p) {
+    return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+
+inline bool dtype_ok(wf_dtype_t dt) { return dt == WF_F32 || dt == WF_BF16; }
+
+inline bool head_dim_ok(int dh) { return dh == 64 || dh == 128; }
+
+wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
+                       int n_kv_heads, int head_dim, int num_splits) {
+    if (!dtype_ok(dt))
+        return WF_ERR_INVALID_ARG;
+    if (gamma < 1 || gamma > kMaxGamma || ctx_len < 0)
+        return WF_ERR_INVALID_ARG;
+    if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads > kMaxQHeads ||
+        n_q_heads % n_kv_heads != 0)
+        return WF_ERR_INVALID_ARG;
+    if (num_splits < 0 || num_splits > kMaxSplits)
+        return WF_ERR_INVALID_ARG;
+    if ((long long)ctx_len + gamma > (long long)INT32_MAX / 2)
+        return WF_ERR_INVALID_ARG;
+    if (!head_dim_ok(head_dim))
+        return WF_ERR_UNSUPPORTED;
+    return WF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t wf_abi_version(void) { return 1; }
+
+const char *wf_status_string(wf_status_t s) {
+    switch (s) {
+    case WF_OK: return "ok";
+    case WF_ERR_INVALID_ARG: return "invalid argument";
+    case WF_ERR_UNSUPPORTED: return "unsupported configuration";
+    case WF_ERR_WORKSPACE: return "workspace missing or too small";
+    case WF_ERR_HIP: return "HIP kernel launch failed";
+    }
+    return "unknown status";
+}
+
+size_t wf_verify_attn_workspace_bytes(wf_dtype_t dt, int32_t gamma,
+                                      int32_t ctx_len, int32_t n_q_heads,
+                                      int32_t n_kv_heads, int32_t head_dim,
+                                      int32_t num_splits) {
+    if (check_attn(dt, gamma, ctx_len, n_q_heads, n_kv_heads, head_dim,
+                   num_splits) != WF_OK)
+        return 0;
+    const wf::AttnPlan p = wf::plan_attn(dt, gamma, ctx_len, n_q_heads,
+                                         n_kv_heads, head_dim, num_splits);
+    return wf::attn_workspace_bytes(p, gamma, n_q_heads, head_dim);
+}
+
+wf_status_t wf_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
+                           const void *v_cache, void *out, int32_t gamma,
+                           int32_t ctx_len, int32_t cap, int32_t n_q_heads,
+                           int32_t n_kv_heads, int32_t head_dim,
+                           float softmax_scale, int32_t num_splits,
+                           void *workspace, size_t workspace_bytes,
+                           void *stream) {
+    wf_status_t st = check_attn(dt, gamma, ctx_len, n_q_heads, n_kv_heads,
+                                head_dim, num_splits);
+    if (st != WF_OK)
+        return st;
+    if (!q || !k_cache || !v_cache || !out)
+        return WF_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) ||
+        !aligned16(out))
+        return WF_ERR_INVALID_ARG;
+    if ((long long)ctx_len + gamma > cap)
+        return WF_ERR_INVALID_ARG;
+    if (!std::isfinite(softmax_scale) || softmax_scale <= 0.f)
+        return WF_ERR_INVALID_ARG;
+    const wf::AttnPlan p = wf::plan_attn(dt, gamma, ctx_len, n_q_heads,
+                                         n_kv_heads, head_dim, num_splits);
+    const size_t need = wf::attn_workspace_bytes(p, gamma, n_q_heads, head_dim);
+    if (!workspace || workspace_bytes < need || !aligned16(workspace))
+        return WF_ERR_WORKSPACE;
+    return wf::launch_attn(dt, q, k_cache, v_cache, out, gamma, ctx_len, cap,
+                           n_q_heads, n_kv_heads, head_dim, softmax_scale, p,
+                           workspace, static_cast<hipStream_t>(stream));
+}
+
+wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
+                               const void *w_v, void *k_cache, void *v_cache,
+                               int32_t n_tok, int32_t start_pos, int32_t cap,
+                               int32_t d_in, int32_t n_kv_heads,
+                               int32_t head_dim, double rope_base,
+                               void *stream) {
+    if (!dtype_ok(dt))
+        return WF_ERR_INVALID_ARG;
+    if (n_tok < 0 || n_tok > kMaxPrefillTokens || start_pos < 0 ||
+        (long long)start_pos + n_tok > cap || d_in < 1 || n_kv_heads < 1)
+        return WF_ERR_INVALID_ARG;
+    if (!std::isfinite(rope_base) || rope_base <= 0.0)
+        return WF_ERR_INVALID_ARG;
+    if (!head_dim_ok(head_dim))
+        return WF_ERR_UNSUPPORTED;
+    if (dt == WF_BF16 && d_in % 32 != 0)
+        return WF_ERR_UNSUPPORTED;
+    if (n_tok == 0)
+        return WF_OK;
+    if (!x || !w_k || !w_v || !k_cache || !v_cache)
+        return WF_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(w_k) || !aligned16(w_v) ||
+        !aligned16(k_cache) || !aligned16(v_cache))
+        return WF_ERR_INVALID_ARG;
+    return wf::launch_prefill(dt, x, w_k, w_v, k_cache, v_cache, n_tok,
+                              start_pos, cap, d_in, n_kv_heads, head_dim,
+                              rope_base, static_cast<hipStream_t>(stream));
+}
+
+size_t wf_lmhead_workspace_bytes(int32_t gamma, int32_t vocab) {
+    if (gamma < 1 || gamma > kMaxGamma || vocab < 1 || vocab > (1 << 30))
+        return 0;
+    return wf::lmhead_workspace_bytes(gamma, vocab);
+}
+
+wf_status_t wf_lmhead_accept_entropy(wf_dtype_t dt, const void *h,
+                                     const void *w_lm, const float *logits,
+                                     const int32_t *draft, int32_t gamma,
+                                     int32_t d, int32_t vocab,
+                                     float tau_entropy, int32_t *argmax_out,
+                                     float *entropy_out, int32_t *accept_out,
+                                     void *workspace, size_t workspace_bytes,
+                                     void *stream) {
+    if (gamma < 1 || gamma > kMaxGamma || vocab < 1 || vocab > (1 << 30))
+        return WF_ERR_INVALID_ARG;
+    if (std::isnan(tau_entropy))
+        return WF_ERR_INVALID_ARG;
+    if (logits) {
+        if (h || w_lm || !aligned16(logits))
+            return WF_ERR_INVALID_ARG;
+    } else {
+        if (!dtype_ok(dt) || !h || !w_lm || d < 1)
+            return WF_ERR_INVALID_ARG;
+        if (!aligned16(h) || !aligned16(w_lm))
+            return WF_ERR_INVALID_ARG;
+        if (dt == WF_BF16 && d % 32 != 0)
+            return WF_ERR_UNSUPPORTED;
+    }
+    if (gamma > 1 && !draft)
+        return WF_ERR_INVALID_ARG;
+    if (!argmax_out || !entropy_out || !accept_out)
+        return WF_ERR_INVALID_ARG;
+    const size_t need = wf::lmhead_workspace_bytes(gamma, vocab);
+    if (!workspace || workspace_bytes < need || !aligned16(workspace))
+        return WF_ERR_WORKSPACE;
+    return wf::launch_lmhead(dt, h, w_lm, logits, draft, gamma, d, vocab,
+                             tau_entropy, argmax_out, entropy_out, accept_out,
+                             workspace, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,46 @@
+// wf_api_internal.h -- host-side plumbing between the C ABI (api.hip) and
+// the kernel launchers.  Internal header; not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/wf.h"
+
+namespace wf {
+
+struct AttnPlan {
+    int rows;            // G * gamma query rows per KV head
+    int nb;              // 16-row blocks per wave (bf16 path)
+    int n_row_groups;    // row groups of 16*nb rows
+    int splits;          // key splits per KV head
+    int keys_per_split;  // multiple of the 32-key tile
+};
+
+AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
+                   int n_kv_heads, int head_dim, int num_splits);
+size_t attn_workspace_bytes(const AttnPlan &p, int gamma, int n_q_heads,
+                            int head_dim);
+wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
+                        const void *v_cache, void *out, int gamma, int ctx_len,
+                        int cap, int n_q_heads, int n_kv_heads, int head_dim,
+                        float softmax_scale, const AttnPlan &p, void *workspace,
+                        hipStream_t stream);
+
+size_t lmhead_workspace_bytes(int gamma, int vocab);
+wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
+                          const float *logits, const int32_t *draft, int gamma,
+                          int d, int vocab, float tau, int32_t *argmax_out,
+                          float *entropy_out, int32_t *accept_out,
+                          void *workspace, hipStream_t stream);
+
+wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
+                           const void *w_v, void *k_cache, void *v_cache,
+                           int n_tok, int start_pos, int cap, int d_in,
+                           int n_kv_heads, int head_dim, double rope_base,
+                           hipStream_t stream);
+
+}  // namespace wf

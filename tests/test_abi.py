@@ -1,0 +1,122 @@
+"""CPU checks of the C ABI: the library loads, exports every function the
+header declares, and rejects invalid arguments on the host before anything
+would touch the GPU (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wf.h")
+
+wf = pytest.importorskip("paper_2606_07710_amd")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(wf_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_three_calls():
+    names = _declared_functions()
+    for n in ("wf_verify_attn", "wf_kv_only_prefill",
+              "wf_lmhead_accept_entropy"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(wf.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    assert set(_declared_functions()) == set(wf.EXPORTED_SYMBOLS)
+
+
+def test_status_strings_and_version():
+    assert wf.abi_version() == 1
+    assert wf.status_string(wf.WF_OK) == "ok"
+    assert "workspace" in wf.status_string(wf.WF_ERR_WORKSPACE)
+    assert wf.status_string(99) == "unknown status"
+
+
+FAKE = ctypes.c_void_p(1 << 20)      # 16-byte aligned, never dereferenced
+ODD = ctypes.c_void_p((1 << 20) + 8)
+
+
+def _attn(**kw):
+    a = dict(dt=1, q=FAKE, k=FAKE, v=FAKE, out=FAKE, gamma=16, ctx=100,
+             cap=116, hq=32, hkv=8, dh=128, scale=0.088, splits=0, ws=FAKE,
+             ws_bytes=1 << 30)
+    a.update(kw)
+    return wf.lib.wf_verify_attn(a["dt"], a["q"], a["k"], a["v"], a["out"],
+                                 a["gamma"], a["ctx"], a["cap"], a["hq"],
+                                 a["hkv"], a["dh"], a["scale"], a["splits"],
+                                 a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), 1), (dict(out=None), 1), (dict(gamma=0), 1),
+    (dict(gamma=65), 1), (dict(ctx=-1), 1), (dict(cap=115), 1),
+    (dict(hq=30), 1), (dict(dh=96), 2), (dict(dh=256), 2),
+    (dict(q=ODD), 1), (dict(scale=0.0), 1), (dict(scale=float("nan")), 1),
+    (dict(splits=-1), 1), (dict(splits=5000), 1), (dict(dt=7), 1),
+    (dict(ws=None), 3), (dict(ws_bytes=16), 3), (dict(ws=ODD), 3),
+])
+def test_verify_attn_rejects(kw, status):
+    assert _attn(**kw) == status
+
+
+def test_workspace_query():
+    need = wf.wf_verify_attn_workspace_bytes(1, 16, 32768, 32, 8, 128)
+    assert need > 0 and need % 4 == 0
+    assert wf.wf_verify_attn_workspace_bytes(1, 0, 32768, 32, 8, 128) == 0
+    forced = wf.wf_verify_attn_workspace_bytes(1, 16, 32768, 32, 8, 128, 7)
+    assert forced == 7 * 16 * 32 * 130 * 4
+    assert wf.wf_lmhead_workspace_bytes(16, 151936) == 16 * 2374 * 16
+    assert wf.wf_lmhead_workspace_bytes(0, 10) == 0
+
+
+def _prefill(**kw):
+    a = dict(dt=1, x=FAKE, wk=FAKE, wv=FAKE, kc=FAKE, vc=FAKE, n=16, start=10,
+             cap=26, d_in=4096, hkv=8, dh=128, base=1e6)
+    a.update(kw)
+    return wf.lib.wf_kv_only_prefill(a["dt"], a["x"], a["wk"], a["wv"],
+                                     a["kc"], a["vc"], a["n"], a["start"],
+                                     a["cap"], a["d_in"], a["hkv"], a["dh"],
+                                     a["base"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), 1), (dict(vc=None), 1), (dict(n=-1), 1),
+    (dict(cap=25), 1), (dict(start=-2), 1), (dict(dh=80), 2),
+    (dict(d_in=100), 2), (dict(base=0.0), 1), (dict(hkv=0), 1),
+    (dict(kc=ODD), 1), (dict(n=5000, cap=6000), 1),
+])
+def test_prefill_rejects(kw, status):
+    assert _prefill(**kw) == status
+
+
+def test_prefill_zero_tokens_is_a_noop():
+    assert _prefill(n=0) == 0
+
+
+def _lm(**kw):
+    a = dict(dt=1, h=FAKE, w=FAKE, logits=None, draft=FAKE, gamma=16,
+             d=4096, vocab=151936, tau=1.0, am=FAKE, ent=FAKE, acc=FAKE,
+             ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return wf.lib.wf_lmhead_accept_entropy(
+        a["dt"], a["h"], a["w"], a["logits"], a["draft"], a["gamma"], a["d"],
+        a["vocab"], a["tau"], a["am"], a["ent"], a["acc"], a["ws"],
+        a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(h=None), 1), (dict(gamma=0), 1), (dict(gamma=65), 1),
+    (dict(vocab=0), 1), (dict(draft=None), 1), (dict(d=100), 2),
+    (dict(logits=FAKE), 1), (dict(am=None), 1), (dict(tau=float("nan")), 1),
+    (dict(ws_bytes=100), 3), (dict(ws=None), 3), (dict(w=ODD), 1),
+])
+def test_lmhead_rejects(kw, status):
+    assert _lm(**kw) == status
