@@ -20,6 +20,8 @@
 //                   read from a per-wave LDS copy of the V tile, stored with
 //                   an XOR swizzle so the transposing reads hit 32 distinct
 //                   banks.
+#include <type_traits>
+
 #include "wf_api_internal.h"
 #include "wf_device.h"
 
@@ -28,7 +30,6 @@ namespace wf {
 namespace {
 
 constexpr int kTileKeys = 32;
-constexpr int kAttnWaves = 4;
 
 struct AttnParams {
     const uint16_t *q16;      // bf16 path
@@ -45,31 +46,77 @@ struct AttnParams {
 };
 
 // ---------------------------------------------------------------------------
-// bf16 split-KV partial kernel.  DH = head_dim, NB = 16-row blocks per row
-// group (rows handled per wave = 16*NB).
+// bf16 split-KV partial kernel.
+//
+// Workgroup = KS key streams x RG row groups of waves.  Stream s handles the
+// tiles s, s+KS, ... of the workgroup's key split; the RG waves of a stream
+// share each tile and own 16*NBW query rows apiece.  Tiles travel HBM -> LDS
+// with global_load_lds (no VGPR staging) into a two-deep ring per stream:
+// while a step computes on one ring half, the next step's tiles land in the
+// other.  All waves advance in lockstep, one barrier per step.
+//
+// LDS tile = K rows then V rows (row = head_dim bf16).  Both are swizzled so
+// the MFMA operand reads are bank-conflict free:
+//   K: 16-byte granule g of local key k sits at granule g ^ (k mod GRAN);
+//      operand reads are ds_read_b128 of (key 16*mb + m16, granule 4*kk + c4).
+//   V: 32-byte segment j of local key k sits at segment j ^ (k mod SEGS);
+//      the V^T operand is two ds_read_b64_tr_b16: source lane q of lane group
+//      c4 points at dims 16*md + 4*(q%4) of key 16*h + 4*c4 + q/4, and the
+//      transpose hands lane q the 4 keys of dim 16*md + q.
+// With the natural key order (M-block mb row m = key 16*mb + m) the S^T
+// accumulator of lane (m16, c4) holds keys 16*mb + 4*c4 + i of its row --
+// exactly the P^T operand the transposed V^T pairs with.
 // ---------------------------------------------------------------------------
-template <int DH, int NB>
-__global__ __launch_bounds__(256) void attn_partial_bf16(AttnParams a) {
-    constexpr int KC = DH / 32;          // 32-dim chunks of a key row
-    constexpr int MD = DH / 16;          // 16-dim output blocks
-    constexpr int GR = DH / 8;           // 16-byte granules per key row
-    constexpr int VLD = kTileKeys * GR / kWave;  // V loads per lane per tile
-    constexpr int ROWS = 16 * NB;
+template <int DH>
+struct TileGeom {
+    static constexpr int kRowBytes = DH * 2;
+    static constexpr int kHalfBytes = kTileKeys * kRowBytes;     // K or V part
+    static constexpr int kTileBytes = 2 * kHalfBytes;
+    static constexpr int kLoadsPerHalf = kHalfBytes / 1024;       // 1 KB per wave load
+    static constexpr int kGran = kRowBytes / 16;
+    static constexpr int kSegs = kRowBytes / 32;
+};
 
-    __shared__ __attribute__((aligned(16))) uint16_t vtile[kAttnWaves][kTileKeys * DH];
-    __shared__ __attribute__((aligned(16))) float osum[ROWS * DH];
-    __shared__ float mls[kAttnWaves][ROWS][2];
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+#define WF_LDS(T) __attribute__((address_space(3))) T
+
+template <int DH, int NBW, int RG, int KS>
+__global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) {
+    using TG = TileGeom<DH>;
+    constexpr int KC = DH / 32;
+    constexpr int MD = DH / 16;
+    constexpr int ROWS_W = 16 * NBW;
+    constexpr int ROWS_WG = ROWS_W * RG;
+    constexpr int NLOAD = 2 * TG::kLoadsPerHalf;      // wave loads per tile
+
+    // Stream-merge regions at the end reuse the ring: region 0 in ring0,
+    // region 1 (when KS > 2) in ring1.  Rows are padded by 4 floats so the
+    // 16 rows of a wave's accumulator tile fall in distinct banks.
+    constexpr int OST = DH + 4;
+    constexpr int NREG = KS / 2;
+    constexpr int RING_BYTES = KS * TG::kTileBytes;
+    constexpr int REGION_BYTES = ROWS_WG * OST * 4;
+    constexpr int RING0_BYTES = RING_BYTES > REGION_BYTES ? RING_BYTES : REGION_BYTES;
+    constexpr int RING1_BYTES = (NREG < 2 || RING_BYTES > REGION_BYTES) ? RING_BYTES : REGION_BYTES;
+    // two ring halves as separate objects, so reads of one never wait on the
+    // in-flight LDS-DMA writes into the other
+    __shared__ __attribute__((aligned(1024))) char ring0[RING0_BYTES];
+    __shared__ __attribute__((aligned(1024))) char ring1[RING1_BYTES];
+    __shared__ float mls[KS][ROWS_WG][2];
+    __shared__ int overflow;
+    if (threadIdx.x == 0)
+        overflow = 0;                        // published by the first barrier
 
     // ---- which (kv head, split, row group) this workgroup owns -------------
-    int unit, rg;
+    int unit, rgw;
     if (a.n_row_groups == 1) {
         unit = blockIdx.x;
-        rg = 0;
+        rgw = 0;
     } else {
         // keep the row groups of one (head, split) on one XCD, adjacent in
         // its dispatch order, so the second reader of a K/V tile hits L2
         const int xcd = blockIdx.x & 7, w = blockIdx.x >> 3;
-        rg = w % a.n_row_groups;
+        rgw = w % a.n_row_groups;
         unit = (w / a.n_row_groups) * 8 + xcd;
     }
     if (unit >= a.n_kv_heads * a.splits)
@@ -81,217 +128,291 @@ __global__ __launch_bounds__(256) void attn_partial_bf16(AttnParams a) {
     const int lane = threadIdx.x % kWave;
     const int m16 = lane & 15;
     const int c4 = lane >> 4;
+    const int stream = wave % KS;
+    const int rgi = wave / KS;
 
-    const int k_begin = split * a.keys_per_split;
-    const int k_end = min(a.n_keys, k_begin + a.keys_per_split);
-    const int n_tiles = (k_end > k_begin) ? (k_end - k_begin + kTileKeys - 1) / kTileKeys : 0;
-
-    // ---- Q^T operands and per-row causal limits ------------------------------
-    bf16x8 qf[NB][KC];
-    int lim[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const int r = rg * ROWS + nb * 16 + m16;
-        if (r < a.rows) {
-            const int i = r / a.group;
-            const int h = g * a.group + (r % a.group);
-            const uint16_t *qp = a.q16 + ((size_t)i * a.n_q_heads + h) * DH + c4 * 8;
-#pragma unroll
-            for (int kk = 0; kk < KC; ++kk)
-                qf[nb][kk] = load_bf16x8(qp + kk * 32);
-            lim[nb] = a.ctx_len + i;
-        } else {
-#pragma unroll
-            for (int kk = 0; kk < KC; ++kk)
-                qf[nb][kk] = zero_bf16x8();
-            lim[nb] = 0x7fffffff;        // padding row: no mask, never stored
-        }
-    }
-
-    f32x4 o[MD][NB];
-    float mrow[NB], lrow[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        mrow[nb] = -INFINITY;
-        lrow[nb] = 0.f;
-#pragma unroll
-        for (int md = 0; md < MD; ++md)
-            o[md][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    // splits own near-equal runs of whole tiles: [s*T/S, (s+1)*T/S)
+    const int tiles_total = (a.n_keys + kTileKeys - 1) / kTileKeys;
+    const int t_first = (int)((long long)split * tiles_total / a.splits);
+    const int t_last = (int)((long long)(split + 1) * tiles_total / a.splits);
+    const int k_begin = t_first * kTileKeys;
+    const int n_tiles = t_last - t_first;
+    const int n_steps = (n_tiles + KS - 1) / KS;
+    const int last_key = a.n_keys - 1;
+    const float sl2 = a.sl2;
 
     const size_t head_off = (size_t)g * a.cap * DH;
-    const uint16_t *kbase = a.k16 + head_off;
-    const uint16_t *vbase = a.v16 + head_off;
-    uint16_t *vt = vtile[wave];
-    const int last_key = a.n_keys - 1;
+    const char *kg = reinterpret_cast<const char *>(a.k16 + head_off);
+    const char *vg = reinterpret_cast<const char *>(a.v16 + head_off);
 
-    // Key of A-row m (16 rows) in M-block mb of a tile: tile base +
-    // 8*(m/4) + 4*mb + m%4, so S^T lane (m16, c4) ends up owning the 8
-    // consecutive keys 8*c4 .. 8*c4+7 of its row.
-    const int krow0 = 8 * (m16 >> 2) + (m16 & 3);
-
-    bf16x8 kn[2][KC], vn[VLD];
-    auto load_tile = [&](int t, bf16x8 (&kr)[2][KC], bf16x8 (&vr)[VLD]) {
+    // Issue this wave's share of the loads of tile t into one ring slot.
+    // Load j < kLoadsPerHalf fills K rows, the rest V rows; lane L of load j
+    // writes LDS bytes 16*(64*j' + L) of its half (j' = j mod kLoadsPerHalf).
+    auto issue = [&](char *ring, int t) {
         const int kb = k_begin + t * kTileKeys;
+        char *slot = ring + stream * TG::kTileBytes;
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            const int key = min(kb + krow0 + 4 * mb, last_key);
-            const uint16_t *p = kbase + (size_t)key * DH + c4 * 8;
-#pragma unroll
-            for (int kk = 0; kk < KC; ++kk)
-                kr[mb][kk] = load_bf16x8(p + kk * 32);
-        }
-#pragma unroll
-        for (int r = 0; r < VLD; ++r) {
-            const int chunk = r * kWave + lane;
-            const int key = kb + chunk / GR;
-            const int gi = chunk % GR;
-            bf16x8 val = load_bf16x8(vbase + (size_t)min(key, last_key) * DH + gi * 8);
-            vr[r] = (key <= last_key) ? val : zero_bf16x8();
+        for (int jr = 0; jr < NLOAD / RG; ++jr) {
+            const int j = rgi + jr * RG;
+            const bool is_v = j >= TG::kLoadsPerHalf;
+            const int jj = is_v ? j - TG::kLoadsPerHalf : j;
+            const int gidx = jj * kWave + lane;            // granule in the half
+            const int kl = gidx / TG::kGran;                // local key
+            const int pg = gidx % TG::kGran;                // physical granule
+            int lg;                                         // logical granule
+            if (!is_v) {
+                lg = pg ^ (kl & (TG::kGran - 1));
+            } else {
+                const int seg = (pg >> 1) ^ (kl & (TG::kSegs - 1));
+                lg = 2 * seg + (pg & 1);
+            }
+            const int key = min(kb + kl, last_key);
+            const char *src = (is_v ? vg : kg) + (size_t)key * TG::kRowBytes + lg * 16;
+            char *dst = slot + (is_v ? TG::kHalfBytes : 0) + jj * 1024;
+            __builtin_amdgcn_global_load_lds(
+                (__attribute__((address_space(1))) void *)src,
+                (WF_LDS(void) *)dst, 16, 0, 0);
         }
     };
 
-    int t = wave;
-    if (t < n_tiles)
-        load_tile(t, kn, vn);
-    for (; t < n_tiles; t += kAttnWaves) {
-        bf16x8 kc[2][KC], vc[VLD];
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int kk = 0; kk < KC; ++kk)
-                kc[mb][kk] = kn[mb][kk];
-#pragma unroll
-        for (int r = 0; r < VLD; ++r)
-            vc[r] = vn[r];
-        if (t + kAttnWaves < n_tiles)
-            load_tile(t + kAttnWaves, kn, vn);
+    // the first tiles start streaming before anything else
+    if (stream < n_tiles)
+        issue(ring0, stream);
 
-        // S^T = K Q^T
-        f32x4 s[2][NB];
+    // ---- Q^T operands and causal limits of this wave's rows ------------------
+    const int row0 = rgw * ROWS_WG + rgi * ROWS_W;
+    bf16x8 qf[NBW][KC];
+    int lim[NBW];
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
+    for (int nb = 0; nb < NBW; ++nb) {
+        const int r = row0 + nb * 16 + m16;
+        const int rc = min(r, a.rows - 1);
+        const int i = rc / a.group;
+        const int h = g * a.group + (rc % a.group);
+        const uint16_t *qp = a.q16 + ((size_t)i * a.n_q_heads + h) * DH + c4 * 8;
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int kk = 0; kk < KC; ++kk)
+            qf[nb][kk] = load_bf16x8(qp + kk * 32);
+        // padding rows (r >= rows) reuse a real row's query and are never
+        // stored; they must not be masked harder than it
+        lim[nb] = a.ctx_len + i;
+    }
+
+    f32x4 o[MD][NBW];
+    float mref[NBW], lrow[NBW];
+
+    // V^T operands of a tile: two transposing LDS reads per 16 dims.  They
+    // are issued before the next step's DMA, because the compiler cannot
+    // tell a transposing read from a write still in flight and would wait
+    // for every outstanding load in front of it.
+    auto read_vt = [&](auto ring_tag, bf16x8 (&vop)[MD]) {
+        constexpr bool ODD = decltype(ring_tag)::value;
+        WF_LDS(const char) *vt = (WF_LDS(const char) *)(ODD ? ring1 : ring0)
+                                 + stream * TG::kTileBytes + TG::kHalfBytes;
+        const int q4 = m16 & 3, qk = m16 >> 2;
 #pragma unroll
-                for (int kk = 0; kk < KC; ++kk)
-                    acc = mfma16x16x32(kc[mb][kk], qf[nb][kk], acc);
-                s[mb][nb] = acc;
+        for (int md = 0; md < MD; ++md) {
+            v4i16 half[2];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                const int kl = 16 * hh + 4 * c4 + qk;
+                const int ps = md ^ (kl & (TG::kSegs - 1));
+                WF_LDS(const char) *src = vt + kl * TG::kRowBytes + ps * 32 + q4 * 8;
+                half[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((WF_LDS(v4i16) *)src);
             }
-
-        // V tile -> LDS (granule swizzle: gi ^ 2*((key/8)%4))
-#pragma unroll
-        for (int r = 0; r < VLD; ++r) {
-            const int chunk = r * kWave + lane;
-            const int kl = chunk / GR;
-            const int gi = chunk % GR;
-            const int gs = gi ^ (2 * ((kl >> 3) & 3));
-            *reinterpret_cast<u32x4 *>(vt + kl * DH + gs * 8) = __builtin_bit_cast(u32x4, vc[r]);
+            typedef short v8i16 __attribute__((ext_vector_type(8)));
+            const v8i16 both = __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7);
+            vop[md] = __builtin_bit_cast(bf16x8, both);
         }
+    };
 
-        // causal mask + online softmax
+    auto compute = [&](auto ring_tag, int t, const bf16x8 (&vop)[MD], auto rescale_tag) {
+        constexpr bool RESCALE = decltype(rescale_tag)::value;
+        constexpr bool ODD = decltype(ring_tag)::value;
+        // LDS pointers derived from the ring object itself, so the compiler
+        // can tell these reads from the DMA writes into the other half
+        WF_LDS(const char) *kt = (WF_LDS(const char) *)(ODD ? ring1 : ring0) + stream * TG::kTileBytes;
+        // S^T = K Q^T, K operands from LDS
+        f32x4 s[2][NBW];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                s[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const int kl = 16 * mb + m16;
+#pragma unroll
+            for (int kk = 0; kk < KC; ++kk) {
+                const int pg = (4 * kk + c4) ^ (kl & (TG::kGran - 1));
+                const bf16x8 kop = __builtin_bit_cast(
+                    bf16x8, *(WF_LDS(const u32x4) *)(kt + kl * TG::kRowBytes + pg * 16));
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb)
+                    s[mb][nb] = mfma16x16x32(kop, qf[nb][kk], s[mb][nb]);
+            }
+        }
+        // causal mask: only tiles reaching past ctx_len
         const int kb = k_begin + t * kTileKeys;
-        const bool need_mask = (kb + kTileKeys - 1) > a.ctx_len;
-        bf16x8 pb[NB];
+        if (kb + kTileKeys - 1 > a.ctx_len) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            float mx = -INFINITY;
+            for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
+                for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = kb + 8 * c4 + 4 * mb + i;
-                    if (need_mask && key > lim[nb])
-                        s[mb][nb][i] = -INFINITY;
-                    mx = fmaxf(mx, s[mb][nb][i]);
+                    for (int i = 0; i < 4; ++i) {
+                        const int key = kb + 16 * mb + 4 * c4 + i;
+                        s[mb][nb][i] = (key > lim[nb]) ? -INFINITY : s[mb][nb][i];
+                    }
+        }
+        float mx[NBW];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) {
+            float m = fmaxf(fmaxf(fmaxf(s[0][nb][0], s[0][nb][1]), fmaxf(s[0][nb][2], s[0][nb][3])),
+                            fmaxf(fmaxf(s[1][nb][0], s[1][nb][1]), fmaxf(s[1][nb][2], s[1][nb][3])));
+            m = fmaxf(m, __shfl_xor(m, 16, kWave));
+            m = fmaxf(m, __shfl_xor(m, 32, kWave));
+            mx[nb] = m;
+        }
+        if constexpr (RESCALE) {
+            bool grow = false;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                grow |= (mx[nb] - mref[nb]) * sl2 > 8.f;
+            if (__ballot(grow)) {
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb) {
+                    const float nr = ((mx[nb] - mref[nb]) * sl2 > 8.f) ? mx[nb] : mref[nb];
+                    const float alpha = (nr == mref[nb]) ? 1.f : fast_exp2((mref[nb] - nr) * sl2);
+                    lrow[nb] *= alpha;
+#pragma unroll
+                    for (int md = 0; md < MD; ++md)
+                        o[md][nb] *= alpha;
+                    mref[nb] = nr;
                 }
-            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-            const float mnew = fmaxf(mrow[nb], mx);
-            const float muse = (mnew == -INFINITY) ? 0.f : mnew;
-            const float alpha = exp2f((mrow[nb] - muse) * a.sl2);
-            const float moff = -muse * a.sl2;
-            mrow[nb] = mnew;
-            float psum = 0.f;
+            }
+        } else {
+            bool over = false;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+                if (mref[nb] == -INFINITY)
+                    mref[nb] = mx[nb];       // O and l are still zero
+                else
+                    over |= (mx[nb] - mref[nb]) * sl2 > 64.f;
+            }
+            if (__ballot(over))
+                overflow = 1;                // the workgroup reruns rescaling
+        }
+        // P = exp2((S - mref) * scale * log2 e) in the P^T operand layout
+        bf16x8 pb[NBW];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) {
+            const float moff = (mref[nb] == -INFINITY) ? 0.f : -mref[nb] * sl2;
             float p[8];
+            float psum = 0.f;
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float e = exp2f(fmaf(s[mb][nb][i], a.sl2, moff));
+                    const float e = fast_exp2(fmaf(s[mb][nb][i], sl2, moff));
                     p[4 * mb + i] = e;
                     psum += e;
                 }
-            lrow[nb] = fmaf(lrow[nb], alpha, psum);
-#pragma unroll
-            for (int md = 0; md < MD; ++md)
-                o[md][nb] *= alpha;
-            uint32_t pw[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                pw[j] = (uint32_t)f32_to_bf16(p[2 * j]) |
-                        ((uint32_t)f32_to_bf16(p[2 * j + 1]) << 16);
-            u32x4 pv = {pw[0], pw[1], pw[2], pw[3]};
+            lrow[nb] += psum;
+            u32x4 pv = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                        pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
             pb[nb] = __builtin_bit_cast(bf16x8, pv);
         }
+        // O^T += V^T P^T
+#pragma unroll
+        for (int md = 0; md < MD; ++md)
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                o[md][nb] = mfma16x16x32(vop[md], pb[nb], o[md][nb]);
+    };
 
-        // O^T += V^T P^T   (A operand: V[8*c4 + j][16*md + m16], j = 0..7)
-        __builtin_amdgcn_wave_barrier();
+    // One pass over the split.  The step loop is unrolled by two so each
+    // half reads a compile-time ring half while the other is being filled.
+    auto pass = [&](auto rescale_tag, bool first_pass) {
 #pragma unroll
-        for (int md = 0; md < MD; ++md) {
-            const int gi = 2 * md + (m16 >> 3);
-            const int gs = gi ^ (2 * c4);
-            const uint16_t *src = vt + (8 * c4) * DH + gs * 8 + (m16 & 7);
-            uint32_t w[4];
+        for (int nb = 0; nb < NBW; ++nb) {
+            mref[nb] = -INFINITY;
+            lrow[nb] = 0.f;
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                w[j] = (uint32_t)src[(2 * j) * DH] | ((uint32_t)src[(2 * j + 1) * DH] << 16);
-            u32x4 av = {w[0], w[1], w[2], w[3]};
-            const bf16x8 va = __builtin_bit_cast(bf16x8, av);
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-                o[md][nb] = mfma16x16x32(va, pb[nb], o[md][nb]);
+            for (int md = 0; md < MD; ++md)
+                o[md][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        __builtin_amdgcn_wave_barrier();
-    }
+        if (!first_pass && stream < n_tiles)
+            issue(ring0, stream);
+        bf16x8 vop[MD];
+        for (int step = 0; step < n_steps; step += 2) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            const bool have0 = stream + KS * step < n_tiles;
+            if (have0)
+                read_vt(std::false_type{}, vop);
+            if (step + 1 < n_steps && stream + KS * (step + 1) < n_tiles)
+                issue(ring1, stream + KS * (step + 1));
+            if (have0)
+                compute(std::false_type{}, stream + KS * step, vop, rescale_tag);
+            if (step + 1 >= n_steps)
+                break;
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            const bool have1 = stream + KS * (step + 1) < n_tiles;
+            if (have1)
+                read_vt(std::true_type{}, vop);
+            if (step + 2 < n_steps && stream + KS * (step + 2) < n_tiles)
+                issue(ring0, stream + KS * (step + 2));
+            if (have1)
+                compute(std::true_type{}, stream + KS * (step + 1), vop, rescale_tag);
+        }
+        __syncthreads();
+    };
+
+    pass(std::false_type{}, true);
+    if (overflow)                            // uniform: read after a barrier
+        pass(std::true_type{}, false);
 
     // ---- per-wave row sums (the 4 K-groups of a row hold disjoint keys) -----
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+    for (int nb = 0; nb < NBW; ++nb) {
         float l = lrow[nb];
         l += __shfl_xor(l, 16, kWave);
         l += __shfl_xor(l, 32, kWave);
         lrow[nb] = l;
         if (c4 == 0) {
-            mls[wave][nb * 16 + m16][0] = mrow[nb];
-            mls[wave][nb * 16 + m16][1] = l;
+            mls[stream][rgi * ROWS_W + nb * 16 + m16][0] = mref[nb];
+            mls[stream][rgi * ROWS_W + nb * 16 + m16][1] = l;
         }
     }
     __syncthreads();
 
-    // ---- merge the four waves in a fixed order through LDS ------------------
-    float fac[NB];
+    // ---- merge the KS streams of each row through LDS ----------------------
+    // Streams s and s + KS/2 share region s % (KS/2): round 0 writes streams
+    // 0..KS/2-1, round 1 adds the rest, and the partial write below sums the
+    // regions -- a fixed order throughout.
+    auto oreg = [&](int r) { return reinterpret_cast<float *>(r ? ring1 : ring0); };
+    float fac[NBW];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const int r = nb * 16 + m16;
+    for (int nb = 0; nb < NBW; ++nb) {
+        const int r = rgi * ROWS_W + nb * 16 + m16;
         float mm = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < kAttnWaves; ++w)
-            mm = fmaxf(mm, mls[w][r][0]);
+        for (int st = 0; st < KS; ++st)
+            mm = fmaxf(mm, mls[st][r][0]);
         const float muse = (mm == -INFINITY) ? 0.f : mm;
-        fac[nb] = (mrow[nb] == -INFINITY) ? 0.f : exp2f((mrow[nb] - muse) * a.sl2);
+        fac[nb] = (mref[nb] == -INFINITY) ? 0.f : fast_exp2((mref[nb] - muse) * sl2);
     }
 #pragma unroll 1
-    for (int w = 0; w < kAttnWaves; ++w) {
-        if (wave == w) {
+    for (int round = 0; round < 2; ++round) {
+        if ((stream >= NREG) == (round == 1)) {
+            float *reg = oreg(stream % NREG);
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
+            for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
                 for (int md = 0; md < MD; ++md) {
-                    float *dst = osum + (nb * 16 + m16) * DH + md * 16 + 4 * c4;
+                    float *dst = reg + (rgi * ROWS_W + nb * 16 + m16) * OST + md * 16 + 4 * c4;
                     f32x4 v = o[md][nb] * fac[nb];
-                    if (w > 0)
+                    if (round == 1)
                         v += *reinterpret_cast<f32x4 *>(dst);
                     *reinterpret_cast<f32x4 *>(dst) = v;
                 }
@@ -301,28 +422,30 @@ __global__ __launch_bounds__(256) void attn_partial_bf16(AttnParams a) {
 
     // ---- write the workgroup partial ----------------------------------------
     const int pairs = a.gamma * a.n_q_heads;
-    for (int idx = threadIdx.x; idx < ROWS * (DH / 4); idx += blockDim.x) {
+    for (int idx = threadIdx.x; idx < ROWS_WG * (DH / 4); idx += blockDim.x) {
         const int rl = idx / (DH / 4);
         const int d4 = idx % (DH / 4);
-        const int r = rg * ROWS + rl;
+        const int r = rgw * ROWS_WG + rl;
         if (r >= a.rows)
             continue;
         const int i = r / a.group;
         const int h = g * a.group + (r % a.group);
         const size_t pr = (size_t)split * pairs + (size_t)i * a.n_q_heads + h;
-        reinterpret_cast<f32x4 *>(a.ws_acc + pr * DH)[d4] =
-            reinterpret_cast<const f32x4 *>(osum + rl * DH)[d4];
+        f32x4 v = reinterpret_cast<const f32x4 *>(oreg(0) + rl * OST)[d4];
+        if (NREG > 1)
+            v += reinterpret_cast<const f32x4 *>(oreg(1) + rl * OST)[d4];
+        reinterpret_cast<f32x4 *>(a.ws_acc + pr * DH)[d4] = v;
         if (d4 == 0) {
             float mm = -INFINITY, ll = 0.f;
 #pragma unroll
-            for (int w = 0; w < kAttnWaves; ++w)
-                mm = fmaxf(mm, mls[w][rl][0]);
+            for (int st = 0; st < KS; ++st)
+                mm = fmaxf(mm, mls[st][rl][0]);
             const float muse = (mm == -INFINITY) ? 0.f : mm;
 #pragma unroll
-            for (int w = 0; w < kAttnWaves; ++w) {
-                const float mw = mls[w][rl][0];
-                const float f = (mw == -INFINITY) ? 0.f : exp2f((mw - muse) * a.sl2);
-                ll = fmaf(mls[w][rl][1], f, ll);
+            for (int st = 0; st < KS; ++st) {
+                const float mw = mls[st][rl][0];
+                const float f = (mw == -INFINITY) ? 0.f : fast_exp2((mw - muse) * sl2);
+                ll = fmaf(mls[st][rl][1], f, ll);
             }
             a.ws_ml[pr * 2] = mm;
             a.ws_ml[pr * 2 + 1] = ll;
@@ -397,8 +520,10 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
 }
 
 // ---------------------------------------------------------------------------
-// Split merge: out = sum_s w_s acc_s / sum_s w_s l_s, w_s = exp(m_s - max m),
-// splits combined in ascending order.  One wave per (row, q head).
+// Split merge: out = sum_s w_s acc_s / sum_s w_s l_s, w_s = exp(m_s - max m).
+// One wave per (row, q head).  Lane j owns splits j, j+64, ...: it computes
+// their weights, which are then broadcast across the wave while every lane
+// accumulates its output dims over the splits in ascending order.
 // ---------------------------------------------------------------------------
 template <int DH, bool OUT_BF16>
 __global__ __launch_bounds__(64) void attn_merge(const float *__restrict__ ws_acc,
@@ -406,6 +531,7 @@ __global__ __launch_bounds__(64) void attn_merge(const float *__restrict__ ws_ac
                                                  void *out, int pairs, int splits,
                                                  float sl2) {
     constexpr int E = DH / kWave;
+    constexpr int B = 32;                    // splits per batch, loads in flight
     const int pr = blockIdx.x;
     const int lane = threadIdx.x;
     float mloc = -INFINITY;
@@ -413,28 +539,46 @@ __global__ __launch_bounds__(64) void attn_merge(const float *__restrict__ ws_ac
         mloc = fmaxf(mloc, ws_ml[((size_t)s * pairs + pr) * 2]);
     const float mm = wave_max(mloc);
     const float muse = (mm == -INFINITY) ? 0.f : mm;
-    float acc[E], lsum = 0.f;
+    float acc[E], lpart = 0.f;
 #pragma unroll
     for (int e = 0; e < E; ++e)
         acc[e] = 0.f;
-    for (int s = 0; s < splits; ++s) {
-        const size_t ps = (size_t)s * pairs + pr;
-        const float ms = ws_ml[ps * 2];
-        const float w = (ms == -INFINITY) ? 0.f : exp2f((ms - muse) * sl2);
-        lsum = fmaf(w, ws_ml[ps * 2 + 1], lsum);
+    const float *col = ws_acc + (size_t)pr * DH + lane;
+    const size_t sstride = (size_t)pairs * DH;
+    for (int s0 = 0; s0 < splits; s0 += B) {
+        // lane j < B weighs split s0 + j
+        float wl = 0.f;
+        if (lane < B && s0 + lane < splits) {
+            const size_t ps = (size_t)(s0 + lane) * pairs + pr;
+            const float ms = ws_ml[ps * 2];
+            wl = (ms == -INFINITY) ? 0.f : fast_exp2((ms - muse) * sl2);
+            lpart = fmaf(wl, ws_ml[ps * 2 + 1], lpart);
+        }
+        const int cnt = min(B, splits - s0);
+        const float *base = col + (size_t)s0 * sstride;
+        float v[B][E];
 #pragma unroll
-        for (int e = 0; e < E; ++e)
-            acc[e] = fmaf(w, ws_acc[ps * DH + lane + e * kWave], acc[e]);
+        for (int j = 0; j < B; ++j)
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                v[j][e] = (j < cnt) ? base[(size_t)min(j, cnt - 1) * sstride + e * kWave] : 0.f;
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            const float wj = __shfl(wl, j, kWave);     // 0 for j >= cnt
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                acc[e] = fmaf(wj, v[j][e], acc[e]);
+        }
     }
-    const float inv = 1.f / lsum;
+    const float inv = 1.f / wave_sum(lpart);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const float v = acc[e] * inv;
+        const float r = acc[e] * inv;
         const size_t oi = (size_t)pr * DH + lane + e * kWave;
         if (OUT_BF16)
-            static_cast<uint16_t *>(out)[oi] = f32_to_bf16(v);
+            static_cast<uint16_t *>(out)[oi] = f32_to_bf16(r);
         else
-            static_cast<float *>(out)[oi] = v;
+            static_cast<float *>(out)[oi] = r;
     }
 }
 
@@ -452,25 +596,43 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
     const int n_tiles = cdiv(n_keys, kTileKeys);
     p.rows = rows;
     if (dt == WF_BF16) {
-        p.nb = rows <= 16 ? 1 : rows <= 32 ? 2 : 4;
-        p.n_row_groups = cdiv(rows, 16 * p.nb);
+        // rows per wave 16*nb; rg row groups x ks key streams per workgroup
+        // (at most 8 waves, so each wave may hold up to 256 registers)
+        if (rows <= 16) {
+            p.nb = 1; p.rg = 1; p.ks = 4;
+        } else if (rows <= 32) {
+            p.nb = 1; p.rg = 2; p.ks = 4;
+        } else if (rows <= 64) {
+            p.nb = 2; p.rg = 2; p.ks = 4;
+        } else {
+            p.nb = 2; p.rg = 4; p.ks = 2;
+        }
+        p.n_row_groups = cdiv(rows, 16 * p.nb * p.rg);
     } else {
         p.nb = 0;
+        p.rg = 1;
+        p.ks = 1;
         p.n_row_groups = 1;
     }
     int splits = num_splits;
     if (splits <= 0) {
-        // aim for ~2 workgroups per CU of the 256-CU chip, but give every
-        // wave of a workgroup at least two tiles to stream
-        const int target = 512 / (n_kv_heads * p.n_row_groups);
-        const int max_by_work = std::max(1, n_tiles / (2 * kAttnWaves));
+        // one workgroup per CU of the 256-CU chip, but give every key
+        // stream of a workgroup at least two tiles
+        const int target = std::max(1, 256 / (n_kv_heads * p.n_row_groups));
+        const int max_by_work = std::max(1, n_tiles / (2 * std::max(p.ks, 4)));
         splits = std::max(1, std::min(target, max_by_work));
     }
     splits = std::min(splits, n_tiles);
-    // keys per split: whole tiles, then drop splits left empty by rounding
-    const int tiles_per_split = cdiv(n_tiles, splits);
-    p.keys_per_split = tiles_per_split * kTileKeys;
-    p.splits = cdiv(n_keys, p.keys_per_split);
+    if (dt == WF_BF16) {
+        // the bf16 kernel deals whole tiles out evenly: [s*T/S, (s+1)*T/S)
+        p.splits = splits;
+        p.keys_per_split = 0;
+    } else {
+        // fp32: contiguous key ranges of whole tiles; drop splits left empty
+        const int tiles_per_split = cdiv(n_tiles, splits);
+        p.keys_per_split = tiles_per_split * kTileKeys;
+        p.splits = cdiv(n_keys, p.keys_per_split);
+    }
     return p;
 }
 
@@ -509,13 +671,15 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
         int blocks = units;
         if (p.n_row_groups > 1)
             blocks = cdiv(units, 8) * 8 * p.n_row_groups;
-        dim3 grid(blocks), block(256);
-#define WF_ATTN_CASE(DHV, NBV)                                               \
-    if (head_dim == DHV && p.nb == NBV) {                                    \
-        attn_partial_bf16<DHV, NBV><<<grid, block, 0, stream>>>(a);          \
+        dim3 grid(blocks), block(64 * p.ks * p.rg);
+#define WF_ATTN_CASE(DHV, NBV, RGV, KSV)                                     \
+    if (head_dim == DHV && p.nb == NBV && p.rg == RGV && p.ks == KSV) {       \
+        attn_partial_bf16<DHV, NBV, RGV, KSV><<<grid, block, 0, stream>>>(a); \
     } else
-        WF_ATTN_CASE(128, 1) WF_ATTN_CASE(128, 2) WF_ATTN_CASE(128, 4)
-        WF_ATTN_CASE(64, 1) WF_ATTN_CASE(64, 2) WF_ATTN_CASE(64, 4)
+        WF_ATTN_CASE(128, 1, 1, 4) WF_ATTN_CASE(128, 1, 2, 4)
+        WF_ATTN_CASE(128, 2, 2, 4) WF_ATTN_CASE(128, 2, 4, 2)
+        WF_ATTN_CASE(64, 1, 1, 4) WF_ATTN_CASE(64, 1, 2, 4)
+        WF_ATTN_CASE(64, 2, 2, 4) WF_ATTN_CASE(64, 2, 4, 2)
         { return WF_ERR_UNSUPPORTED; }
 #undef WF_ATTN_CASE
     } else {

@@ -63,14 +63,12 @@ __global__ __launch_bounds__(512) void lm_tiles_bf16(const uint16_t *__restrict_
 #pragma unroll
     for (int mb = 0; mb < kLmMB; ++mb)
         wp[mb] = w + (size_t)min(v0 + 16 * mb + m16, vocab - 1) * d + c4 * 8;
+    // Rows past gamma read row gamma-1 instead: they only feed MFMA output
+    // columns that are never used, and nothing waits on a load early.
     const uint16_t *hp[NBL];
-    bool hvalid[NBL];
 #pragma unroll
-    for (int nb = 0; nb < NBL; ++nb) {
-        const int r = nb * 16 + m16;
-        hvalid[nb] = r < gamma;
-        hp[nb] = h + (size_t)min(r, gamma - 1) * d + c4 * 8;
-    }
+    for (int nb = 0; nb < NBL; ++nb)
+        hp[nb] = h + (size_t)min(nb * 16 + m16, gamma - 1) * d + c4 * 8;
 
     f32x4 acc[kLmMB][NBL];
 #pragma unroll
@@ -89,29 +87,43 @@ __global__ __launch_bounds__(512) void lm_tiles_bf16(const uint16_t *__restrict_
         for (int mb = 0; mb < kLmMB; ++mb)
             wr[mb] = load_bf16x8(wp[mb] + off);
 #pragma unroll
-        for (int nb = 0; nb < NBL; ++nb) {
-            const bf16x8 v = load_bf16x8(hp[nb] + off);
-            hr[nb] = hvalid[nb] ? v : zero_bf16x8();
-        }
+        for (int nb = 0; nb < NBL; ++nb)
+            hr[nb] = load_bf16x8(hp[nb] + off);
     };
+    auto mac = [&](const bf16x8 (&wr)[kLmMB], const bf16x8 (&hr)[NBL]) {
 #pragma unroll
-    for (int p = 0; p < kLmPrefetch; ++p)
-        if (p < cpw)
-            load_chunk(p, wb[p], hb[p]);
-    for (int u0 = 0; u0 < cpw; u0 += kLmPrefetch) {
+        for (int mb = 0; mb < kLmMB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < NBL; ++nb)
+                acc[mb][nb] = mfma16x16x32(wr[mb], hr[nb], acc[mb][nb]);
+    };
+    // Steady state without branches, so the compiler's wait counting stays
+    // exact and kLmPrefetch chunks stay in flight: consume a group of chunks
+    // while refilling the same registers with the next group.
+    const int ngroups = cpw / kLmPrefetch;
+    if (ngroups > 0) {
 #pragma unroll
         for (int p = 0; p < kLmPrefetch; ++p) {
-            const int u = u0 + p;
-            if (u < cpw) {
+            load_chunk(p, wb[p], hb[p]);
+            __builtin_amdgcn_sched_barrier(0);   // issue chunk by chunk
+        }
+        for (int gi = 0; gi < ngroups - 1; ++gi) {
 #pragma unroll
-                for (int mb = 0; mb < kLmMB; ++mb)
-#pragma unroll
-                    for (int nb = 0; nb < NBL; ++nb)
-                        acc[mb][nb] = mfma16x16x32(wb[p][mb], hb[p][nb], acc[mb][nb]);
-                if (u + kLmPrefetch < cpw)
-                    load_chunk(u + kLmPrefetch, wb[p], hb[p]);
+            for (int p = 0; p < kLmPrefetch; ++p) {
+                mac(wb[p], hb[p]);
+                load_chunk((gi + 1) * kLmPrefetch + p, wb[p], hb[p]);
+                // keep each refill right behind the MFMAs that free its
+                // registers, so kLmPrefetch chunks stay in flight
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
+#pragma unroll
+        for (int p = 0; p < kLmPrefetch; ++p)
+            mac(wb[p], hb[p]);
+    }
+    for (int u = ngroups * kLmPrefetch; u < cpw; ++u) {
+        load_chunk(u, wb[0], hb[0]);
+        mac(wb[0], hb[0]);
     }
 
     // partial logits of the 8 waves meet in LDS in a fixed order

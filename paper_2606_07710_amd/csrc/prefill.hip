@@ -69,14 +69,12 @@ __global__ __launch_bounds__(512) void prefill_bf16(PrefillParams a) {
     const uint16_t *wp[2] = {
         w + (size_t)(f_lo + m16) * a.d_in + c4 * 8,
         w + (size_t)(f_lo + DH / 2 + m16) * a.d_in + c4 * 8};
+    // Tokens past n_tok read the last token instead: they only feed MFMA
+    // output columns that are never stored, and nothing waits on a load early.
     const uint16_t *xp[NBT];
-    bool xvalid[NBT];
 #pragma unroll
-    for (int nb = 0; nb < NBT; ++nb) {
-        const int t = t0 + nb * 16 + m16;
-        xvalid[nb] = t < a.n_tok;
-        xp[nb] = x + (size_t)min(t, a.n_tok - 1) * a.d_in + c4 * 8;
-    }
+    for (int nb = 0; nb < NBT; ++nb)
+        xp[nb] = x + (size_t)min(t0 + nb * 16 + m16, a.n_tok - 1) * a.d_in + c4 * 8;
 
     f32x4 acc[2][NBT];
 #pragma unroll
@@ -93,29 +91,42 @@ __global__ __launch_bounds__(512) void prefill_bf16(PrefillParams a) {
         wr[0] = load_bf16x8(wp[0] + off);
         wr[1] = load_bf16x8(wp[1] + off);
 #pragma unroll
-        for (int nb = 0; nb < NBT; ++nb) {
-            const bf16x8 v = load_bf16x8(xp[nb] + off);
-            xr[nb] = xvalid[nb] ? v : zero_bf16x8();
-        }
+        for (int nb = 0; nb < NBT; ++nb)
+            xr[nb] = load_bf16x8(xp[nb] + off);
     };
+    auto mac = [&](const bf16x8 (&wr)[2], const bf16x8 (&xr)[NBT]) {
 #pragma unroll
-    for (int p = 0; p < kPfPrefetch; ++p)
-        if (p < cpw)
-            load_chunk(p, wb[p], xb[p]);
-    for (int u0 = 0; u0 < cpw; u0 += kPfPrefetch) {
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < NBT; ++nb)
+                acc[mb][nb] = mfma16x16x32(wr[mb], xr[nb], acc[mb][nb]);
+    };
+    // Branch-free steady state (exact wait counting, kPfPrefetch chunks in
+    // flight), peeled last group, then any remainder chunks.
+    const int ngroups = cpw / kPfPrefetch;
+    if (ngroups > 0) {
 #pragma unroll
         for (int p = 0; p < kPfPrefetch; ++p) {
-            const int u = u0 + p;
-            if (u < cpw) {
+            load_chunk(p, wb[p], xb[p]);
+            __builtin_amdgcn_sched_barrier(0);   // issue chunk by chunk
+        }
+        for (int gi = 0; gi < ngroups - 1; ++gi) {
 #pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                    for (int nb = 0; nb < NBT; ++nb)
-                        acc[mb][nb] = mfma16x16x32(wb[p][mb], xb[p][nb], acc[mb][nb]);
-                if (u + kPfPrefetch < cpw)
-                    load_chunk(u + kPfPrefetch, wb[p], xb[p]);
+            for (int p = 0; p < kPfPrefetch; ++p) {
+                mac(wb[p], xb[p]);
+                load_chunk((gi + 1) * kPfPrefetch + p, wb[p], xb[p]);
+                // keep each refill right behind the MFMAs that free its
+                // registers, so kPfPrefetch chunks stay in flight
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
+#pragma unroll
+        for (int p = 0; p < kPfPrefetch; ++p)
+            mac(wb[p], xb[p]);
+    }
+    for (int u = ngroups * kPfPrefetch; u < cpw; ++u) {
+        load_chunk(u, wb[0], xb[0]);
+        mac(wb[0], xb[0]);
     }
 
     // lane (m16, c4) holds D[feature 4*c4 + i][token nb*16 + m16]

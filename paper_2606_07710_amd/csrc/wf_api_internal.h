@@ -8,14 +8,16 @@
 #include <cstddef>
 #include <cstdint>
 
-#include "../../include/wf.h"
+#include "wf.h"
 
 namespace wf {
 
 struct AttnPlan {
     int rows;            // G * gamma query rows per KV head
     int nb;              // 16-row blocks per wave (bf16 path)
-    int n_row_groups;    // row groups of 16*nb rows
+    int rg;              // row groups of waves per workgroup
+    int ks;              // key streams per workgroup
+    int n_row_groups;    // workgroup row groups of 16*nb*rg rows
     int splits;          // key splits per KV head
     int keys_per_split;  // multiple of the 32-key tile
 };
