@@ -41,7 +41,10 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="replay the step as one captured HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-layers", type=int, default=None)
+    ap.add_argument("--cpu-budget-s", type=float, default=20.0,
+                    help="approximate seconds of oracle work for cpu_baseline")
+    ap.add_argument("--cpu-sample-layers", type=int, default=None,
+                    help="cap on the layers the cpu baseline runs")
     ap.add_argument("--copy-probe-mib", type=int, default=1024,
                     help="size of the plain device copy run after timing "
                          "(reference for HBM traffic counters); 0 = off")
@@ -56,10 +59,10 @@ class Step:
     """Pre-marshalled C-ABI calls of one verification step."""
 
     def __init__(self, w, layers, head, outs, lmouts, draft, tau, ws_attn,
-                 ws_lm, wf):
+                 ws_pre, ws_lm, wf):
         self.w, self.layers, self.head = w, layers, head
         self.outs, self.lmouts, self.draft, self.tau = outs, lmouts, draft, tau
-        self.ws_attn, self.ws_lm, self.wf = ws_attn, ws_lm, wf
+        self.ws_attn, self.ws_pre, self.ws_lm, self.wf = ws_attn, ws_pre, ws_lm, wf
 
     def build(self, stream_ptr):
         w, wf = self.w, self.wf
@@ -80,7 +83,8 @@ class Step:
                 self.pre.append((code, P(t["x"]), P(t["w_k"]), P(t["w_v"]), P(kc),
                                  P(vc), w.n_prefill, w.prefill_start,
                                  kc.shape[1], w.hidden, w.n_kv_heads,
-                                 w.head_dim, w.rope_base, s))
+                                 w.head_dim, w.rope_base, P(self.ws_pre),
+                                 self.ws_pre.numel(), s))
         am, ent, acc = self.lmouts[0]
         self.lm = [(code, P(self.head["h"]), P(self.head["w_lm"]), None,
                     P(self.draft), w.gamma, w.hidden, w.vocab, self.tau, P(am),
@@ -92,77 +96,83 @@ class Step:
                             P(am2), P(ent2), P(acc2), P(self.ws_lm),
                             self.ws_lm.numel(), s))
 
-    def run(self, check=False, attn_events=None, phase_events=None):
+    def run(self, check=False):
         lib = self.wf.lib
-        pe = phase_events
-        if pe:
-            pe[0].record()
-        for l, a in enumerate(self.attn):
-            if attn_events:
-                attn_events[l][0].record()
+        for a in self.attn:
             rc = lib.wf_verify_attn(*a)
-            if attn_events:
-                attn_events[l][1].record()
             if check and rc:
                 raise RuntimeError(f"wf_verify_attn: {self.wf.status_string(rc)}")
-        if pe:
-            pe[1].record()
         for a in self.pre:
             rc = lib.wf_kv_only_prefill(*a)
             if check and rc:
                 raise RuntimeError(f"wf_kv_only_prefill: {self.wf.status_string(rc)}")
-        if pe:
-            pe[2].record()
         for a in self.lm:
             rc = lib.wf_lmhead_accept_entropy(*a)
             if check and rc:
                 raise RuntimeError(f"wf_lmhead_accept_entropy: {self.wf.status_string(rc)}")
-        if pe:
-            pe[3].record()
+
+    def phases(self):
+        """(name, C function, argument tuples) of the step's three phases."""
+        lib = self.wf.lib
+        return [("attention", lib.wf_verify_attn, self.attn),
+                ("prefill", lib.wf_kv_only_prefill, self.pre),
+                ("lmhead", lib.wf_lmhead_accept_entropy, self.lm)]
 
 
-def cpu_baseline(w, layers, head, sample_layers):
+def cpu_baseline(w, layers, head, budget_s, max_layers=None):
     """The oracle as it stands, on host cores, over a bounded sample of the
-    step: `sample_layers` layers of attention and prefill plus the LM head;
-    scaled to one full step."""
+    step: the LM head, then as many layers of attention and prefill as fit
+    in about `budget_s` seconds (all of them if they fit); scaled to one
+    full step."""
     import oracle
     import workloads as W
     n = w.ctx_len + w.gamma
+    h, wl = W.to_oracle(head["h"]), W.to_oracle(head["w_lm"])
+    t0 = time.perf_counter()
+    oracle.lmhead_rows(h, wl)
+    t_lm = time.perf_counter() - t0
+    del h, wl
+    if w.router_logits:
+        z = head["router_logits"].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.lmhead_rows(logits=z)
+        t_lm += time.perf_counter() - t0
+    log(f"cpu baseline: LM head {t_lm:.2f}s")
     t_attn = t_pre = 0.0
-    for l in range(sample_layers):
-        t = layers[l]
+    done = 0
+    limit = w.n_layers if max_layers is None else min(max_layers, w.n_layers)
+    while done < limit:
+        t = layers[done]
         q = W.to_oracle(t["q"])
         k = W.to_oracle(t["k_cache"][:, :n].contiguous())
         v = W.to_oracle(t["v_cache"][:, :n].contiguous())
         t0 = time.perf_counter()
         oracle.verify_attn(q, k, v, w.ctx_len)
         t_attn += time.perf_counter() - t0
+        del q, k, v
         if w.n_prefill:
             x, wk, wv = (W.to_oracle(t[k_]) for k_ in ("x", "w_k", "w_v"))
             t0 = time.perf_counter()
             oracle.kv_only_prefill(x, wk, wv, w.prefill_start, w.n_kv_heads,
                                    w.head_dim, w.rope_base)
             t_pre += time.perf_counter() - t0
-        log(f"cpu baseline: layer {l} done")
-    h, wl = W.to_oracle(head["h"]), W.to_oracle(head["w_lm"])
-    t0 = time.perf_counter()
-    oracle.lmhead_rows(h, wl)
-    t_lm = time.perf_counter() - t0
-    if w.router_logits:
-        z = head["router_logits"].cpu().numpy()
-        t0 = time.perf_counter()
-        oracle.lmhead_rows(logits=z)
-        t_lm += time.perf_counter() - t0
-    per_step_s = (t_attn + t_pre) / sample_layers * w.n_layers + t_lm
+        done += 1
+        spent = t_lm + t_attn + t_pre
+        log(f"cpu baseline: layer {done - 1} done ({spent:.1f}s)")
+        if spent + (t_attn + t_pre) / done > budget_s:
+            break
+    per_step_s = (t_attn + t_pre) / done * w.n_layers + t_lm
+    whole = done == w.n_layers
     return {
         "value": round(per_step_s * 1e6, 1),
         "unit": "us",
         "cores": oracle.num_threads(),
         "kind": "oracle",
-        "sample": (f"{sample_layers} of {w.n_layers} layers (attention, all "
-                   f"{w.gamma * w.n_q_heads} rows x heads"
-                   + (", KV-only prefill" if w.n_prefill else "")
-                   + ") + full LM head; scaled to one step"),
+        "sample": ("the whole step: " if whole else
+                   f"{done} of {w.n_layers} layers, scaled to one step: ")
+                  + f"attention over all {w.gamma * w.n_q_heads} rows x heads"
+                  + (", KV-only prefill" if w.n_prefill else "")
+                  + ", full LM head",
         "measured_s": round(t_attn + t_pre + t_lm, 2),
     }
 
@@ -201,6 +211,10 @@ def main():
         wf.wf_verify_attn_workspace_bytes(1 if w.dtype == "bf16" else 0,
                                           w.gamma, w.ctx_len, w.n_q_heads,
                                           w.n_kv_heads, w.head_dim), dev)
+    ws_pre = wf.alloc_workspace(
+        wf.wf_kv_only_prefill_workspace_bytes(1 if w.dtype == "bf16" else 0,
+                                              w.n_prefill, w.hidden,
+                                              w.n_kv_heads, w.head_dim), dev)
     ws_lm = wf.alloc_workspace(wf.wf_lmhead_workspace_bytes(w.gamma, w.vocab), dev)
     lmouts = [(torch.empty(w.gamma, dtype=torch.int32, device=dev),
                torch.empty(w.gamma, dtype=torch.float32, device=dev),
@@ -219,7 +233,8 @@ def main():
                             device=dev)
     tau = float(np.median(ent.cpu().numpy()))
 
-    step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_lm, wf)
+    step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_pre,
+                ws_lm, wf)
     stream = torch.cuda.current_stream()
     step.build(stream.cuda_stream)
     step.run(check=True)
@@ -266,22 +281,32 @@ def main():
     log(f"timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step "
         f"(host wall {wall / args.steps * 1e6:.1f} us/step)")
 
-    # ---- timed region 2: per-call events on the dominant kernel ------------
-    n_l = w.n_layers
-    ev = lambda: torch.cuda.Event(enable_timing=True)
-    attn_ev = [[[ev(), ev()] for _ in range(n_l)] for _ in range(args.steps)]
-    phase_ev = [[ev() for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for s in range(args.steps):
-        step.run(attn_events=attn_ev[s], phase_events=phase_ev[s])
-    torch.cuda.synchronize()
-    attn_ms = [a.elapsed_time(b) for evs in attn_ev for a, b in evs]
-    phases = np.array([[p[0].elapsed_time(p[1]), p[1].elapsed_time(p[2]),
-                        p[2].elapsed_time(p[3])] for p in phase_ev])
-    attn_avg_ms = float(np.mean(attn_ms))
-    log(f"attention call avg {attn_avg_ms * 1e3:.2f} us, phases (us) "
-        f"attn {phases[:, 0].mean() * 1e3:.1f} prefill "
-        f"{phases[:, 1].mean() * 1e3:.1f} lmhead {phases[:, 2].mean() * 1e3:.1f}")
+    # ---- timed region 2: each phase alone, calls back to back --------------
+    # Events bracket only whole runs of one kind of call, so a per-call
+    # average includes no event overhead and matches what a kernel trace
+    # reports for the kernels of that call.
+    per_call_ms = {}
+    for name, fn, calls in step.phases():
+        if not calls:
+            per_call_ms[name] = 0.0
+            continue
+        for a in calls:                       # warm this phase alone
+            fn(*a)
+        a_ev = torch.cuda.Event(enable_timing=True)
+        b_ev = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a_ev.record()
+        for _ in range(args.steps):
+            for a in calls:
+                fn(*a)
+        b_ev.record()
+        torch.cuda.synchronize()
+        per_call_ms[name] = a_ev.elapsed_time(b_ev) / (args.steps * len(calls))
+    attn_avg_ms = per_call_ms["attention"]
+    breakdown = {name: round(per_call_ms[name] * len(calls) * 1e3, 1)
+                 for name, _, calls in step.phases()}
+    log(f"per call (us): " + ", ".join(f"{k} {v * 1e3:.2f}"
+                                       for k, v in per_call_ms.items()))
 
     by = w.algorithmic_bytes()
     achieved = by["attn_per_layer"] / (attn_avg_ms * 1e-3) / 1e9
@@ -298,9 +323,9 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        sample = args.cpu_sample_layers or (w.n_layers if w.n_layers <= 2 else 4)
-        log(f"cpu baseline on {sample} layers ...")
-        cpu = cpu_baseline(w, layers, head, sample)
+        log(f"cpu baseline: about {args.cpu_budget_s:.0f}s of oracle work ...")
+        cpu = cpu_baseline(w, layers, head, args.cpu_budget_s,
+                           args.cpu_sample_layers)
 
     line = {
         "metric": "verify-step us and achieved HBM GB/s (gamma=16, 32K ctx, "
@@ -326,11 +351,9 @@ def main():
                    "graph": bool(graph is not None)},
         "step_hbm_gbps": round(step_gbps, 1),
         "step_algorithmic_bytes": by["total"],
-        "breakdown_us": {"attention": round(float(phases[:, 0].mean()) * 1e3, 1),
-                         "prefill": round(float(phases[:, 1].mean()) * 1e3, 1),
-                         "lmhead": round(float(phases[:, 2].mean()) * 1e3, 1)},
+        "breakdown_us": breakdown,
         "roofline": {
-            "kernel": "wf_verify_attn (one layer: split partial + merge)",
+            "kernel": "wf_verify_attn, one layer (attn_partial_bf16 + attn_merge)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": PEAK_HBM_GBPS,

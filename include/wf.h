@@ -28,8 +28,13 @@
  *     non-OK status nothing was enqueued.  A failed kernel launch returns
  *     WF_ERR_HIP.
  *   - Workspaces are caller-owned scratch of at least the size the matching
- *     *_workspace_bytes query returns.  Contents need no initialisation and
- *     are clobbered.  Two calls that overlap in time must not share one.
+ *     *_workspace_bytes query returns, ZERO-FILLED before their first use.
+ *     Each starts with a 64 KiB block of arrival counters, with which the
+ *     last workgroup of a cross-workgroup reduction finishes it; partial
+ *     results follow that block.  Every call leaves the counter block at
+ *     zero again, so a workspace zeroed once serves any later call, of any
+ *     of the three kinds and any sizes.  Two calls that overlap in time
+ *     must not share one.
  *   - Reductions use a fixed order, so repeated calls on the same inputs and
  *     the same split count return bit-identical results.
  *   - Row-major throughout; "[a][b][c]" lists dimensions slowest first.
@@ -130,13 +135,24 @@ size_t wf_verify_attn_workspace_bytes(wf_dtype_t dt, int32_t gamma,
  * Limits:   0 <= n_tok <= 4096 (0 is a no-op); start_pos >= 0;
  *           start_pos + n_tok <= cap; head_dim in {64, 128};
  *           d_in >= 1, and d_in % 32 == 0 for WF_BF16.
+ * workspace >= wf_kv_only_prefill_workspace_bytes(...) bytes (may be NULL
+ *           when that is 0: fp32, or no tokens).  The bf16 path splits the
+ *           input dimension across workgroups and sums the slices in a
+ *           fixed order.
  * ---------------------------------------------------------------------- */
 wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                                const void *w_v, void *k_cache, void *v_cache,
                                int32_t n_tok, int32_t start_pos, int32_t cap,
                                int32_t d_in, int32_t n_kv_heads,
                                int32_t head_dim, double rope_base,
+                               void *workspace, size_t workspace_bytes,
                                void *stream);
+
+/* Workspace for wf_kv_only_prefill (0 when none is needed or for invalid
+ * arguments). */
+size_t wf_kv_only_prefill_workspace_bytes(wf_dtype_t dt, int32_t n_tok,
+                                          int32_t d_in, int32_t n_kv_heads,
+                                          int32_t head_dim);
 
 /* ------------------------------------------------------------------------
  * wf_lmhead_accept_entropy -- LM head, greedy acceptance and entropy route.

@@ -22,6 +22,7 @@ EXPORTED_SYMBOLS = (
     "wf_abi_version", "wf_status_string", "wf_verify_attn",
     "wf_verify_attn_workspace_bytes", "wf_kv_only_prefill",
     "wf_lmhead_accept_entropy", "wf_lmhead_workspace_bytes",
+    "wf_kv_only_prefill_workspace_bytes",
 )
 
 
@@ -49,8 +50,10 @@ def _load():
                                                    i32, i32]
     lib.wf_verify_attn_workspace_bytes.restype = sz
     lib.wf_kv_only_prefill.argtypes = [i32, p, p, p, p, p, i32, i32, i32, i32,
-                                       i32, i32, f64, p]
+                                       i32, i32, f64, p, sz, p]
     lib.wf_kv_only_prefill.restype = i32
+    lib.wf_kv_only_prefill_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
+    lib.wf_kv_only_prefill_workspace_bytes.restype = sz
     lib.wf_lmhead_accept_entropy.argtypes = [i32, p, p, p, p, i32, i32, i32,
                                              f32, p, p, p, p, sz, p]
     lib.wf_lmhead_accept_entropy.restype = i32
@@ -111,8 +114,11 @@ def wf_lmhead_workspace_bytes(gamma, vocab) -> int:
 
 
 def alloc_workspace(nbytes: int, device) -> torch.Tensor:
-    """Caller-owned scratch for the workspace arguments (16-byte aligned)."""
-    return torch.empty(max(16, (nbytes + 15) // 16 * 16), dtype=torch.uint8,
+    """Caller-owned scratch for the workspace arguments: 16-byte aligned and
+    zero-filled, as the calls require before a workspace's first use (each
+    call leaves its arrival counters at zero again, so one workspace serves
+    any number of calls that do not overlap in time)."""
+    return torch.zeros(max(16, (nbytes + 15) // 16 * 16), dtype=torch.uint8,
                        device=device)
 
 
@@ -142,17 +148,30 @@ def wf_verify_attn(q, k_cache, v_cache, out, ctx_len, softmax_scale=None,
     return out
 
 
+def wf_kv_only_prefill_workspace_bytes(dtype, n_tok, d_in, n_kv_heads,
+                                       head_dim) -> int:
+    code = dtype if isinstance(dtype, int) else (
+        WF_F32 if dtype == torch.float32 else WF_BF16)
+    return int(lib.wf_kv_only_prefill_workspace_bytes(code, n_tok, d_in,
+                                                      n_kv_heads, head_dim))
+
+
 def wf_kv_only_prefill(x, w_k, w_v, k_cache, v_cache, start_pos, rope_base,
-                       stream=None):
+                       workspace=None, stream=None):
     """x [n][d_in]; w_k, w_v [Hkv*D][d_in]; caches [Hkv][cap][D]."""
     n_tok, d_in = x.shape
     hkv, cap, dh = k_cache.shape
     code = _dtype_code(x)
+    need = wf_kv_only_prefill_workspace_bytes(code, n_tok, d_in, hkv, dh)
+    if workspace is None and need:
+        workspace = alloc_workspace(need, x.device)
     st = lib.wf_kv_only_prefill(code, _dev(x, "x"), _dev(w_k, "w_k"),
                                 _dev(w_v, "w_v"), _dev(k_cache, "k_cache"),
                                 _dev(v_cache, "v_cache"), n_tok,
                                 int(start_pos), cap, d_in, hkv, dh,
-                                float(rope_base), _stream(stream))
+                                float(rope_base), _dev(workspace, "workspace"),
+                                workspace.numel() if workspace is not None else 0,
+                                _stream(stream))
     _check(st, "wf_kv_only_prefill")
 
 

@@ -42,7 +42,7 @@ wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
 
 extern "C" {
 
-int32_t wf_abi_version(void) { return 1; }
+int32_t wf_abi_version(void) { return 3; }
 
 const char *wf_status_string(wf_status_t s) {
     switch (s) {
@@ -97,16 +97,15 @@ wf_status_t wf_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
                            workspace, static_cast<hipStream_t>(stream));
 }
 
-wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
-                               const void *w_v, void *k_cache, void *v_cache,
-                               int32_t n_tok, int32_t start_pos, int32_t cap,
-                               int32_t d_in, int32_t n_kv_heads,
-                               int32_t head_dim, double rope_base,
-                               void *stream) {
+namespace {
+wf_status_t check_prefill(wf_dtype_t dt, int n_tok, int start_pos, int cap,
+                          int d_in, int n_kv_heads, int head_dim,
+                          double rope_base) {
     if (!dtype_ok(dt))
         return WF_ERR_INVALID_ARG;
     if (n_tok < 0 || n_tok > kMaxPrefillTokens || start_pos < 0 ||
-        (long long)start_pos + n_tok > cap || d_in < 1 || n_kv_heads < 1)
+        (long long)start_pos + n_tok > cap || d_in < 1 || n_kv_heads < 1 ||
+        n_kv_heads > kMaxQHeads)
         return WF_ERR_INVALID_ARG;
     if (!std::isfinite(rope_base) || rope_base <= 0.0)
         return WF_ERR_INVALID_ARG;
@@ -114,6 +113,29 @@ wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
         return WF_ERR_UNSUPPORTED;
     if (dt == WF_BF16 && d_in % 32 != 0)
         return WF_ERR_UNSUPPORTED;
+    return WF_OK;
+}
+}  // namespace
+
+size_t wf_kv_only_prefill_workspace_bytes(wf_dtype_t dt, int32_t n_tok,
+                                          int32_t d_in, int32_t n_kv_heads,
+                                          int32_t head_dim) {
+    if (check_prefill(dt, n_tok, 0, n_tok, d_in, n_kv_heads, head_dim, 1.0) != WF_OK)
+        return 0;
+    return wf::prefill_workspace_bytes(dt, n_tok, d_in, n_kv_heads, head_dim);
+}
+
+wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
+                               const void *w_v, void *k_cache, void *v_cache,
+                               int32_t n_tok, int32_t start_pos, int32_t cap,
+                               int32_t d_in, int32_t n_kv_heads,
+                               int32_t head_dim, double rope_base,
+                               void *workspace, size_t workspace_bytes,
+                               void *stream) {
+    const wf_status_t st = check_prefill(dt, n_tok, start_pos, cap, d_in,
+                                         n_kv_heads, head_dim, rope_base);
+    if (st != WF_OK)
+        return st;
     if (n_tok == 0)
         return WF_OK;
     if (!x || !w_k || !w_v || !k_cache || !v_cache)
@@ -121,9 +143,12 @@ wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
     if (!aligned16(x) || !aligned16(w_k) || !aligned16(w_v) ||
         !aligned16(k_cache) || !aligned16(v_cache))
         return WF_ERR_INVALID_ARG;
+    const size_t need = wf::prefill_workspace_bytes(dt, n_tok, d_in, n_kv_heads, head_dim);
+    if (need && (!workspace || workspace_bytes < need || !aligned16(workspace)))
+        return WF_ERR_WORKSPACE;
     return wf::launch_prefill(dt, x, w_k, w_v, k_cache, v_cache, n_tok,
                               start_pos, cap, d_in, n_kv_heads, head_dim,
-                              rope_base, static_cast<hipStream_t>(stream));
+                              rope_base, workspace, static_cast<hipStream_t>(stream));
 }
 
 size_t wf_lmhead_workspace_bytes(int32_t gamma, int32_t vocab) {

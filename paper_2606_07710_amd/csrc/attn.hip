@@ -638,7 +638,7 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
 
 size_t attn_workspace_bytes(const AttnPlan &p, int gamma, int n_q_heads, int head_dim) {
     const size_t pairs = (size_t)gamma * n_q_heads;
-    return (size_t)p.splits * pairs * (head_dim + 2) * sizeof(float);
+    return kCounterBytes + (size_t)p.splits * pairs * (head_dim + 2) * sizeof(float);
 }
 
 wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
@@ -648,7 +648,7 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
                         hipStream_t stream) {
     AttnParams a{};
     const size_t pairs = (size_t)gamma * n_q_heads;
-    a.ws_acc = static_cast<float *>(workspace);
+    a.ws_acc = reinterpret_cast<float *>(static_cast<char *>(workspace) + kCounterBytes);
     a.ws_ml = a.ws_acc + (size_t)p.splits * pairs * head_dim;
     a.gamma = gamma;
     a.ctx_len = ctx_len;

@@ -12,9 +12,9 @@
 //   and stream W with a 4-deep prefetch; partial logits meet in LDS.
 //   fp32: plain VALU dot products.
 //   logits-only mode: the tile reads given fp32 logits.
-// Stage 2 (one workgroup): per row, merge the tile states in ascending tile
-// order, emit argmax and entropy, then the accept length, bonus token and
-// route.
+// Stage 2 (one workgroup per row): merge the row's tile states in a fixed
+// order and emit argmax and entropy; the last row to finish then emits the
+// accept length, bonus token and route.
 #include "wf_api_internal.h"
 #include "wf_device.h"
 
@@ -45,12 +45,75 @@ __device__ __forceinline__ void tile_states(const float (*zs)[kLmTile + 4],
     }
 }
 
+// Second kernel: workgroup r merges row r's tile states (thread t takes
+// tiles t, t + 256, ... in order, then a fixed butterfly across the wave and
+// the four waves in order) into argmax and entropy.  The last row workgroup
+// to arrive (device-scope ticket) applies greedy acceptance and the entropy
+// route; it resets the ticket counter for the next call.
+constexpr int kFinishThreads = 256;
+constexpr int kFinishBatch = 16;
+
+struct LmFinish {
+    RowState *states;        // [gamma][n_tiles]
+    unsigned *fcnt;          // ticket counter, zero between calls
+    const int32_t *draft;
+    int32_t *argmax_out;
+    float *entropy_out;
+    int32_t *accept_out;
+    int gamma, n_tiles;
+    float tau;
+};
+
+__global__ __launch_bounds__(kFinishThreads) void lm_finish_rows(LmFinish f) {
+    __shared__ RowState ws[kFinishThreads / kWave];
+    const int r = blockIdx.x;
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    const RowState *row = f.states + (size_t)r * f.n_tiles;
+    // batches of kFinishBatch loads in flight per thread (clamped addresses,
+    // masked merges), merged in ascending tile order
+    RowState s = state_empty();
+    for (int base = threadIdx.x; base < f.n_tiles; base += kFinishThreads * kFinishBatch) {
+        RowState buf[kFinishBatch];
+#pragma unroll
+        for (int b = 0; b < kFinishBatch; ++b)
+            buf[b] = row[min(base + b * kFinishThreads, f.n_tiles - 1)];
+#pragma unroll
+        for (int b = 0; b < kFinishBatch; ++b)
+            if (base + b * kFinishThreads < f.n_tiles)
+                s = state_merge(s, buf[b]);
+    }
+    s = wave_merge(s);
+    if (lane == 0)
+        ws[wave] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        RowState m = ws[0];
+#pragma unroll
+        for (int w = 1; w < kFinishThreads / kWave; ++w)
+            m = state_merge(m, ws[w]);
+        f.argmax_out[r] = m.a;
+        f.entropy_out[r] = state_entropy(m);
+    }
+    if (!arrive_last(f.fcnt, (unsigned)f.gamma))
+        return;
+    if (threadIdx.x == 0) {
+        int n = 0;
+        while (n < f.gamma - 1 && f.draft[n] == f.argmax_out[n])
+            ++n;
+        f.accept_out[0] = n;
+        f.accept_out[1] = f.argmax_out[n];
+        f.accept_out[2] = (f.entropy_out[n] > f.tau) ? 1 : 0;
+        *f.fcnt = 0u;
+    }
+}
+
 template <int NBL>
 __global__ __launch_bounds__(512) void lm_tiles_bf16(const uint16_t *__restrict__ h,
                                                      const uint16_t *__restrict__ w,
-                                                     RowState *__restrict__ states,
-                                                     int gamma, int d, int vocab,
-                                                     int n_tiles) {
+                                                     LmFinish f, int d, int vocab) {
+    RowState *states = f.states;
+    const int gamma = f.gamma, n_tiles = f.n_tiles;
     __shared__ __attribute__((aligned(16))) float zs[kMaxGamma][kLmTile + 4];
     const int tile = blockIdx.x;
     const int v0 = tile * kLmTile;
@@ -152,9 +215,9 @@ __global__ __launch_bounds__(512) void lm_tiles_bf16(const uint16_t *__restrict_
 
 __global__ __launch_bounds__(256) void lm_tiles_f32(const float *__restrict__ h,
                                                     const float *__restrict__ w,
-                                                    RowState *__restrict__ states,
-                                                    int gamma, int d, int vocab,
-                                                    int n_tiles) {
+                                                    LmFinish f, int d, int vocab) {
+    RowState *states = f.states;
+    const int gamma = f.gamma, n_tiles = f.n_tiles;
     constexpr int kRowsPerThread = kMaxGamma / 4;
     __shared__ __attribute__((aligned(16))) float zs[kMaxGamma][kLmTile + 4];
     const int tile = blockIdx.x;
@@ -187,14 +250,12 @@ __global__ __launch_bounds__(256) void lm_tiles_f32(const float *__restrict__ h,
 }
 
 __global__ __launch_bounds__(256) void lm_tiles_logits(const float *__restrict__ logits,
-                                                       RowState *__restrict__ states,
-                                                       int gamma, int vocab,
-                                                       int n_tiles) {
+                                                       LmFinish f, int vocab) {
     const int tile = blockIdx.x;
     const int v0 = tile * kLogitsTile;
     const int wave = threadIdx.x / kWave;
     const int lane = threadIdx.x % kWave;
-    for (int r = wave; r < gamma; r += 4) {
+    for (int r = wave; r < f.gamma; r += 4) {
         const float *row = logits + (size_t)r * vocab;
         RowState s = state_empty();
 #pragma unroll
@@ -205,44 +266,7 @@ __global__ __launch_bounds__(256) void lm_tiles_logits(const float *__restrict__
         }
         s = wave_merge(s);
         if (lane == 0)
-            states[(size_t)r * n_tiles + tile] = s;
-    }
-}
-
-__global__ __launch_bounds__(1024) void lm_finish(const RowState *__restrict__ states,
-                                                  int n_tiles,
-                                                  const int32_t *__restrict__ draft,
-                                                  int gamma, float tau,
-                                                  int32_t *__restrict__ argmax_out,
-                                                  float *__restrict__ entropy_out,
-                                                  int32_t *__restrict__ accept_out) {
-    __shared__ int32_t am[kMaxGamma];
-    __shared__ float ent[kMaxGamma];
-    const int wave = threadIdx.x / kWave;
-    const int lane = threadIdx.x % kWave;
-    const int n_waves = blockDim.x / kWave;
-    for (int r = wave; r < gamma; r += n_waves) {
-        const RowState *row = states + (size_t)r * n_tiles;
-        RowState s = state_empty();
-        for (int t = lane; t < n_tiles; t += kWave)
-            s = state_merge(s, row[t]);
-        s = wave_merge(s);
-        if (lane == 0) {
-            const float H = state_entropy(s);
-            argmax_out[r] = s.a;
-            entropy_out[r] = H;
-            am[r] = s.a;
-            ent[r] = H;
-        }
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int n = 0;
-        while (n < gamma - 1 && draft[n] == am[n])
-            ++n;
-        accept_out[0] = n;
-        accept_out[1] = am[n];
-        accept_out[2] = (ent[n] > tau) ? 1 : 0;
+            f.states[(size_t)r * f.n_tiles + tile] = s;
     }
 }
 
@@ -250,41 +274,49 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
+// The counter block at the workspace start holds the ticket counter; the
+// tile states (sized for the finest tiling) follow it.
 size_t lmhead_workspace_bytes(int gamma, int vocab) {
-    return (size_t)gamma * cdiv(vocab, kLmTile) * sizeof(RowState);
+    return kCounterBytes + (size_t)gamma * cdiv(vocab, kLmTile) * sizeof(RowState);
 }
+
 
 wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
                           const float *logits, const int32_t *draft, int gamma,
                           int d, int vocab, float tau, int32_t *argmax_out,
                           float *entropy_out, int32_t *accept_out,
                           void *workspace, hipStream_t stream) {
-    RowState *states = static_cast<RowState *>(workspace);
-    int n_tiles;
+    char *ws = static_cast<char *>(workspace);
+    LmFinish f;
+    f.states = reinterpret_cast<RowState *>(ws + kCounterBytes);
+    f.fcnt = reinterpret_cast<unsigned *>(ws);
+    f.draft = draft;
+    f.argmax_out = argmax_out;
+    f.entropy_out = entropy_out;
+    f.accept_out = accept_out;
+    f.gamma = gamma;
+    f.tau = tau;
     if (logits) {
-        n_tiles = cdiv(vocab, kLogitsTile);
-        lm_tiles_logits<<<n_tiles, 256, 0, stream>>>(logits, states, gamma, vocab, n_tiles);
+        f.n_tiles = cdiv(vocab, kLogitsTile);
+        lm_tiles_logits<<<f.n_tiles, 256, 0, stream>>>(logits, f, vocab);
     } else if (dt == WF_BF16) {
-        n_tiles = cdiv(vocab, kLmTile);
+        f.n_tiles = cdiv(vocab, kLmTile);
         const uint16_t *hb = static_cast<const uint16_t *>(h);
         const uint16_t *wb = static_cast<const uint16_t *>(w_lm);
         const int nbl = cdiv(gamma, 16);
         switch (nbl) {
-        case 1: lm_tiles_bf16<1><<<n_tiles, 512, 0, stream>>>(hb, wb, states, gamma, d, vocab, n_tiles); break;
-        case 2: lm_tiles_bf16<2><<<n_tiles, 512, 0, stream>>>(hb, wb, states, gamma, d, vocab, n_tiles); break;
-        case 3: lm_tiles_bf16<3><<<n_tiles, 512, 0, stream>>>(hb, wb, states, gamma, d, vocab, n_tiles); break;
-        default: lm_tiles_bf16<4><<<n_tiles, 512, 0, stream>>>(hb, wb, states, gamma, d, vocab, n_tiles); break;
+        case 1: lm_tiles_bf16<1><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, d, vocab); break;
+        case 2: lm_tiles_bf16<2><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, d, vocab); break;
+        case 3: lm_tiles_bf16<3><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, d, vocab); break;
+        default: lm_tiles_bf16<4><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, d, vocab); break;
         }
     } else {
-        n_tiles = cdiv(vocab, kLmTile);
-        lm_tiles_f32<<<n_tiles, 256, 0, stream>>>(static_cast<const float *>(h),
-                                                 static_cast<const float *>(w_lm),
-                                                 states, gamma, d, vocab, n_tiles);
+        f.n_tiles = cdiv(vocab, kLmTile);
+        lm_tiles_f32<<<f.n_tiles, 256, 0, stream>>>(static_cast<const float *>(h),
+                                                   static_cast<const float *>(w_lm),
+                                                   f, d, vocab);
     }
-    if (hipGetLastError() != hipSuccess)
-        return WF_ERR_HIP;
-    lm_finish<<<1, 1024, 0, stream>>>(states, n_tiles, draft, gamma, tau, argmax_out,
-                                      entropy_out, accept_out);
+    lm_finish_rows<<<gamma, kFinishThreads, 0, stream>>>(f);
     if (hipGetLastError() != hipSuccess)
         return WF_ERR_HIP;
     return WF_OK;

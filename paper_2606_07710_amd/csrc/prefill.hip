@@ -5,13 +5,13 @@
 //
 //   K[g][p+t] = RoPE(W_k[g] x_t, p+t),   V[g][p+t] = W_v[g] x_t
 //
-// bf16 path: one workgroup per (KV head, K or V, pair of 16-feature blocks
-// f and f + head_dim/2).  Pairing the two halves of the rotate-half RoPE in
-// one workgroup puts both elements of every rotation pair in the same lane
-// of the MFMA accumulators, so RoPE is a register-only epilogue.  Eight
-// waves split the input dimension; their partial sums meet in LDS in a fixed
-// order.  Tokens are the MFMA N dimension (blocks of 16, up to 64 per
-// launch row of the grid).
+// bf16 path: the work unit is (KV head, K or V, pair of 16-feature blocks f
+// and f + head_dim/2).  Pairing the two halves of the rotate-half RoPE puts
+// both elements of every rotation pair in the same lane of the MFMA
+// accumulators, so RoPE is a register epilogue.  The input dimension is
+// split across workgroups so a handful of units still spreads over the whole
+// chip; each slice writes an fp32 partial, and a second kernel sums the
+// slices in order, rotates and writes the cache rows.  Tokens are the MFMA N dimension (blocks of 16).
 // RoPE angles are formed in fp64: at positions ~65K an fp32 angle would be
 // off by ~4e-3 rad.
 #include "wf_api_internal.h"
@@ -21,8 +21,8 @@ namespace wf {
 
 namespace {
 
-constexpr int kPfWaves = 8;
-constexpr int kPfPrefetch = 4;
+constexpr int kPfMaxChunksPerWave = 8;   // 32-wide chunks per wave per k-slice
+constexpr int kPfTargetWorkgroups = 512;
 
 struct PrefillParams {
     const void *x;
@@ -32,6 +32,8 @@ struct PrefillParams {
     void *v_cache;
     int n_tok, start_pos, cap, d_in, n_kv_heads;
     double rope_base;
+    float *ws;                 // bf16 path: split-K partials
+    int chunks_per_split;      // 32-wide chunks of d_in per k-slice
 };
 
 __device__ __forceinline__ void rope_pair(float &lo, float &hi, int i, int dh,
@@ -46,17 +48,25 @@ __device__ __forceinline__ void rope_pair(float &lo, float &hi, int i, int dh,
     hi = b * cf + a * sf;
 }
 
+// Split-K: workgroup (unit, k-slice, token block) computes D[feature][token]
+// over its slice of the input dimension for the unit's two 16-feature blocks
+// (f and f + head_dim/2 of one head, K or V), writes the fp32 partial to
+// ws[unit][token block][kslice][2][16][TOK].
 template <int DH, int NBT>
-__global__ __launch_bounds__(512) void prefill_bf16(PrefillParams a) {
+__global__ __launch_bounds__(256) void prefill_partial_bf16(PrefillParams a) {
     constexpr int PAIRS = DH / 32;       // 16-feature block pairs per head
     constexpr int TOK = 16 * NBT;
-    __shared__ float zs[2][16][TOK + 1];
+    constexpr int WAVES = 4;
+    constexpr int MAXC = kPfMaxChunksPerWave;
+    __shared__ float zs[WAVES][2][16][TOK + 1];
 
     const int unit = blockIdx.x;         // (g, kind, pair)
+    const int ks = blockIdx.y;
+    const int tb = blockIdx.z;
     const int pair = unit % PAIRS;
     const int kind = (unit / PAIRS) % 2; // 0 = K, 1 = V
     const int g = unit / (2 * PAIRS);
-    const int t0 = blockIdx.y * TOK;
+    const int t0 = tb * TOK;
 
     const int wave = threadIdx.x / kWave;
     const int lane = threadIdx.x % kWave;
@@ -66,95 +76,101 @@ __global__ __launch_bounds__(512) void prefill_bf16(PrefillParams a) {
     const uint16_t *w = static_cast<const uint16_t *>(kind ? a.w_v : a.w_k);
     const uint16_t *x = static_cast<const uint16_t *>(a.x);
     const int f_lo = g * DH + 16 * pair;           // first feature, low half
-    const uint16_t *wp[2] = {
-        w + (size_t)(f_lo + m16) * a.d_in + c4 * 8,
-        w + (size_t)(f_lo + DH / 2 + m16) * a.d_in + c4 * 8};
+    const int c_begin = ks * a.chunks_per_split;   // 32-wide chunks of d_in
+    const uint16_t *wp0 = w + (size_t)(f_lo + m16) * a.d_in + c4 * 8;
+    const uint16_t *wp1 = w + (size_t)(f_lo + DH / 2 + m16) * a.d_in + c4 * 8;
     // Tokens past n_tok read the last token instead: they only feed MFMA
-    // output columns that are never stored, and nothing waits on a load early.
+    // output columns that are never stored.
     const uint16_t *xp[NBT];
 #pragma unroll
     for (int nb = 0; nb < NBT; ++nb)
         xp[nb] = x + (size_t)min(t0 + nb * 16 + m16, a.n_tok - 1) * a.d_in + c4 * 8;
 
+    // every load of this wave's chunks is issued before the first MFMA
+    bf16x8 wr[MAXC][2], xr[MAXC][NBT];
+#pragma unroll
+    for (int u = 0; u < MAXC; ++u) {
+        const int c = wave + WAVES * u;
+        if (c < a.chunks_per_split) {
+            const int off = (c_begin + c) * 32;
+            wr[u][0] = load_bf16x8(wp0 + off);
+            wr[u][1] = load_bf16x8(wp1 + off);
+#pragma unroll
+            for (int nb = 0; nb < NBT; ++nb)
+                xr[u][nb] = load_bf16x8(xp[nb] + off);
+        }
+    }
     f32x4 acc[2][NBT];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NBT; ++nb)
             acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int nchunks = a.d_in / 32;
-    const int cpw = (wave < nchunks) ? (nchunks - wave + kPfWaves - 1) / kPfWaves : 0;
-    bf16x8 wb[kPfPrefetch][2], xb[kPfPrefetch][NBT];
-    auto load_chunk = [&](int u, bf16x8 (&wr)[2], bf16x8 (&xr)[NBT]) {
-        const int off = (wave + kPfWaves * u) * 32;
-        wr[0] = load_bf16x8(wp[0] + off);
-        wr[1] = load_bf16x8(wp[1] + off);
 #pragma unroll
-        for (int nb = 0; nb < NBT; ++nb)
-            xr[nb] = load_bf16x8(xp[nb] + off);
-    };
-    auto mac = [&](const bf16x8 (&wr)[2], const bf16x8 (&xr)[NBT]) {
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int nb = 0; nb < NBT; ++nb)
-                acc[mb][nb] = mfma16x16x32(wr[mb], xr[nb], acc[mb][nb]);
-    };
-    // Branch-free steady state (exact wait counting, kPfPrefetch chunks in
-    // flight), peeled last group, then any remainder chunks.
-    const int ngroups = cpw / kPfPrefetch;
-    if (ngroups > 0) {
-#pragma unroll
-        for (int p = 0; p < kPfPrefetch; ++p) {
-            load_chunk(p, wb[p], xb[p]);
-            __builtin_amdgcn_sched_barrier(0);   // issue chunk by chunk
-        }
-        for (int gi = 0; gi < ngroups - 1; ++gi) {
-#pragma unroll
-            for (int p = 0; p < kPfPrefetch; ++p) {
-                mac(wb[p], xb[p]);
-                load_chunk((gi + 1) * kPfPrefetch + p, wb[p], xb[p]);
-                // keep each refill right behind the MFMAs that free its
-                // registers, so kPfPrefetch chunks stay in flight
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-#pragma unroll
-        for (int p = 0; p < kPfPrefetch; ++p)
-            mac(wb[p], xb[p]);
-    }
-    for (int u = ngroups * kPfPrefetch; u < cpw; ++u) {
-        load_chunk(u, wb[0], xb[0]);
-        mac(wb[0], xb[0]);
-    }
-
-    // lane (m16, c4) holds D[feature 4*c4 + i][token nb*16 + m16]
-#pragma unroll 1
-    for (int ww = 0; ww < kPfWaves; ++ww) {
-        if (wave == ww) {
+    for (int u = 0; u < MAXC; ++u) {
+        if (wave + WAVES * u < a.chunks_per_split) {
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                 for (int nb = 0; nb < NBT; ++nb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        float &dst = zs[mb][4 * c4 + i][nb * 16 + m16];
-                        dst = (ww > 0) ? dst + acc[mb][nb][i] : acc[mb][nb][i];
-                    }
+                    acc[mb][nb] = mfma16x16x32(wr[u][mb], xr[u][nb], acc[mb][nb]);
         }
-        __syncthreads();
+    }
+    // lane (m16, c4) holds D[feature 4*c4 + i][token nb*16 + m16]
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBT; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                zs[wave][mb][4 * c4 + i][nb * 16 + m16] = acc[mb][nb][i];
+    __syncthreads();
+    // sum the waves in a fixed order and write the partial
+    const int ksplit = gridDim.y;
+    const size_t ub = (size_t)unit * gridDim.z + tb;           // (unit, token block)
+    float *part = a.ws + ub * ksplit * (2 * 16 * TOK);
+    float *dst = part + (size_t)ks * (2 * 16 * TOK);
+    for (int idx = threadIdx.x; idx < 2 * 16 * TOK; idx += blockDim.x) {
+        const int mb = idx / (16 * TOK);
+        const int e = (idx / TOK) % 16;
+        const int tl = idx % TOK;
+        float v = zs[0][mb][e][tl];
+#pragma unroll
+        for (int ww = 1; ww < WAVES; ++ww)
+            v += zs[ww][mb][e][tl];
+        dst[idx] = v;
     }
 
-    // epilogue: thread per (feature e of the block, token)
+    // The last k-slice workgroup of this (unit, token block) to finish sums
+    // the slices in slice order, applies RoPE to K and writes the cache rows.
+}
+
+// Workgroup (unit, token block) sums the unit's k-slice partials in slice
+// order, applies RoPE to K and writes the cache rows.
+template <int DH, int NBT>
+__global__ __launch_bounds__(256) void prefill_finish_bf16(PrefillParams a, int ksplit) {
+    constexpr int PAIRS = DH / 32;
+    constexpr int TOK = 16 * NBT;
+    const int unit = blockIdx.x;
+    const int tb = blockIdx.y;
+    const int pair = unit % PAIRS;
+    const int kind = (unit / PAIRS) % 2;
+    const int g = unit / (2 * PAIRS);
+    const int t0 = tb * TOK;
+    const size_t ub = (size_t)unit * gridDim.y + tb;
+    const float *part = a.ws + ub * ksplit * (2 * 16 * TOK);
     uint16_t *cache = static_cast<uint16_t *>(kind ? a.v_cache : a.k_cache);
     for (int idx = threadIdx.x; idx < 16 * TOK; idx += blockDim.x) {
-        const int e = idx % 16;
-        const int tl = idx / 16;
+        const int e = idx / TOK;
+        const int tl = idx % TOK;
         const int t = t0 + tl;
         if (t >= a.n_tok)
             continue;
-        float lo = zs[0][e][tl], hi = zs[1][e][tl];
+        float lo = 0.f, hi = 0.f;
+        for (int k = 0; k < ksplit; ++k) {
+            lo += part[k * (2 * 16 * TOK) + e * TOK + tl];
+            hi += part[k * (2 * 16 * TOK) + 16 * TOK + e * TOK + tl];
+        }
         const int pos = a.start_pos + t;
         if (kind == 0)
             rope_pair(lo, hi, 16 * pair + e, DH, pos, a.rope_base);
@@ -196,21 +212,47 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
+PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim) {
+    PrefillPlan p{};
+    p.nbt = std::min(4, std::max(1, cdiv(n_tok, 16)));
+    p.token_blocks = std::max(1, cdiv(n_tok, 16 * p.nbt));
+    p.units = n_kv_heads * 2 * (head_dim / 32);
+    const int chunks = d_in / 32;
+    // enough k-slices to cover the chip, each wave owning 1..8 chunks
+    int ks = std::max(1, cdiv(kPfTargetWorkgroups, p.units * p.token_blocks));
+    ks = std::min(ks, std::max(1, chunks / 4));                   // >= 4 chunks per slice
+    ks = std::max(ks, cdiv(chunks, 4 * kPfMaxChunksPerWave));    // <= 32 chunks per slice
+    p.chunks_per_split = cdiv(chunks, ks);
+    p.ksplit = cdiv(chunks, p.chunks_per_split);
+    return p;
+}
+
+size_t prefill_workspace_bytes(wf_dtype_t dt, int n_tok, int d_in, int n_kv_heads,
+                               int head_dim) {
+    if (dt != WF_BF16 || n_tok == 0)
+        return 0;
+    const PrefillPlan p = plan_prefill(n_tok, d_in, n_kv_heads, head_dim);
+    const size_t part = (size_t)p.units * p.token_blocks * p.ksplit * 2 * 16 * (16 * p.nbt) * sizeof(float);
+    return kCounterBytes + part;
+}
+
 wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            const void *w_v, void *k_cache, void *v_cache,
                            int n_tok, int start_pos, int cap, int d_in,
                            int n_kv_heads, int head_dim, double rope_base,
-                           hipStream_t stream) {
+                           void *workspace, hipStream_t stream) {
     PrefillParams a{x, w_k, w_v, k_cache, v_cache, n_tok, start_pos, cap, d_in,
-                    n_kv_heads, rope_base};
+                    n_kv_heads, rope_base, nullptr, 0};
     if (dt == WF_BF16) {
-        const int nbt = std::min(4, cdiv(n_tok, 16));
-        const int tok_per_row = 16 * nbt;
-        dim3 grid(n_kv_heads * 2 * (head_dim / 32), cdiv(n_tok, tok_per_row));
-        dim3 block(512);
-#define WF_PF_CASE(DHV, NBV)                                        \
-    if (head_dim == DHV && nbt == NBV) {                            \
-        prefill_bf16<DHV, NBV><<<grid, block, 0, stream>>>(a);      \
+        const PrefillPlan p = plan_prefill(n_tok, d_in, n_kv_heads, head_dim);
+        a.chunks_per_split = p.chunks_per_split;
+        a.ws = reinterpret_cast<float *>(static_cast<char *>(workspace) + kCounterBytes);
+        dim3 grid(p.units, p.ksplit, p.token_blocks), block(256);
+        dim3 fgrid(p.units, p.token_blocks);
+#define WF_PF_CASE(DHV, NBV)                                                        \
+    if (head_dim == DHV && p.nbt == NBV) {                                          \
+        prefill_partial_bf16<DHV, NBV><<<grid, block, 0, stream>>>(a);              \
+        prefill_finish_bf16<DHV, NBV><<<fgrid, block, 0, stream>>>(a, p.ksplit);    \
     } else
         WF_PF_CASE(128, 1) WF_PF_CASE(128, 2) WF_PF_CASE(128, 3) WF_PF_CASE(128, 4)
         WF_PF_CASE(64, 1) WF_PF_CASE(64, 2) WF_PF_CASE(64, 3) WF_PF_CASE(64, 4)

@@ -12,6 +12,13 @@
 
 namespace wf {
 
+// Every workspace starts with a fixed block of arrival counters (the same
+// offset and size for the three kinds of call), followed by that call's
+// partial results.  Calls leave the counters at zero, so a workspace zeroed
+// once can be reused by any later call, whatever its kind or sizes.
+constexpr size_t kCounterBytes = 65536;
+constexpr int kCounterSlots = static_cast<int>(kCounterBytes / sizeof(unsigned));
+
 struct AttnPlan {
     int rows;            // G * gamma query rows per KV head
     int nb;              // 16-row blocks per wave (bf16 path)
@@ -39,10 +46,21 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
                           float *entropy_out, int32_t *accept_out,
                           void *workspace, hipStream_t stream);
 
+struct PrefillPlan {
+    int nbt;             // 16-token blocks per workgroup
+    int token_blocks;    // workgroups along the tokens
+    int units;           // (kv head, K|V, RoPE block pair) work units
+    int ksplit;          // slices of the input dimension
+    int chunks_per_split;
+};
+
+PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim);
+size_t prefill_workspace_bytes(wf_dtype_t dt, int n_tok, int d_in, int n_kv_heads,
+                               int head_dim);
 wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            const void *w_v, void *k_cache, void *v_cache,
                            int n_tok, int start_pos, int cap, int d_in,
                            int n_kv_heads, int head_dim, double rope_base,
-                           hipStream_t stream);
+                           void *workspace, hipStream_t stream);
 
 }  // namespace wf

@@ -143,4 +143,34 @@ __device__ __forceinline__ float state_entropy(RowState s) {
     return log1pf(s.sp) - s.t / (1.f + s.sp);
 }
 
+// Halves of a device-scope fence.
+__device__ __forceinline__ void fence_release_agent() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+}
+__device__ __forceinline__ void fence_acquire_agent() {
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// "Last workgroup to arrive finishes the reduction": every workgroup calls
+// this once its results are stored; it returns true (uniformly within the
+// workgroup) in the one workgroup that draws the last of `expected` tickets
+// from *counter, and that workgroup then sees every other workgroup's stored
+// results.  The workgroup barrier orders all threads' stores before thread
+// 0's device-scope release, so the L2 write-back runs once per workgroup,
+// and only the last workgroup pays for the acquire.  The caller resets the
+// counter to zero when it is done.
+__device__ __forceinline__ bool arrive_last(unsigned *counter, unsigned expected) {
+    __shared__ int last;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        fence_release_agent();
+        const bool l = atomicAdd(counter, 1u) == expected - 1u;
+        if (l)
+            fence_acquire_agent();
+        last = l;
+    }
+    __syncthreads();
+    return last != 0;
+}
+
 }  // namespace wf

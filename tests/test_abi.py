@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert wf.abi_version() == 1
+    assert wf.abi_version() == 3
     assert wf.status_string(wf.WF_OK) == "ok"
     assert "workspace" in wf.status_string(wf.WF_ERR_WORKSPACE)
     assert wf.status_string(99) == "unknown status"
@@ -67,34 +67,49 @@ def test_verify_attn_rejects(kw, status):
     assert _attn(**kw) == status
 
 
+# every workspace starts with the same block of arrival counters
+COUNTER_BLOCK = 65536
+
+
 def test_workspace_query():
     need = wf.wf_verify_attn_workspace_bytes(1, 16, 32768, 32, 8, 128)
     assert need > 0 and need % 4 == 0
     assert wf.wf_verify_attn_workspace_bytes(1, 0, 32768, 32, 8, 128) == 0
     forced = wf.wf_verify_attn_workspace_bytes(1, 16, 32768, 32, 8, 128, 7)
-    assert forced == 7 * 16 * 32 * 130 * 4
-    assert wf.wf_lmhead_workspace_bytes(16, 151936) == 16 * 2374 * 16
+    assert forced == COUNTER_BLOCK + 7 * 16 * 32 * 130 * 4
+    # counter block, then one 16-byte row state per (row, 64-entry tile)
+    assert wf.wf_lmhead_workspace_bytes(16, 151936) == COUNTER_BLOCK + 16 * 2374 * 16
     assert wf.wf_lmhead_workspace_bytes(0, 10) == 0
 
 
 def _prefill(**kw):
     a = dict(dt=1, x=FAKE, wk=FAKE, wv=FAKE, kc=FAKE, vc=FAKE, n=16, start=10,
-             cap=26, d_in=4096, hkv=8, dh=128, base=1e6)
+             cap=26, d_in=4096, hkv=8, dh=128, base=1e6, ws=FAKE,
+             ws_bytes=1 << 30)
     a.update(kw)
     return wf.lib.wf_kv_only_prefill(a["dt"], a["x"], a["wk"], a["wv"],
                                      a["kc"], a["vc"], a["n"], a["start"],
                                      a["cap"], a["d_in"], a["hkv"], a["dh"],
-                                     a["base"], None)
+                                     a["base"], a["ws"], a["ws_bytes"], None)
 
 
 @pytest.mark.parametrize("kw,status", [
     (dict(x=None), 1), (dict(vc=None), 1), (dict(n=-1), 1),
     (dict(cap=25), 1), (dict(start=-2), 1), (dict(dh=80), 2),
     (dict(d_in=100), 2), (dict(base=0.0), 1), (dict(hkv=0), 1),
-    (dict(kc=ODD), 1), (dict(n=5000, cap=6000), 1),
+    (dict(kc=ODD), 1), (dict(n=5000, cap=6000), 1), (dict(ws=None), 3),
+    (dict(ws_bytes=64), 3), (dict(ws=ODD), 3),
 ])
 def test_prefill_rejects(kw, status):
     assert _prefill(**kw) == status
+
+
+def test_prefill_workspace_query():
+    need = wf.wf_kv_only_prefill_workspace_bytes(1, 16, 4096, 8, 128)
+    assert need > 0 and need % 16 == 0
+    assert wf.wf_kv_only_prefill_workspace_bytes(0, 16, 4096, 8, 128) == 0
+    assert wf.wf_kv_only_prefill_workspace_bytes(1, 0, 4096, 8, 128) == 0
+    assert wf.wf_kv_only_prefill_workspace_bytes(1, 16, 100, 8, 128) == 0
 
 
 def test_prefill_zero_tokens_is_a_noop():
