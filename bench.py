@@ -40,6 +40,10 @@ def parse():
                          "gamma 16, 16 catch-up tokens)")
     ap.add_argument("--graph", action="store_true",
                     help="replay the step as one captured HIP graph")
+    ap.add_argument("--serial", action="store_true",
+                    help="issue every call on one stream (default: the "
+                         "catch-up prefill runs on a second stream, "
+                         "concurrently with the verification attention)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0,
                     help="approximate seconds of oracle work for cpu_baseline")
@@ -64,11 +68,20 @@ class Step:
         self.outs, self.lmouts, self.draft, self.tau = outs, lmouts, draft, tau
         self.ws_attn, self.ws_pre, self.ws_lm, self.wf = ws_attn, ws_pre, ws_lm, wf
 
-    def build(self, stream_ptr):
+    def build(self, stream, catchup=None):
+        """Marshal every call for `stream`; with `catchup` (a second stream),
+        the KV-only prefill calls go there and run concurrently with the
+        verification attention: they write disjoint cache rows and read
+        nothing the attention writes."""
+        import torch
         w, wf = self.w, self.wf
         P = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
         code = wf.WF_BF16 if w.dtype == "bf16" else wf.WF_F32
-        s = ctypes.c_void_p(stream_ptr)
+        s = ctypes.c_void_p(stream.cuda_stream)
+        s2 = ctypes.c_void_p((catchup or stream).cuda_stream)
+        self.stream, self.catchup = stream, catchup
+        self.fork = torch.cuda.Event()
+        self.join = torch.cuda.Event()
         self.attn = []
         self.pre = []
         for l, t in enumerate(self.layers):
@@ -84,7 +97,7 @@ class Step:
                                  P(vc), w.n_prefill, w.prefill_start,
                                  kc.shape[1], w.hidden, w.n_kv_heads,
                                  w.head_dim, w.rope_base, P(self.ws_pre),
-                                 self.ws_pre.numel(), s))
+                                 self.ws_pre.numel(), s2))
         am, ent, acc = self.lmouts[0]
         self.lm = [(code, P(self.head["h"]), P(self.head["w_lm"]), None,
                     P(self.draft), w.gamma, w.hidden, w.vocab, self.tau, P(am),
@@ -98,25 +111,38 @@ class Step:
 
     def run(self, check=False):
         lib = self.wf.lib
-        for a in self.attn:
+        if self.catchup is not None:
+            self.fork.record(self.stream)
+            self.catchup.wait_event(self.fork)
+        for l, a in enumerate(self.attn):
             rc = lib.wf_verify_attn(*a)
             if check and rc:
                 raise RuntimeError(f"wf_verify_attn: {self.wf.status_string(rc)}")
-        for a in self.pre:
-            rc = lib.wf_kv_only_prefill(*a)
-            if check and rc:
-                raise RuntimeError(f"wf_kv_only_prefill: {self.wf.status_string(rc)}")
+            if self.catchup is not None and l < len(self.pre):
+                rc = lib.wf_kv_only_prefill(*self.pre[l])
+                if check and rc:
+                    raise RuntimeError(f"wf_kv_only_prefill: {self.wf.status_string(rc)}")
+        if self.catchup is None:
+            for a in self.pre:
+                rc = lib.wf_kv_only_prefill(*a)
+                if check and rc:
+                    raise RuntimeError(f"wf_kv_only_prefill: {self.wf.status_string(rc)}")
+        else:
+            self.join.record(self.catchup)
+            self.stream.wait_event(self.join)
         for a in self.lm:
             rc = lib.wf_lmhead_accept_entropy(*a)
             if check and rc:
                 raise RuntimeError(f"wf_lmhead_accept_entropy: {self.wf.status_string(rc)}")
 
     def phases(self):
-        """(name, C function, argument tuples) of the step's three phases."""
+        """(name, C function, argument tuples, stream) of the step's three
+        phases."""
         lib = self.wf.lib
-        return [("attention", lib.wf_verify_attn, self.attn),
-                ("prefill", lib.wf_kv_only_prefill, self.pre),
-                ("lmhead", lib.wf_lmhead_accept_entropy, self.lm)]
+        return [("attention", lib.wf_verify_attn, self.attn, self.stream),
+                ("prefill", lib.wf_kv_only_prefill, self.pre,
+                 self.catchup or self.stream),
+                ("lmhead", lib.wf_lmhead_accept_entropy, self.lm, self.stream)]
 
 
 def cpu_baseline(w, layers, head, budget_s, max_layers=None):
@@ -236,7 +262,8 @@ def main():
     step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_pre,
                 ws_lm, wf)
     stream = torch.cuda.current_stream()
-    step.build(stream.cuda_stream)
+    catchup = None if args.serial else torch.cuda.Stream()
+    step.build(stream, catchup)
     step.run(check=True)
     torch.cuda.synchronize()
     log(f"step ok: accept {tuple(acc.tolist())} (expected n = {k})")
@@ -246,13 +273,13 @@ def main():
         graph = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
         with torch.cuda.stream(side):
-            step.build(side.cuda_stream)
+            step.build(side, catchup)
             step.run(check=True)
         torch.cuda.synchronize()
         with torch.cuda.graph(graph):
-            step.build(torch.cuda.current_stream().cuda_stream)
+            step.build(torch.cuda.current_stream(), catchup)
             step.run(check=True)
-        step.build(stream.cuda_stream)
+        step.build(stream, catchup)
         torch.cuda.synchronize()
 
     def one_step():
@@ -285,8 +312,9 @@ def main():
     # Events bracket only whole runs of one kind of call, so a per-call
     # average includes no event overhead and matches what a kernel trace
     # reports for the kernels of that call.
+    # (on the stream each phase's calls are marshalled for)
     per_call_ms = {}
-    for name, fn, calls in step.phases():
+    for name, fn, calls, st in step.phases():
         if not calls:
             per_call_ms[name] = 0.0
             continue
@@ -295,16 +323,16 @@ def main():
         a_ev = torch.cuda.Event(enable_timing=True)
         b_ev = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        a_ev.record()
+        a_ev.record(st)
         for _ in range(args.steps):
             for a in calls:
                 fn(*a)
-        b_ev.record()
+        b_ev.record(st)
         torch.cuda.synchronize()
         per_call_ms[name] = a_ev.elapsed_time(b_ev) / (args.steps * len(calls))
     attn_avg_ms = per_call_ms["attention"]
     breakdown = {name: round(per_call_ms[name] * len(calls) * 1e3, 1)
-                 for name, _, calls in step.phases()}
+                 for name, _, calls, _ in step.phases()}
     log(f"per call (us): " + ", ".join(f"{k} {v * 1e3:.2f}"
                                        for k, v in per_call_ms.items()))
 
@@ -348,10 +376,12 @@ def main():
                    "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
                    "ctx_len": w.ctx_len, "gamma": w.gamma,
                    "catch_up_tokens": w.n_prefill, "vocab": w.vocab,
-                   "graph": bool(graph is not None)},
+                   "graph": bool(graph is not None),
+                   "schedule": "serial" if catchup is None else
+                               "catch-up prefill on a second stream"},
         "step_hbm_gbps": round(step_gbps, 1),
         "step_algorithmic_bytes": by["total"],
-        "breakdown_us": breakdown,
+        "breakdown_us": breakdown,   # each phase run alone, back to back
         "roofline": {
             "kernel": "wf_verify_attn, one layer (attn_partial_bf16 + attn_merge)",
             "bound": "hbm",

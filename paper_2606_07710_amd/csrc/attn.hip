@@ -80,7 +80,37 @@ struct TileGeom {
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 #define WF_LDS(T) __attribute__((address_space(3))) T
 
-template <int DH, int NBW, int RG, int KS>
+template <int N>
+using ic = std::integral_constant<int, N>;
+
+// 32-bit LDS byte address of a __shared__ object.
+__device__ __forceinline__ unsigned lds_addr(const void *p) {
+    return (unsigned)(uintptr_t)(const WF_LDS(char) *)p;
+}
+
+// s_waitcnt vmcnt(n) for the few counts the pipeline needs (n must be a
+// compile-time immediate).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt immediate out of range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// HBM -> LDS copy of 16 bytes per lane: lane L's 16 bytes at `src` land at
+// LDS byte lds + 16*L (lds wave-uniform).  Written as inline assembly so
+// the compiler does not know these loads write LDS: it would otherwise make
+// every LDS read wait for all of them.  Completion is tracked by the
+// explicit vmcnt waits of the pipeline.
+__device__ __forceinline__ void lds_dma16(const void *src, unsigned lds) {
+    asm volatile("s_mov_b32 m0, %1\n\t"
+                 "s_nop 0\n\t"
+                 "global_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(src), "s"(lds)
+                 : "memory", "m0");
+}
+
+template <int DH, int NBW, int RG, int KS, int NBUF>
 __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) {
     using TG = TileGeom<DH>;
     constexpr int KC = DH / 32;
@@ -88,24 +118,42 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     constexpr int ROWS_W = 16 * NBW;
     constexpr int ROWS_WG = ROWS_W * RG;
     constexpr int NLOAD = 2 * TG::kLoadsPerHalf;      // wave loads per tile
+    constexpr int LPW = NLOAD / RG;                   // loads per wave per stage
+    static_assert(NLOAD % RG == 0, "tile loads must split evenly over row groups");
+    static_assert(NBUF >= 2 && NBUF <= 4, "ring depth 2..4");
+    constexpr int STAGE_BYTES = KS * TG::kTileBytes;  // one tile per stream
 
-    // Stream-merge regions at the end reuse the ring: region 0 in ring0,
-    // region 1 (when KS > 2) in ring1.  Rows are padded by 4 floats so the
-    // 16 rows of a wave's accumulator tile fall in distinct banks.
+    // Stream-merge regions at the end reuse ring buffers 0 and 1.  Rows are
+    // padded by 4 floats so the 16 rows of a wave's accumulator tile fall in
+    // distinct banks.
     constexpr int OST = DH + 4;
-    constexpr int NREG = KS / 2;
-    constexpr int RING_BYTES = KS * TG::kTileBytes;
+    constexpr int NREG = KS >= 4 ? 2 : 1;
     constexpr int REGION_BYTES = ROWS_WG * OST * 4;
-    constexpr int RING0_BYTES = RING_BYTES > REGION_BYTES ? RING_BYTES : REGION_BYTES;
-    constexpr int RING1_BYTES = (NREG < 2 || RING_BYTES > REGION_BYTES) ? RING_BYTES : REGION_BYTES;
-    // two ring halves as separate objects, so reads of one never wait on the
-    // in-flight LDS-DMA writes into the other
+    constexpr int RING0_BYTES = STAGE_BYTES > REGION_BYTES ? STAGE_BYTES : REGION_BYTES;
+    constexpr int RING1_BYTES = NREG < 2 ? STAGE_BYTES : RING0_BYTES;
+    static_assert(RING0_BYTES + RING1_BYTES + (NBUF - 2) * STAGE_BYTES +
+                  KS * ROWS_WG * 8 + 16 <= 160 * 1024, "LDS budget");
+    // The ring buffers are separate objects, so the compiler can tell reads
+    // of one buffer from the LDS-DMA writes still landing in the others.
     __shared__ __attribute__((aligned(1024))) char ring0[RING0_BYTES];
     __shared__ __attribute__((aligned(1024))) char ring1[RING1_BYTES];
+    __shared__ __attribute__((aligned(1024))) char ring2[NBUF > 2 ? STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) char ring3[NBUF > 3 ? STAGE_BYTES : 16];
     __shared__ float mls[KS][ROWS_WG][2];
     __shared__ int overflow;
     if (threadIdx.x == 0)
         overflow = 0;                        // published by the first barrier
+    auto ring = [&](auto bi) -> char * {
+        constexpr int B = decltype(bi)::value;
+        if constexpr (B == 0)
+            return ring0;
+        else if constexpr (B == 1)
+            return ring1;
+        else if constexpr (B == 2)
+            return ring2;
+        else
+            return ring3;
+    };
 
     // ---- which (kv head, split, row group) this workgroup owns -------------
     int unit, rgw;
@@ -124,7 +172,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     const int g = unit % a.n_kv_heads;
     const int split = unit / a.n_kv_heads;
 
-    const int wave = threadIdx.x / kWave;
+    const int wave = wave_id();
     const int lane = threadIdx.x % kWave;
     const int m16 = lane & 15;
     const int c4 = lane >> 4;
@@ -145,14 +193,18 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     const char *kg = reinterpret_cast<const char *>(a.k16 + head_off);
     const char *vg = reinterpret_cast<const char *>(a.v16 + head_off);
 
-    // Issue this wave's share of the loads of tile t into one ring slot.
-    // Load j < kLoadsPerHalf fills K rows, the rest V rows; lane L of load j
-    // writes LDS bytes 16*(64*j' + L) of its half (j' = j mod kLoadsPerHalf).
-    auto issue = [&](char *ring, int t) {
+    // Issue this wave's LPW loads of its stream's tile of stage `st` into
+    // ring buffer `bi`.  Load j < kLoadsPerHalf fills K rows, the rest V
+    // rows; lane L of load j writes LDS bytes 16*(64*j' + L) of its half
+    // (j' = j mod kLoadsPerHalf).  A stream whose tile lies past the split
+    // (ragged last stage) loads the split's last tile again, so every wave
+    // issues the same number of loads per stage; that copy is never used.
+    auto issue = [&](auto bi, int st) __attribute__((always_inline)) {
+        const int t = min(KS * st + stream, n_tiles - 1);
         const int kb = k_begin + t * kTileKeys;
-        char *slot = ring + stream * TG::kTileBytes;
+        const unsigned slot = lds_addr(ring(bi)) + stream * TG::kTileBytes;
 #pragma unroll
-        for (int jr = 0; jr < NLOAD / RG; ++jr) {
+        for (int jr = 0; jr < LPW; ++jr) {
             const int j = rgi + jr * RG;
             const bool is_v = j >= TG::kLoadsPerHalf;
             const int jj = is_v ? j - TG::kLoadsPerHalf : j;
@@ -168,47 +220,53 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             }
             const int key = min(kb + kl, last_key);
             const char *src = (is_v ? vg : kg) + (size_t)key * TG::kRowBytes + lg * 16;
-            char *dst = slot + (is_v ? TG::kHalfBytes : 0) + jj * 1024;
-            __builtin_amdgcn_global_load_lds(
-                (__attribute__((address_space(1))) void *)src,
-                (WF_LDS(void) *)dst, 16, 0, 0);
+            lds_dma16(src, slot + (is_v ? TG::kHalfBytes : 0) + jj * 1024);
         }
     };
-
-    // the first tiles start streaming before anything else
-    if (stream < n_tiles)
-        issue(ring0, stream);
 
     // ---- Q^T operands and causal limits of this wave's rows ------------------
     const int row0 = rgw * ROWS_WG + rgi * ROWS_W;
     bf16x8 qf[NBW][KC];
     int lim[NBW];
+    auto load_q = [&]() {
 #pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) {
-        const int r = row0 + nb * 16 + m16;
-        const int rc = min(r, a.rows - 1);
-        const int i = rc / a.group;
-        const int h = g * a.group + (rc % a.group);
-        const uint16_t *qp = a.q16 + ((size_t)i * a.n_q_heads + h) * DH + c4 * 8;
+        for (int nb = 0; nb < NBW; ++nb) {
+            const int r = row0 + nb * 16 + m16;
+            const int rc = min(r, a.rows - 1);
+            const int i = rc / a.group;
+            const int h = g * a.group + (rc % a.group);
+            const uint16_t *qp = a.q16 + ((size_t)i * a.n_q_heads + h) * DH + c4 * 8;
 #pragma unroll
-        for (int kk = 0; kk < KC; ++kk)
-            qf[nb][kk] = load_bf16x8(qp + kk * 32);
-        // padding rows (r >= rows) reuse a real row's query and are never
-        // stored; they must not be masked harder than it
-        lim[nb] = a.ctx_len + i;
-    }
+            for (int kk = 0; kk < KC; ++kk)
+                qf[nb][kk] = load_bf16x8(qp + kk * 32);
+            // padding rows (r >= rows) reuse a real row's query and are never
+            // stored; they must not be masked harder than it
+            lim[nb] = a.ctx_len + i;
+        }
+    };
 
     f32x4 o[MD][NBW];
     float mref[NBW], lrow[NBW];
 
-    // V^T operands of a tile: two transposing LDS reads per 16 dims.  They
-    // are issued before the next step's DMA, because the compiler cannot
-    // tell a transposing read from a write still in flight and would wait
-    // for every outstanding load in front of it.
-    auto read_vt = [&](auto ring_tag, bf16x8 (&vop)[MD]) {
-        constexpr bool ODD = decltype(ring_tag)::value;
-        WF_LDS(const char) *vt = (WF_LDS(const char) *)(ODD ? ring1 : ring0)
-                                 + stream * TG::kTileBytes + TG::kHalfBytes;
+    // Operands of a tile from LDS:
+    //   K: ds_read_b128 of (key 16*mb + m16, granule 4*kk + c4).
+    //   V^T: two transposing reads per 16 dims.
+    auto read_k = [&](auto bi, bf16x8 (&kop)[2][KC]) __attribute__((always_inline)) {
+        const WF_LDS(char) *kt = (const WF_LDS(char) *)ring(bi) + stream * TG::kTileBytes;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const int kl = 16 * mb + m16;
+#pragma unroll
+            for (int kk = 0; kk < KC; ++kk) {
+                const int pg = (4 * kk + c4) ^ (kl & (TG::kGran - 1));
+                kop[mb][kk] = __builtin_bit_cast(
+                    bf16x8, *(const WF_LDS(u32x4) *)(kt + kl * TG::kRowBytes + pg * 16));
+            }
+        }
+    };
+    auto read_vt = [&](auto bi, bf16x8 (&vop)[MD]) __attribute__((always_inline)) {
+        const WF_LDS(char) *vt = (const WF_LDS(char) *)ring(bi) + stream * TG::kTileBytes +
+                                 TG::kHalfBytes;
         const int q4 = m16 & 3, qk = m16 >> 2;
 #pragma unroll
         for (int md = 0; md < MD; ++md) {
@@ -217,8 +275,8 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             for (int hh = 0; hh < 2; ++hh) {
                 const int kl = 16 * hh + 4 * c4 + qk;
                 const int ps = md ^ (kl & (TG::kSegs - 1));
-                WF_LDS(const char) *src = vt + kl * TG::kRowBytes + ps * 32 + q4 * 8;
-                half[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((WF_LDS(v4i16) *)src);
+                half[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (WF_LDS(v4i16) *)(vt + kl * TG::kRowBytes + ps * 32 + q4 * 8));
             }
             typedef short v8i16 __attribute__((ext_vector_type(8)));
             const v8i16 both = __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7);
@@ -226,29 +284,23 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
         }
     };
 
-    auto compute = [&](auto ring_tag, int t, const bf16x8 (&vop)[MD], auto rescale_tag) {
+    auto compute = [&](auto bi, int t, auto rescale_tag) __attribute__((always_inline)) {
         constexpr bool RESCALE = decltype(rescale_tag)::value;
-        constexpr bool ODD = decltype(ring_tag)::value;
-        // LDS pointers derived from the ring object itself, so the compiler
-        // can tell these reads from the DMA writes into the other half
-        WF_LDS(const char) *kt = (WF_LDS(const char) *)(ODD ? ring1 : ring0) + stream * TG::kTileBytes;
-        // S^T = K Q^T, K operands from LDS
+        bf16x8 kop[2][KC], vop[MD];
+        read_k(bi, kop);
+        read_vt(bi, vop);
+        // S^T = K Q^T
         f32x4 s[2][NBW];
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
                 s[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const int kl = 16 * mb + m16;
 #pragma unroll
-            for (int kk = 0; kk < KC; ++kk) {
-                const int pg = (4 * kk + c4) ^ (kl & (TG::kGran - 1));
-                const bf16x8 kop = __builtin_bit_cast(
-                    bf16x8, *(WF_LDS(const u32x4) *)(kt + kl * TG::kRowBytes + pg * 16));
+            for (int kk = 0; kk < KC; ++kk)
 #pragma unroll
                 for (int nb = 0; nb < NBW; ++nb)
-                    s[mb][nb] = mfma16x16x32(kop, qf[nb][kk], s[mb][nb]);
-            }
+                    s[mb][nb] = mfma16x16x32(kop[mb][kk], qf[nb][kk], s[mb][nb]);
         }
         // causal mask: only tiles reaching past ctx_len
         const int kb = k_begin + t * kTileKeys;
@@ -263,16 +315,21 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                         s[mb][nb][i] = (key > lim[nb]) ? -INFINITY : s[mb][nb][i];
                     }
         }
-        float mx[NBW];
+        // lane-local maxima over the lane's 8 keys of each row
+        float lmx[NBW];
 #pragma unroll
-        for (int nb = 0; nb < NBW; ++nb) {
-            float m = fmaxf(fmaxf(fmaxf(s[0][nb][0], s[0][nb][1]), fmaxf(s[0][nb][2], s[0][nb][3])),
+        for (int nb = 0; nb < NBW; ++nb)
+            lmx[nb] = fmaxf(fmaxf(fmaxf(s[0][nb][0], s[0][nb][1]), fmaxf(s[0][nb][2], s[0][nb][3])),
                             fmaxf(fmaxf(s[1][nb][0], s[1][nb][1]), fmaxf(s[1][nb][2], s[1][nb][3])));
+        auto row_max = [&](float m) {
             m = fmaxf(m, __shfl_xor(m, 16, kWave));
-            m = fmaxf(m, __shfl_xor(m, 32, kWave));
-            mx[nb] = m;
-        }
+            return fmaxf(m, __shfl_xor(m, 32, kWave));
+        };
         if constexpr (RESCALE) {
+            float mx[NBW];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                mx[nb] = row_max(lmx[nb]);
             bool grow = false;
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
@@ -290,14 +347,27 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                 }
             }
         } else {
+            // The reference maximum of a row is its maximum over the first
+            // tile with a visible key (O and l are still zero until then);
+            // only that tile needs the cross-lane reduction.
+            bool unset = false;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                unset |= mref[nb] == -INFINITY;
+            if (__ballot(unset)) {
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb) {
+                    const float m = row_max(lmx[nb]);
+                    if (mref[nb] == -INFINITY)
+                        mref[nb] = m;
+                }
+            }
+            // all lanes of a row share its reference, so a lane-local test
+            // catches any growth of the row maximum
             bool over = false;
 #pragma unroll
-            for (int nb = 0; nb < NBW; ++nb) {
-                if (mref[nb] == -INFINITY)
-                    mref[nb] = mx[nb];       // O and l are still zero
-                else
-                    over |= (mx[nb] - mref[nb]) * sl2 > 64.f;
-            }
+            for (int nb = 0; nb < NBW; ++nb)
+                over |= (lmx[nb] - mref[nb]) * sl2 > 64.f;
             if (__ballot(over))
                 overflow = 1;                // the workgroup reruns rescaling
         }
@@ -329,9 +399,34 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                 o[md][nb] = mfma16x16x32(vop[md], pb[nb], o[md][nb]);
     };
 
-    // One pass over the split.  The step loop is unrolled by two so each
-    // half reads a compile-time ring half while the other is being filled.
-    auto pass = [&](auto rescale_tag, bool first_pass) {
+    // One pipeline step: stage st sits in ring buffer bi.  Up to NBUF-1
+    // stages are in flight; the wait leaves the later ones outstanding.
+    // After the barrier stage st is complete in LDS (each wave waited for
+    // its own loads of it) and every wave is done with the buffer of stage
+    // st-1 (its reads returned before they fed the MFMAs), which then
+    // receives stage st+NBUF-1.  The barrier is a bare s_barrier: the
+    // compiler-generated fence of __syncthreads() would wait for the loads
+    // of every later stage as well.
+    auto step = [&](auto bi, int st, auto rescale_tag) __attribute__((always_inline)) {
+        constexpr int B = decltype(bi)::value;
+        const int later = min(NBUF - 2, n_steps - 1 - st);   // stages issued after st
+        if (later >= 2)
+            wait_vmcnt<2 * LPW>();
+        else if (later == 1)
+            wait_vmcnt<LPW>();
+        else
+            wait_vmcnt<0>();
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (st + NBUF - 1 < n_steps)
+            issue(ic<(B + NBUF - 1) % NBUF>{}, st + NBUF - 1);
+        const int t = KS * st + stream;
+        if (t < n_tiles)
+            compute(bi, t, rescale_tag);
+    };
+
+    // One pass over the split; the step loop is unrolled by the ring depth so
+    // every step names its ring buffer at compile time.
+    auto pass = [&](auto rescale_tag, bool first_pass) __attribute__((always_inline)) {
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb) {
             mref[nb] = -INFINITY;
@@ -340,30 +435,45 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             for (int md = 0; md < MD; ++md)
                 o[md][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        if (!first_pass && stream < n_tiles)
-            issue(ring0, stream);
-        bf16x8 vop[MD];
-        for (int step = 0; step < n_steps; step += 2) {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
-            const bool have0 = stream + KS * step < n_tiles;
-            if (have0)
-                read_vt(std::false_type{}, vop);
-            if (step + 1 < n_steps && stream + KS * (step + 1) < n_tiles)
-                issue(ring1, stream + KS * (step + 1));
-            if (have0)
-                compute(std::false_type{}, stream + KS * step, vop, rescale_tag);
-            if (step + 1 >= n_steps)
+        if (first_pass)
+            load_q();
+        issue(ic<0>{}, 0);
+        if (NBUF > 2 && 1 < n_steps)
+            issue(ic<1 % NBUF>{}, 1);
+        if (NBUF > 3 && 2 < n_steps)
+            issue(ic<2 % NBUF>{}, 2);
+        if (first_pass) {
+            // The Q loads precede every DMA; once they are in, tie the
+            // registers so the compiler sees no load pending on them in
+            // the step loop (it would otherwise drain all DMA there).
+            const int issued = min(NBUF - 1, n_steps);
+            if (issued >= 3)
+                wait_vmcnt<3 * LPW>();
+            else if (issued == 2)
+                wait_vmcnt<2 * LPW>();
+            else
+                wait_vmcnt<LPW>();
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+                for (int kk = 0; kk < KC; ++kk)
+                    asm volatile("" : "+v"(qf[nb][kk]));
+        }
+        for (int st = 0; st < n_steps; st += NBUF) {
+            step(ic<0>{}, st, rescale_tag);
+            if (st + 1 >= n_steps)
                 break;
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
-            const bool have1 = stream + KS * (step + 1) < n_tiles;
-            if (have1)
-                read_vt(std::true_type{}, vop);
-            if (step + 2 < n_steps && stream + KS * (step + 2) < n_tiles)
-                issue(ring0, stream + KS * (step + 2));
-            if (have1)
-                compute(std::true_type{}, stream + KS * (step + 1), vop, rescale_tag);
+            step(ic<1>{}, st + 1, rescale_tag);
+            if constexpr (NBUF > 2) {
+                if (st + 2 >= n_steps)
+                    break;
+                step(ic<2 % NBUF>{}, st + 2, rescale_tag);
+            }
+            if constexpr (NBUF > 3) {
+                if (st + 3 >= n_steps)
+                    break;
+                step(ic<3 % NBUF>{}, st + 3, rescale_tag);
+            }
         }
         __syncthreads();
     };
@@ -387,10 +497,9 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     __syncthreads();
 
     // ---- merge the KS streams of each row through LDS ----------------------
-    // Streams s and s + KS/2 share region s % (KS/2): round 0 writes streams
-    // 0..KS/2-1, round 1 adds the rest, and the partial write below sums the
-    // regions -- a fixed order throughout.
-    auto oreg = [&](int r) { return reinterpret_cast<float *>(r ? ring1 : ring0); };
+    // Stream s adds into region s % NREG in round s / NREG (round 0 stores),
+    // and the partial write below sums the regions -- a fixed order.
+    auto oreg = [&](int r) { return (WF_LDS(float) *)(r ? ring1 : ring0); };
     float fac[NBW];
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
@@ -403,18 +512,18 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
         fac[nb] = (mref[nb] == -INFINITY) ? 0.f : fast_exp2((mref[nb] - muse) * sl2);
     }
 #pragma unroll 1
-    for (int round = 0; round < 2; ++round) {
-        if ((stream >= NREG) == (round == 1)) {
-            float *reg = oreg(stream % NREG);
+    for (int round = 0; round < KS / NREG; ++round) {
+        if (stream / NREG == round) {
+            WF_LDS(float) *reg = oreg(stream % NREG);
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
                 for (int md = 0; md < MD; ++md) {
-                    float *dst = reg + (rgi * ROWS_W + nb * 16 + m16) * OST + md * 16 + 4 * c4;
+                    WF_LDS(float) *dst = reg + (rgi * ROWS_W + nb * 16 + m16) * OST + md * 16 + 4 * c4;
                     f32x4 v = o[md][nb] * fac[nb];
-                    if (round == 1)
-                        v += *reinterpret_cast<f32x4 *>(dst);
-                    *reinterpret_cast<f32x4 *>(dst) = v;
+                    if (round > 0)
+                        v += *(WF_LDS(f32x4) *)dst;
+                    *(WF_LDS(f32x4) *)dst = v;
                 }
         }
         __syncthreads();
@@ -431,9 +540,9 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
         const int i = r / a.group;
         const int h = g * a.group + (r % a.group);
         const size_t pr = (size_t)split * pairs + (size_t)i * a.n_q_heads + h;
-        f32x4 v = reinterpret_cast<const f32x4 *>(oreg(0) + rl * OST)[d4];
+        f32x4 v = ((WF_LDS(const f32x4) *)(oreg(0) + rl * OST))[d4];
         if (NREG > 1)
-            v += reinterpret_cast<const f32x4 *>(oreg(1) + rl * OST)[d4];
+            v += ((WF_LDS(const f32x4) *)(oreg(1) + rl * OST))[d4];
         reinterpret_cast<f32x4 *>(a.ws_acc + pr * DH)[d4] = v;
         if (d4 == 0) {
             float mm = -INFINITY, ll = 0.f;
@@ -598,20 +707,22 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
     if (dt == WF_BF16) {
         // rows per wave 16*nb; rg row groups x ks key streams per workgroup
         // (at most 8 waves, so each wave may hold up to 256 registers)
+        // and a ring of nbuf stages of ks tiles (LDS: nbuf*ks tiles)
         if (rows <= 16) {
-            p.nb = 1; p.rg = 1; p.ks = 4;
+            p.nb = 1; p.rg = 1; p.ks = 4; p.nbuf = 2;
         } else if (rows <= 32) {
-            p.nb = 1; p.rg = 2; p.ks = 4;
+            p.nb = 1; p.rg = 2; p.ks = 4; p.nbuf = 2;
         } else if (rows <= 64) {
-            p.nb = 2; p.rg = 2; p.ks = 4;
+            p.nb = 1; p.rg = 4; p.ks = 2; p.nbuf = 3;
         } else {
-            p.nb = 2; p.rg = 4; p.ks = 2;
+            p.nb = 2; p.rg = 4; p.ks = 2; p.nbuf = 3;
         }
         p.n_row_groups = cdiv(rows, 16 * p.nb * p.rg);
     } else {
         p.nb = 0;
         p.rg = 1;
         p.ks = 1;
+        p.nbuf = 0;
         p.n_row_groups = 1;
     }
     int splits = num_splits;
@@ -672,14 +783,15 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
         if (p.n_row_groups > 1)
             blocks = cdiv(units, 8) * 8 * p.n_row_groups;
         dim3 grid(blocks), block(64 * p.ks * p.rg);
-#define WF_ATTN_CASE(DHV, NBV, RGV, KSV)                                     \
-    if (head_dim == DHV && p.nb == NBV && p.rg == RGV && p.ks == KSV) {       \
-        attn_partial_bf16<DHV, NBV, RGV, KSV><<<grid, block, 0, stream>>>(a); \
+#define WF_ATTN_CASE(DHV, NBV, RGV, KSV, NBUFV)                                      \
+    if (head_dim == DHV && p.nb == NBV && p.rg == RGV && p.ks == KSV &&               \
+        p.nbuf == NBUFV) {                                                            \
+        attn_partial_bf16<DHV, NBV, RGV, KSV, NBUFV><<<grid, block, 0, stream>>>(a);  \
     } else
-        WF_ATTN_CASE(128, 1, 1, 4) WF_ATTN_CASE(128, 1, 2, 4)
-        WF_ATTN_CASE(128, 2, 2, 4) WF_ATTN_CASE(128, 2, 4, 2)
-        WF_ATTN_CASE(64, 1, 1, 4) WF_ATTN_CASE(64, 1, 2, 4)
-        WF_ATTN_CASE(64, 2, 2, 4) WF_ATTN_CASE(64, 2, 4, 2)
+        WF_ATTN_CASE(128, 1, 1, 4, 2) WF_ATTN_CASE(128, 1, 2, 4, 2)
+        WF_ATTN_CASE(128, 1, 4, 2, 3) WF_ATTN_CASE(128, 2, 4, 2, 3)
+        WF_ATTN_CASE(64, 1, 1, 4, 2) WF_ATTN_CASE(64, 1, 2, 4, 2)
+        WF_ATTN_CASE(64, 1, 4, 2, 3) WF_ATTN_CASE(64, 2, 4, 2, 3)
         { return WF_ERR_UNSUPPORTED; }
 #undef WF_ATTN_CASE
     } else {

@@ -67,7 +67,7 @@ struct LmFinish {
 __global__ __launch_bounds__(kFinishThreads) void lm_finish_rows(LmFinish f) {
     __shared__ RowState ws[kFinishThreads / kWave];
     const int r = blockIdx.x;
-    const int wave = threadIdx.x / kWave;
+    const int wave = wave_id();
     const int lane = threadIdx.x % kWave;
     const RowState *row = f.states + (size_t)r * f.n_tiles;
     // batches of kFinishBatch loads in flight per thread (clamped addresses,
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(512) void lm_tiles_bf16(const uint16_t *__restrict_
     __shared__ __attribute__((aligned(16))) float zs[kMaxGamma][kLmTile + 4];
     const int tile = blockIdx.x;
     const int v0 = tile * kLmTile;
-    const int wave = threadIdx.x / kWave;
+    const int wave = wave_id();
     const int lane = threadIdx.x % kWave;
     const int m16 = lane & 15;
     const int c4 = lane >> 4;
@@ -253,7 +253,7 @@ __global__ __launch_bounds__(256) void lm_tiles_logits(const float *__restrict__
                                                        LmFinish f, int vocab) {
     const int tile = blockIdx.x;
     const int v0 = tile * kLogitsTile;
-    const int wave = threadIdx.x / kWave;
+    const int wave = wave_id();
     const int lane = threadIdx.x % kWave;
     for (int r = wave; r < f.gamma; r += 4) {
         const float *row = logits + (size_t)r * vocab;

@@ -68,7 +68,7 @@ __global__ __launch_bounds__(256) void prefill_partial_bf16(PrefillParams a) {
     const int g = unit / (2 * PAIRS);
     const int t0 = tb * TOK;
 
-    const int wave = threadIdx.x / kWave;
+    const int wave = wave_id();
     const int lane = threadIdx.x % kWave;
     const int m16 = lane & 15;
     const int c4 = lane >> 4;

@@ -24,6 +24,7 @@ struct AttnPlan {
     int nb;              // 16-row blocks per wave (bf16 path)
     int rg;              // row groups of waves per workgroup
     int ks;              // key streams per workgroup
+    int nbuf;            // LDS ring depth in stages of ks tiles (bf16 path)
     int n_row_groups;    // workgroup row groups of 16*nb*rg rows
     int splits;          // key splits per KV head
     int keys_per_split;  // multiple of the 32-key tile

@@ -143,6 +143,13 @@ __device__ __forceinline__ float state_entropy(RowState s) {
     return log1pf(s.sp) - s.t / (1.f + s.sp);
 }
 
+// Index of the calling wave in its workgroup, as a wave-uniform (scalar)
+// value: derived from threadIdx.x the compiler would treat it as varying per
+// lane and turn every branch on it into a divergent one.
+__device__ __forceinline__ int wave_id() {
+    return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+}
+
 // Halves of a device-scope fence.
 __device__ __forceinline__ void fence_release_agent() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
