@@ -145,6 +145,31 @@ class Step:
                 ("lmhead", lib.wf_lmhead_accept_entropy, self.lm, self.stream)]
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "verify_attn_8b_ctx32k_hbm_traffic.md")
+
+
+def measured_traffic():
+    """HBM bytes per wf_verify_attn call from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), or None when the
+    summary is missing or the kernel sources changed since it was taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines()
+                  if line.startswith("traffic_"))
+    try:
+        h = hashlib.sha256()
+        for src in fields["traffic_sources"].split():
+            h.update(open(os.path.join(ROOT, src), "rb").read())
+        if h.hexdigest() != fields["traffic_sources_sha256"].strip():
+            return None
+        return int(fields["traffic_bytes_per_call"])
+    except (KeyError, OSError, ValueError):
+        return None
+
+
 def cpu_baseline(w, layers, head, budget_s, max_layers=None):
     """The oracle as it stands, on host cores, over a bounded sample of the
     step: the LM head, then as many layers of attention and prefill as fit
@@ -389,7 +414,7 @@ def main():
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic() if w.cfg == 3 else None,
             "bytes_per_launch": by["attn_per_layer"],
             "avg_launch_us": round(attn_avg_ms * 1e3, 2),
         },

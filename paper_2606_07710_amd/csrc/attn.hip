@@ -630,64 +630,85 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
 
 // ---------------------------------------------------------------------------
 // Split merge: out = sum_s w_s acc_s / sum_s w_s l_s, w_s = exp(m_s - max m).
-// One wave per (row, q head).  Lane j owns splits j, j+64, ...: it computes
-// their weights, which are then broadcast across the wave while every lane
-// accumulates its output dims over the splits in ascending order.
+// One wave per (row, q head).  Lane L owns float4 column L % (head_dim/4)
+// of the splits L / (head_dim/4), + G, + 2G, ... (G split groups per wave),
+// accumulated in ascending order; the groups are then added with a fixed
+// butterfly.  The first batch of partial loads is issued before the weights
+// are formed, so a merge over up to G*kMergeBatch splits is one round trip.
 // ---------------------------------------------------------------------------
+constexpr int kMergeBatch = 16;          // float4 loads in flight per lane
+constexpr int kMaxSplits = 1024;
+
 template <int DH, bool OUT_BF16>
 __global__ __launch_bounds__(64) void attn_merge(const float *__restrict__ ws_acc,
                                                  const float *__restrict__ ws_ml,
                                                  void *out, int pairs, int splits,
                                                  float sl2) {
-    constexpr int E = DH / kWave;
-    constexpr int B = 32;                    // splits per batch, loads in flight
+    constexpr int Q = DH / 4;                // float4 columns of a row
+    constexpr int G = kWave / Q;             // split groups per wave
+    constexpr int B = kMergeBatch;
+    __shared__ float wsh[kMaxSplits];
     const int pr = blockIdx.x;
     const int lane = threadIdx.x;
+    const int d4 = lane % Q;
+    const int grp = lane / Q;
+    const f32x4 *col = reinterpret_cast<const f32x4 *>(ws_acc + (size_t)pr * DH) + d4;
+    const size_t sstride = (size_t)pairs * Q;    // float4 stride between splits
+
+    auto load_batch = [&](int s0, f32x4 (&v)[B]) {
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            v[b] = col[(size_t)min(s0 + G * b, splits - 1) * sstride];
+    };
+    f32x4 v[B];
+    load_batch(grp, v);
+
+    // weights of every split (lane j: splits j, j + 64, ...)
     float mloc = -INFINITY;
     for (int s = lane; s < splits; s += kWave)
         mloc = fmaxf(mloc, ws_ml[((size_t)s * pairs + pr) * 2]);
     const float mm = wave_max(mloc);
     const float muse = (mm == -INFINITY) ? 0.f : mm;
-    float acc[E], lpart = 0.f;
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-        acc[e] = 0.f;
-    const float *col = ws_acc + (size_t)pr * DH + lane;
-    const size_t sstride = (size_t)pairs * DH;
-    for (int s0 = 0; s0 < splits; s0 += B) {
-        // lane j < B weighs split s0 + j
-        float wl = 0.f;
-        if (lane < B && s0 + lane < splits) {
-            const size_t ps = (size_t)(s0 + lane) * pairs + pr;
-            const float ms = ws_ml[ps * 2];
-            wl = (ms == -INFINITY) ? 0.f : fast_exp2((ms - muse) * sl2);
-            lpart = fmaf(wl, ws_ml[ps * 2 + 1], lpart);
-        }
-        const int cnt = min(B, splits - s0);
-        const float *base = col + (size_t)s0 * sstride;
-        float v[B][E];
-#pragma unroll
-        for (int j = 0; j < B; ++j)
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                v[j][e] = (j < cnt) ? base[(size_t)min(j, cnt - 1) * sstride + e * kWave] : 0.f;
-#pragma unroll
-        for (int j = 0; j < B; ++j) {
-            const float wj = __shfl(wl, j, kWave);     // 0 for j >= cnt
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                acc[e] = fmaf(wj, v[j][e], acc[e]);
-        }
+    float lpart = 0.f;
+    for (int s = lane; s < splits; s += kWave) {
+        const size_t ps = (size_t)s * pairs + pr;
+        const float ms = ws_ml[ps * 2];
+        const float w = (ms == -INFINITY) ? 0.f : fast_exp2((ms - muse) * sl2);
+        wsh[s] = w;
+        lpart = fmaf(w, ws_ml[ps * 2 + 1], lpart);
     }
     const float inv = 1.f / wave_sum(lpart);
+    __syncthreads();
+
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = grp;; s0 += G * B) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const float r = acc[e] * inv;
-        const size_t oi = (size_t)pr * DH + lane + e * kWave;
-        if (OUT_BF16)
-            static_cast<uint16_t *>(out)[oi] = f32_to_bf16(r);
-        else
-            static_cast<float *>(out)[oi] = r;
+        for (int b = 0; b < B; ++b) {
+            const int sp = s0 + G * b;
+            if (sp < splits)
+                acc += wsh[sp] * v[b];
+        }
+        if (s0 + G * B >= splits)
+            break;
+        load_batch(s0 + G * B, v);
+    }
+#pragma unroll
+    for (int off = Q; off < kWave; off *= 2) {
+        f32x4 o;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            o[c] = __shfl_xor(acc[c], off, kWave);
+        acc += o;
+    }
+    if (grp == 0) {
+        const size_t oi = (size_t)pr * DH + 4 * d4;
+        const f32x4 r = acc * inv;
+        if (OUT_BF16) {
+            uint2 pk = {pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
+            *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(out) + oi) = pk;
+        } else {
+            *reinterpret_cast<f32x4 *>(static_cast<float *>(out) + oi) = r;
+        }
     }
 }
 

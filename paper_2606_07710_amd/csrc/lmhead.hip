@@ -15,6 +15,8 @@
 // Stage 2 (one workgroup per row): merge the row's tile states in a fixed
 // order and emit argmax and entropy; the last row to finish then emits the
 // accept length, bonus token and route.
+#include <type_traits>
+
 #include "wf_api_internal.h"
 #include "wf_device.h"
 
@@ -28,6 +30,7 @@ constexpr int kLmWaves = 8;
 constexpr int kLmPrefetch = 4;       // 32-dim chunks in flight per wave
 constexpr int kLogitsTile = 256;     // vocabulary entries per logits tile
 constexpr int kMaxGamma = 64;
+constexpr int kLmStreamGrid = 256;      // persistent grid: one workgroup per CU
 
 // ---- shared epilogue: tile logits in LDS -> one state per row --------------
 // zs is [kMaxGamma][kLmTile + 4]; zs[r][v] holds row r's logit of v0 + v.
@@ -213,6 +216,133 @@ __global__ __launch_bounds__(512) void lm_tiles_bf16(const uint16_t *__restrict_
     tile_states(zs, states, tile, n_tiles, v0, gamma, vocab, wave, kLmWaves, lane);
 }
 
+// Persistent bf16 LM head for up to 16 verify rows and a hidden size of
+// CPW * 32 * 8: workgroup b owns a contiguous run of 16-row vocabulary
+// blocks and walks it in tiles of kLmTile rows.  Each of the 8 waves owns a
+// contiguous CPW*32-dim slice of the hidden dimension, keeps its slice of h
+// in registers for the whole run, and streams W with kLmPrefetch chunks in
+// flight; the prefetch runs on across tile boundaries, so the stream never
+// drains.  Per tile the 8 partial logit blocks meet in LDS (double
+// buffered: one barrier per tile) and every row's tile state is folded
+// into a running state in ascending vocabulary order; the workgroup writes
+// one state per row at the end.
+template <int CPW>
+__global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict__ h,
+                                                      const uint16_t *__restrict__ w,
+                                                      LmFinish f, int vocab) {
+    constexpr int D = CPW * 32 * kLmWaves;
+    constexpr int P = kLmPrefetch;
+    static_assert(CPW % P == 0 && CPW >= P, "chunks per wave");
+    __shared__ __attribute__((aligned(16))) float zs[2][kLmWaves][16][kLmTile + 4];
+    const int gamma = f.gamma;
+    const int wave = wave_id();
+    const int lane = threadIdx.x % kWave;
+    const int m16 = lane & 15;
+    const int c4 = lane >> 4;
+
+    const int nblk = (vocab + 15) / 16;
+    const int b0 = (int)((long long)blockIdx.x * nblk / gridDim.x);
+    const int b1 = (int)((long long)(blockIdx.x + 1) * nblk / gridDim.x);
+    const int ntile = (b1 - b0 + kLmMB - 1) / kLmMB;
+
+    // this wave's slice of h: chunk u covers dims (wave*CPW + u)*32 + 8*c4 ..
+    bf16x8 hr[CPW];
+    {
+        const uint16_t *hp = h + (size_t)min(m16, gamma - 1) * D + wave * CPW * 32 + c4 * 8;
+#pragma unroll
+        for (int u = 0; u < CPW; ++u)
+            hr[u] = load_bf16x8(hp + u * 32);
+    }
+    // W rows of tile t, block mb.  Rows past the workgroup's run (a ragged
+    // last tile) re-read its last row, which is in L2, and are masked out of
+    // the states.
+    const int row_end = min(b1 * 16, vocab) - 1;
+    auto wrow = [&](int t, int mb) {
+        const int row = min((b0 + kLmMB * t + mb) * 16 + m16, row_end);
+        return w + (size_t)row * D + wave * CPW * 32 + c4 * 8;
+    };
+
+    bf16x8 wb[P][kLmMB];
+    {
+        const int t0 = min(0, ntile - 1);
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+#pragma unroll
+            for (int mb = 0; mb < kLmMB; ++mb)
+                wb[p][mb] = load_bf16x8(wrow(t0, mb) + p * 32);
+    }
+    RowState run[2] = {state_empty(), state_empty()};
+
+    // One tile; all but the last also load the head chunks of the next tile
+    // (the last tile is peeled so that no branch sits in the steady state).
+    auto tile = [&](int t, auto last_tag) __attribute__((always_inline)) {
+        constexpr bool LAST = decltype(last_tag)::value;
+        const uint16_t *cur[kLmMB], *nxt[kLmMB];
+#pragma unroll
+        for (int mb = 0; mb < kLmMB; ++mb) {
+            cur[mb] = wrow(t, mb);
+            nxt[mb] = wrow(LAST ? t : t + 1, mb);
+        }
+        f32x4 acc[kLmMB];
+#pragma unroll
+        for (int mb = 0; mb < kLmMB; ++mb)
+            acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int u = 0; u < CPW; ++u) {
+            const int p = u % P;
+#pragma unroll
+            for (int mb = 0; mb < kLmMB; ++mb)
+                acc[mb] = mfma16x16x32(wb[p][mb], hr[u], acc[mb]);
+            // refill the slot with the chunk P ahead (near the end of the
+            // tile: the next tile's head chunks)
+            if (u + P < CPW) {
+#pragma unroll
+                for (int mb = 0; mb < kLmMB; ++mb)
+                    wb[p][mb] = load_bf16x8(cur[mb] + (u + P) * 32);
+            } else if (!LAST) {
+#pragma unroll
+                for (int mb = 0; mb < kLmMB; ++mb)
+                    wb[p][mb] = load_bf16x8(nxt[mb] + (u + P - CPW) * 32);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // lane (m16, c4) holds logits of vocabulary rows 16*mb + 4*c4 + i of
+        // the tile for verify row m16
+        const int buf = t & 1;
+#pragma unroll
+        for (int mb = 0; mb < kLmMB; ++mb)
+            *reinterpret_cast<f32x4 *>(&zs[buf][wave][m16][16 * mb + 4 * c4]) = acc[mb];
+        __syncthreads();
+        // rows wave and wave + 8, column = lane: sum the 8 waves in order
+        const int blk = b0 + kLmMB * t + lane / 16;
+        const int v = blk * 16 + (lane & 15);
+        const bool valid = blk < b1 && v < vocab;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int r = wave + kLmWaves * k;
+            if (r < gamma) {
+                float z = zs[buf][0][r][lane];
+#pragma unroll
+                for (int ww = 1; ww < kLmWaves; ++ww)
+                    z += zs[buf][ww][r][lane];
+                RowState st = valid ? state_single(z, v) : state_empty();
+                st = wave_merge(st);
+                run[k] = state_merge(run[k], st);
+            }
+        }
+    };
+    for (int t = 0; t + 1 < ntile; ++t)
+        tile(t, std::false_type{});
+    if (ntile > 0)
+        tile(ntile - 1, std::true_type{});
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int r = wave + kLmWaves * k;
+        if (r < gamma && lane == 0)
+            f.states[(size_t)r * f.n_tiles + blockIdx.x] = run[k];
+    }
+}
+
 __global__ __launch_bounds__(256) void lm_tiles_f32(const float *__restrict__ h,
                                                     const float *__restrict__ w,
                                                     LmFinish f, int d, int vocab) {
@@ -299,6 +429,15 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
     if (logits) {
         f.n_tiles = cdiv(vocab, kLogitsTile);
         lm_tiles_logits<<<f.n_tiles, 256, 0, stream>>>(logits, f, vocab);
+    } else if (dt == WF_BF16 && gamma <= 16 && (d == 4096 || d == 5120)) {
+        // persistent: one workgroup per CU, one state per row per workgroup
+        f.n_tiles = std::min(kLmStreamGrid, cdiv(vocab, kLmTile));
+        const uint16_t *hb = static_cast<const uint16_t *>(h);
+        const uint16_t *wb = static_cast<const uint16_t *>(w_lm);
+        if (d == 4096)
+            lm_stream_bf16<16><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, vocab);
+        else
+            lm_stream_bf16<20><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, vocab);
     } else if (dt == WF_BF16) {
         f.n_tiles = cdiv(vocab, kLmTile);
         const uint16_t *hb = static_cast<const uint16_t *>(h);
