@@ -2,24 +2,23 @@
 // KV cache (parallel target verification, Sec. 3.2 of the WhiFlash paper).
 //
 // Split-KV design for batch 1 on MI355X.  Every workgroup owns one KV head g
-// and one contiguous slice ("split") of the key range, and processes all
-// G*gamma query rows of that head at once, so every K/V byte is fetched from
-// HBM exactly once.  Inside the workgroup four waves stream interleaved
-// 32-key tiles; each keeps an fp32 online-softmax state per row.  The waves
-// merge through LDS and the workgroup writes one fp32 partial (unnormalised
-// output row, running max, running sum) per (split, row).  A second kernel
-// combines the splits in a fixed order.
+// and one contiguous slice ("split") of the key range, and processes the
+// G*gamma query rows of that head (up to 64 per workgroup), so every K/V
+// byte is fetched from HBM once.  Its waves form KS key streams x RG row
+// groups; each keeps an fp32 online-softmax state per row.  The streams
+// merge through LDS and the workgroup writes one partial per (split, row):
+// the unnormalised output row (bf16 on the bf16 path, fp32 otherwise) and
+// the fp32 running max and sum.  A second kernel combines the splits in a
+// fixed order.
 //
 // bf16 path, per 32-key tile and wave (16x16x32 bf16 MFMA):
-//   S^T = K * Q^T : A = 16 keys x 32 dims straight from global memory,
+//   S^T = K * Q^T : A = 16 keys x 32 dims from the LDS copy of the K tile,
 //                   B = Q^T held in registers for the whole kernel.
 //   P   = exp2((S - m) * scale * log2 e), online max/sum per row.
 //   O^T += V^T * P^T : B = P^T comes out of the S^T accumulator already in
-//                   operand layout (the key order inside a tile is chosen so
-//                   each lane owns 8 consecutive keys of its row); A = V^T is
-//                   read from a per-wave LDS copy of the V tile, stored with
-//                   an XOR swizzle so the transposing reads hit 32 distinct
-//                   banks.
+//                   operand layout (each lane owns 8 consecutive keys of its
+//                   row); A = V^T comes from transposing reads of the LDS
+//                   copy of the V tile.
 #include <type_traits>
 
 #include "wf_api_internal.h"
@@ -38,8 +37,9 @@ struct AttnParams {
     const float *q32;         // fp32 path
     const float *k32;
     const float *v32;
-    float *ws_acc;            // [splits][gamma*n_q_heads][head_dim]
-    float *ws_ml;             // [splits][gamma*n_q_heads][2]
+    void *ws_o;               // [splits][gamma*n_q_heads][head_dim], unnormalised
+                              // partial outputs: bf16 (bf16 path) or fp32
+    float *ws_ml;             // [splits][gamma*n_q_heads][2]: running max, sum
     int gamma, ctx_len, cap, n_q_heads, n_kv_heads, group, rows, n_keys;
     int splits, keys_per_split, n_row_groups;
     float sl2;                // softmax_scale * log2(e)
@@ -543,7 +543,10 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
         f32x4 v = ((WF_LDS(const f32x4) *)(oreg(0) + rl * OST))[d4];
         if (NREG > 1)
             v += ((WF_LDS(const f32x4) *)(oreg(1) + rl * OST))[d4];
-        reinterpret_cast<f32x4 *>(a.ws_acc + pr * DH)[d4] = v;
+        // bf16 partials: the split merge weighs them by at most 1 and the
+        // output is rounded to bf16 anyway
+        const uint2 pk = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        reinterpret_cast<uint2 *>(static_cast<uint16_t *>(a.ws_o) + pr * DH)[d4] = pk;
         if (d4 == 0) {
             float mm = -INFINITY, ll = 0.f;
 #pragma unroll
@@ -621,7 +624,7 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
     const size_t prs = (size_t)split * a.gamma * a.n_q_heads + pr;
 #pragma unroll
     for (int e = 0; e < E; ++e)
-        a.ws_acc[prs * DH + lane + e * kWave] = acc[e];
+        static_cast<float *>(a.ws_o)[prs * DH + lane + e * kWave] = acc[e];
     if (lane == 0) {
         a.ws_ml[prs * 2] = m;
         a.ws_ml[prs * 2 + 1] = l;
@@ -639,12 +642,13 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
 constexpr int kMergeBatch = 16;          // float4 loads in flight per lane
 constexpr int kMaxSplits = 1024;
 
-template <int DH, bool OUT_BF16>
-__global__ __launch_bounds__(64) void attn_merge(const float *__restrict__ ws_acc,
+// BF16: partials and output in bf16 (else fp32).
+template <int DH, bool BF16>
+__global__ __launch_bounds__(64) void attn_merge(const void *__restrict__ ws_o,
                                                  const float *__restrict__ ws_ml,
                                                  void *out, int pairs, int splits,
                                                  float sl2) {
-    constexpr int Q = DH / 4;                // float4 columns of a row
+    constexpr int Q = DH / 4;                // 4-element columns of a row
     constexpr int G = kWave / Q;             // split groups per wave
     constexpr int B = kMergeBatch;
     __shared__ float wsh[kMaxSplits];
@@ -652,13 +656,21 @@ __global__ __launch_bounds__(64) void attn_merge(const float *__restrict__ ws_ac
     const int lane = threadIdx.x;
     const int d4 = lane % Q;
     const int grp = lane / Q;
-    const f32x4 *col = reinterpret_cast<const f32x4 *>(ws_acc + (size_t)pr * DH) + d4;
-    const size_t sstride = (size_t)pairs * Q;    // float4 stride between splits
+    const size_t sstride = (size_t)pairs * Q;    // column stride between splits
 
     auto load_batch = [&](int s0, f32x4 (&v)[B]) {
 #pragma unroll
-        for (int b = 0; b < B; ++b)
-            v[b] = col[(size_t)min(s0 + G * b, splits - 1) * sstride];
+        for (int b = 0; b < B; ++b) {
+            const size_t idx = (size_t)min(s0 + G * b, splits - 1) * sstride +
+                               (size_t)pr * Q + d4;
+            if constexpr (BF16) {
+                const uint2 pk = reinterpret_cast<const uint2 *>(ws_o)[idx];
+                v[b] = f32x4{bf16_to_f32((uint16_t)pk.x), bf16_to_f32((uint16_t)(pk.x >> 16)),
+                             bf16_to_f32((uint16_t)pk.y), bf16_to_f32((uint16_t)(pk.y >> 16))};
+            } else {
+                v[b] = reinterpret_cast<const f32x4 *>(ws_o)[idx];
+            }
+        }
     };
     f32x4 v[B];
     load_batch(grp, v);
@@ -703,7 +715,7 @@ __global__ __launch_bounds__(64) void attn_merge(const float *__restrict__ ws_ac
     if (grp == 0) {
         const size_t oi = (size_t)pr * DH + 4 * d4;
         const f32x4 r = acc * inv;
-        if (OUT_BF16) {
+        if (BF16) {
             uint2 pk = {pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
             *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(out) + oi) = pk;
         } else {
@@ -726,6 +738,7 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
     const int n_tiles = cdiv(n_keys, kTileKeys);
     p.rows = rows;
     if (dt == WF_BF16) {
+        p.part_bytes = 2;
         // rows per wave 16*nb; rg row groups x ks key streams per workgroup
         // (at most 8 waves, so each wave may hold up to 256 registers)
         // and a ring of nbuf stages of ks tiles (LDS: nbuf*ks tiles)
@@ -740,6 +753,7 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
         }
         p.n_row_groups = cdiv(rows, 16 * p.nb * p.rg);
     } else {
+        p.part_bytes = 4;
         p.nb = 0;
         p.rg = 1;
         p.ks = 1;
@@ -768,9 +782,11 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
     return p;
 }
 
+// Workspace: counter block, then [splits][pairs][2] fp32 (max, sum), then
+// the [splits][pairs][head_dim] partial outputs (p.part_bytes each).
 size_t attn_workspace_bytes(const AttnPlan &p, int gamma, int n_q_heads, int head_dim) {
     const size_t pairs = (size_t)gamma * n_q_heads;
-    return kCounterBytes + (size_t)p.splits * pairs * (head_dim + 2) * sizeof(float);
+    return kCounterBytes + (size_t)p.splits * pairs * (2 * sizeof(float) + (size_t)head_dim * p.part_bytes);
 }
 
 wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
@@ -780,8 +796,8 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
                         hipStream_t stream) {
     AttnParams a{};
     const size_t pairs = (size_t)gamma * n_q_heads;
-    a.ws_acc = reinterpret_cast<float *>(static_cast<char *>(workspace) + kCounterBytes);
-    a.ws_ml = a.ws_acc + (size_t)p.splits * pairs * head_dim;
+    a.ws_ml = reinterpret_cast<float *>(static_cast<char *>(workspace) + kCounterBytes);
+    a.ws_o = a.ws_ml + (size_t)p.splits * pairs * 2;
     a.gamma = gamma;
     a.ctx_len = ctx_len;
     a.cap = cap;
@@ -832,14 +848,14 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
     const bool ob = (dt == WF_BF16);
     if (head_dim == 128) {
         if (ob)
-            attn_merge<128, true><<<mgrid, mblock, 0, stream>>>(a.ws_acc, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
+            attn_merge<128, true><<<mgrid, mblock, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
         else
-            attn_merge<128, false><<<mgrid, mblock, 0, stream>>>(a.ws_acc, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
+            attn_merge<128, false><<<mgrid, mblock, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
     } else {
         if (ob)
-            attn_merge<64, true><<<mgrid, mblock, 0, stream>>>(a.ws_acc, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
+            attn_merge<64, true><<<mgrid, mblock, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
         else
-            attn_merge<64, false><<<mgrid, mblock, 0, stream>>>(a.ws_acc, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
+            attn_merge<64, false><<<mgrid, mblock, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
     }
     if (hipGetLastError() != hipSuccess)
         return WF_ERR_HIP;

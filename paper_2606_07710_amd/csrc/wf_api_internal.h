@@ -28,6 +28,7 @@ struct AttnPlan {
     int n_row_groups;    // workgroup row groups of 16*nb*rg rows
     int splits;          // key splits per KV head
     int keys_per_split;  // multiple of the 32-key tile
+    int part_bytes;      // bytes per partial-output element (bf16 path: 2)
 };
 
 AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,

@@ -76,7 +76,8 @@ def test_workspace_query():
     assert need > 0 and need % 4 == 0
     assert wf.wf_verify_attn_workspace_bytes(1, 0, 32768, 32, 8, 128) == 0
     forced = wf.wf_verify_attn_workspace_bytes(1, 16, 32768, 32, 8, 128, 7)
-    assert forced == COUNTER_BLOCK + 7 * 16 * 32 * 130 * 4
+    # bf16 partial outputs, fp32 (max, sum) per split and (row, head)
+    assert forced == COUNTER_BLOCK + 7 * 16 * 32 * (128 * 2 + 8)
     # counter block, then one 16-byte row state per (row, 64-entry tile)
     assert wf.wf_lmhead_workspace_bytes(16, 151936) == COUNTER_BLOCK + 16 * 2374 * 16
     assert wf.wf_lmhead_workspace_bytes(0, 10) == 0
