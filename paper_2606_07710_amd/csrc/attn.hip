@@ -127,8 +127,11 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     // padded by 4 floats so the 16 rows of a wave's accumulator tile fall in
     // distinct banks.
     constexpr int OST = DH + 4;
-    constexpr int NREG = KS >= 4 ? 2 : 1;
     constexpr int REGION_BYTES = ROWS_WG * OST * 4;
+    constexpr int MAX_RS = STAGE_BYTES > REGION_BYTES ? STAGE_BYTES : REGION_BYTES;
+    // two regions (one merge round for two streams) when they fit
+    constexpr int NREG = (KS >= 2 && 2 * MAX_RS + (NBUF - 2) * STAGE_BYTES +
+                          KS * ROWS_WG * 8 + 16 <= 160 * 1024) ? 2 : 1;
     constexpr int RING0_BYTES = STAGE_BYTES > REGION_BYTES ? STAGE_BYTES : REGION_BYTES;
     constexpr int RING1_BYTES = NREG < 2 ? STAGE_BYTES : RING0_BYTES;
     static_assert(RING0_BYTES + RING1_BYTES + (NBUF - 2) * STAGE_BYTES +
