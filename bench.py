@@ -40,10 +40,12 @@ def parse():
                          "gamma 16, 16 catch-up tokens)")
     ap.add_argument("--graph", action="store_true",
                     help="replay the step as one captured HIP graph")
-    ap.add_argument("--serial", action="store_true",
-                    help="issue every call on one stream (default: the "
-                         "catch-up prefill runs on a second stream, "
-                         "concurrently with the verification attention)")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run the catch-up prefill on a second stream, "
+                         "concurrent with the verification attention.  Off by "
+                         "default: in a round the catch-up follows the route "
+                         "decision and reads the target's features of the "
+                         "accepted tokens, so it depends on the verification")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0,
                     help="approximate seconds of oracle work for cpu_baseline")
@@ -287,7 +289,7 @@ def main():
     step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_pre,
                 ws_lm, wf)
     stream = torch.cuda.current_stream()
-    catchup = None if args.serial else torch.cuda.Stream()
+    catchup = torch.cuda.Stream() if args.overlap else None
     step.build(stream, catchup)
     step.run(check=True)
     torch.cuda.synchronize()
@@ -402,7 +404,7 @@ def main():
                    "ctx_len": w.ctx_len, "gamma": w.gamma,
                    "catch_up_tokens": w.n_prefill, "vocab": w.vocab,
                    "graph": bool(graph is not None),
-                   "schedule": "serial" if catchup is None else
+                   "schedule": "one stream, model order" if catchup is None else
                                "catch-up prefill on a second stream"},
         "step_hbm_gbps": round(step_gbps, 1),
         "step_algorithmic_bytes": by["total"],

@@ -166,10 +166,24 @@ __global__ __launch_bounds__(256) void prefill_finish_bf16(PrefillParams a, int 
         const int t = t0 + tl;
         if (t >= a.n_tok)
             continue;
+        // slices in ascending order; loads batched so they are in flight
+        // together (clamped, masked at the add)
+        constexpr int KB = 16;
         float lo = 0.f, hi = 0.f;
-        for (int k = 0; k < ksplit; ++k) {
-            lo += part[k * (2 * 16 * TOK) + e * TOK + tl];
-            hi += part[k * (2 * 16 * TOK) + 16 * TOK + e * TOK + tl];
+        for (int k0 = 0; k0 < ksplit; k0 += KB) {
+            float vl[KB], vh[KB];
+#pragma unroll
+            for (int b = 0; b < KB; ++b) {
+                const int k = min(k0 + b, ksplit - 1);
+                vl[b] = part[k * (2 * 16 * TOK) + e * TOK + tl];
+                vh[b] = part[k * (2 * 16 * TOK) + 16 * TOK + e * TOK + tl];
+            }
+#pragma unroll
+            for (int b = 0; b < KB; ++b)
+                if (k0 + b < ksplit) {
+                    lo += vl[b];
+                    hi += vh[b];
+                }
         }
         const int pos = a.start_pos + t;
         if (kind == 0)
