@@ -29,12 +29,12 @@
  *     WF_ERR_HIP.
  *   - Workspaces are caller-owned scratch of at least the size the matching
  *     *_workspace_bytes query returns, ZERO-FILLED before their first use.
- *     Each starts with a 64 KiB block of arrival counters, with which the
- *     last workgroup of a cross-workgroup reduction finishes it; partial
- *     results follow that block.  Every call leaves the counter block at
- *     zero again, so a workspace zeroed once serves any later call, of any
- *     of the three kinds and any sizes.  Two calls that overlap in time
- *     must not share one.
+ *     Each starts with a 4 MiB zero block of arrival counters and exchange
+ *     slots, through which workgroups of one call combine results; partial
+ *     results follow that block.  Every call leaves the zero block at zero
+ *     again, so a workspace zeroed once serves any later call, of any of the
+ *     three kinds and any sizes.  Two calls that overlap in time must not
+ *     share one.
  *   - Reductions use a fixed order, so repeated calls on the same inputs and
  *     the same split count return bit-identical results.
  *   - Row-major throughout; "[a][b][c]" lists dimensions slowest first.
@@ -137,8 +137,9 @@ size_t wf_verify_attn_workspace_bytes(wf_dtype_t dt, int32_t gamma,
  *           d_in >= 1, and d_in % 32 == 0 for WF_BF16.
  * workspace >= wf_kv_only_prefill_workspace_bytes(...) bytes (may be NULL
  *           when that is 0: fp32, or no tokens).  The bf16 path splits the
- *           input dimension across workgroups and sums the slices in a
- *           fixed order.
+ *           input dimension across a power-of-two number of workgroups whose
+ *           sums meet up a fixed binary tree (deterministic), using exchange
+ *           slots in the workspace's zero block.
  * ---------------------------------------------------------------------- */
 wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                                const void *w_v, void *k_cache, void *v_cache,

@@ -113,6 +113,8 @@ wf_status_t check_prefill(wf_dtype_t dt, int n_tok, int start_pos, int cap,
         return WF_ERR_UNSUPPORTED;
     if (dt == WF_BF16 && d_in % 32 != 0)
         return WF_ERR_UNSUPPORTED;
+    if (dt == WF_BF16 && n_tok > 0 && !wf::prefill_fits(n_tok, d_in, n_kv_heads, head_dim))
+        return WF_ERR_UNSUPPORTED;
     return WF_OK;
 }
 }  // namespace

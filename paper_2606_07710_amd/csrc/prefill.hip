@@ -7,11 +7,13 @@
 //
 // bf16 path: the work unit is (KV head, K or V, pair of 16-feature blocks f
 // and f + head_dim/2).  Pairing the two halves of the rotate-half RoPE puts
-// both elements of every rotation pair in the same lane of the MFMA
-// accumulators, so RoPE is a register epilogue.  The input dimension is
-// split across workgroups so a handful of units still spreads over the whole
-// chip; each slice writes an fp32 partial, and a second kernel sums the
-// slices in order, rotates and writes the cache rows.  Tokens are the MFMA N dimension (blocks of 16).
+// both elements of every rotation pair in the same thread after the
+// reduction, so RoPE is a register epilogue.  The input dimension is split
+// across a power-of-two number of workgroups so a handful of units still
+// spreads over the whole chip; the slices' sums meet up a fixed binary tree
+// of device-scope atomic exchanges (deterministic: every node adds exactly
+// two values), and the thread that leaves the root rotates and writes the
+// cache pair.  Tokens are the MFMA N dimension (blocks of 16).
 // RoPE angles are formed in fp64: at positions ~65K an fp32 angle would be
 // off by ~4e-3 rad.
 #include "wf_api_internal.h"
@@ -32,7 +34,7 @@ struct PrefillParams {
     void *v_cache;
     int n_tok, start_pos, cap, d_in, n_kv_heads;
     double rope_base;
-    float *ws;                 // bf16 path: split-K partials
+    unsigned long long *slots; // bf16 path: k-slice exchange slots, zero between calls
     int chunks_per_split;      // 32-wide chunks of d_in per k-slice
 };
 
@@ -50,10 +52,10 @@ __device__ __forceinline__ void rope_pair(float &lo, float &hi, int i, int dh,
 
 // Split-K: workgroup (unit, k-slice, token block) computes D[feature][token]
 // over its slice of the input dimension for the unit's two 16-feature blocks
-// (f and f + head_dim/2 of one head, K or V), writes the fp32 partial to
-// ws[unit][token block][kslice][2][16][TOK].
+// (f and f + head_dim/2 of one head, K or V); the slices then meet through
+// the exchange tree below.
 template <int DH, int NBT>
-__global__ __launch_bounds__(256) void prefill_partial_bf16(PrefillParams a) {
+__global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
     constexpr int PAIRS = DH / 32;       // 16-feature block pairs per head
     constexpr int TOK = 16 * NBT;
     constexpr int WAVES = 4;
@@ -77,6 +79,9 @@ __global__ __launch_bounds__(256) void prefill_partial_bf16(PrefillParams a) {
     const uint16_t *x = static_cast<const uint16_t *>(a.x);
     const int f_lo = g * DH + 16 * pair;           // first feature, low half
     const int c_begin = ks * a.chunks_per_split;   // 32-wide chunks of d_in
+    // chunks of this slice (the last slices of a power-of-two split may be
+    // short or empty)
+    const int n_c = max(0, min(a.chunks_per_split, a.d_in / 32 - c_begin));
     const uint16_t *wp0 = w + (size_t)(f_lo + m16) * a.d_in + c4 * 8;
     const uint16_t *wp1 = w + (size_t)(f_lo + DH / 2 + m16) * a.d_in + c4 * 8;
     // Tokens past n_tok read the last token instead: they only feed MFMA
@@ -86,34 +91,37 @@ __global__ __launch_bounds__(256) void prefill_partial_bf16(PrefillParams a) {
     for (int nb = 0; nb < NBT; ++nb)
         xp[nb] = x + (size_t)min(t0 + nb * 16 + m16, a.n_tok - 1) * a.d_in + c4 * 8;
 
-    // every load of this wave's chunks is issued before the first MFMA
-    bf16x8 wr[MAXC][2], xr[MAXC][NBT];
-#pragma unroll
-    for (int u = 0; u < MAXC; ++u) {
-        const int c = wave + WAVES * u;
-        if (c < a.chunks_per_split) {
-            const int off = (c_begin + c) * 32;
-            wr[u][0] = load_bf16x8(wp0 + off);
-            wr[u][1] = load_bf16x8(wp1 + off);
-#pragma unroll
-            for (int nb = 0; nb < NBT; ++nb)
-                xr[u][nb] = load_bf16x8(xp[nb] + off);
-        }
-    }
     f32x4 acc[2][NBT];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NBT; ++nb)
             acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // wave-strided chunks c = wave, wave + 4, ...; batches of MAXC chunks
+    // whose loads are all issued before the batch's first MFMA
+    for (int cb = wave; cb < n_c; cb += WAVES * MAXC) {
+        bf16x8 wr[MAXC][2], xr[MAXC][NBT];
 #pragma unroll
-    for (int u = 0; u < MAXC; ++u) {
-        if (wave + WAVES * u < a.chunks_per_split) {
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
+        for (int u = 0; u < MAXC; ++u) {
+            const int c = cb + WAVES * u;
+            if (c < n_c) {
+                const int off = (c_begin + c) * 32;
+                wr[u][0] = load_bf16x8(wp0 + off);
+                wr[u][1] = load_bf16x8(wp1 + off);
 #pragma unroll
                 for (int nb = 0; nb < NBT; ++nb)
-                    acc[mb][nb] = mfma16x16x32(wr[u][mb], xr[u][nb], acc[mb][nb]);
+                    xr[u][nb] = load_bf16x8(xp[nb] + off);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < MAXC; ++u) {
+            if (cb + WAVES * u < n_c) {
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                    for (int nb = 0; nb < NBT; ++nb)
+                        acc[mb][nb] = mfma16x16x32(wr[u][mb], xr[u][nb], acc[mb][nb]);
+            }
         }
     }
     // lane (m16, c4) holds D[feature 4*c4 + i][token nb*16 + m16]
@@ -125,66 +133,50 @@ __global__ __launch_bounds__(256) void prefill_partial_bf16(PrefillParams a) {
             for (int i = 0; i < 4; ++i)
                 zs[wave][mb][4 * c4 + i][nb * 16 + m16] = acc[mb][nb][i];
     __syncthreads();
-    // sum the waves in a fixed order and write the partial
+    // Thread (e, token) sums the waves in order for its rotation pair
+    // (feature 16*pair + e of the low half and its partner in the high
+    // half), then combines the k-slices up a fixed binary tree: leaf
+    // ksplit + k, node i with children 2i and 2i+1, one 64-bit exchange slot
+    // per internal node and pair.  The first slice to reach a node parks its
+    // (lo, hi) there; the second takes it, adds (a commutative fp32 add, so
+    // the result does not depend on who came first), resets the slot and
+    // climbs on.  Whoever leaves the root finishes the pair: RoPE for K,
+    // bf16 cache write.  Slot 0 means empty; a parked pair is stored as
+    // (bits(hi) << 32) | (bits(lo) + 1), never 0 for arithmetic results.
     const int ksplit = gridDim.y;
     const size_t ub = (size_t)unit * gridDim.z + tb;           // (unit, token block)
-    float *part = a.ws + ub * ksplit * (2 * 16 * TOK);
-    float *dst = part + (size_t)ks * (2 * 16 * TOK);
-    for (int idx = threadIdx.x; idx < 2 * 16 * TOK; idx += blockDim.x) {
-        const int mb = idx / (16 * TOK);
-        const int e = (idx / TOK) % 16;
-        const int tl = idx % TOK;
-        float v = zs[0][mb][e][tl];
-#pragma unroll
-        for (int ww = 1; ww < WAVES; ++ww)
-            v += zs[ww][mb][e][tl];
-        dst[idx] = v;
-    }
-
-    // The last k-slice workgroup of this (unit, token block) to finish sums
-    // the slices in slice order, applies RoPE to K and writes the cache rows.
-}
-
-// Workgroup (unit, token block) sums the unit's k-slice partials in slice
-// order, applies RoPE to K and writes the cache rows.
-template <int DH, int NBT>
-__global__ __launch_bounds__(256) void prefill_finish_bf16(PrefillParams a, int ksplit) {
-    constexpr int PAIRS = DH / 32;
-    constexpr int TOK = 16 * NBT;
-    const int unit = blockIdx.x;
-    const int tb = blockIdx.y;
-    const int pair = unit % PAIRS;
-    const int kind = (unit / PAIRS) % 2;
-    const int g = unit / (2 * PAIRS);
-    const int t0 = tb * TOK;
-    const size_t ub = (size_t)unit * gridDim.y + tb;
-    const float *part = a.ws + ub * ksplit * (2 * 16 * TOK);
+    unsigned long long *slots = a.slots + ub * (size_t)(ksplit - 1) * (16 * TOK);
     uint16_t *cache = static_cast<uint16_t *>(kind ? a.v_cache : a.k_cache);
     for (int idx = threadIdx.x; idx < 16 * TOK; idx += blockDim.x) {
         const int e = idx / TOK;
         const int tl = idx % TOK;
-        const int t = t0 + tl;
-        if (t >= a.n_tok)
-            continue;
-        // slices in ascending order; loads batched so they are in flight
-        // together (clamped, masked at the add)
-        constexpr int KB = 16;
-        float lo = 0.f, hi = 0.f;
-        for (int k0 = 0; k0 < ksplit; k0 += KB) {
-            float vl[KB], vh[KB];
+        float lo = zs[0][0][e][tl], hi = zs[0][1][e][tl];
 #pragma unroll
-            for (int b = 0; b < KB; ++b) {
-                const int k = min(k0 + b, ksplit - 1);
-                vl[b] = part[k * (2 * 16 * TOK) + e * TOK + tl];
-                vh[b] = part[k * (2 * 16 * TOK) + 16 * TOK + e * TOK + tl];
-            }
-#pragma unroll
-            for (int b = 0; b < KB; ++b)
-                if (k0 + b < ksplit) {
-                    lo += vl[b];
-                    hi += vh[b];
-                }
+        for (int ww = 1; ww < WAVES; ++ww) {
+            lo += zs[ww][0][e][tl];
+            hi += zs[ww][1][e][tl];
         }
+        unsigned node = (unsigned)(ksplit + ks);
+        bool mine = true;
+        while (node > 1) {
+            unsigned long long *slot = slots + (size_t)(node / 2 - 1) * (16 * TOK) + idx;
+            const unsigned long long packed =
+                ((unsigned long long)__float_as_uint(hi) << 32) |
+                (unsigned long long)(__float_as_uint(lo) + 1u);
+            const unsigned long long old =
+                __hip_atomic_exchange(slot, packed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (old == 0ull) {
+                mine = false;          // the sibling finishes this node
+                break;
+            }
+            lo += __uint_as_float((unsigned)old - 1u);
+            hi += __uint_as_float((unsigned)(old >> 32));
+            __hip_atomic_store(slot, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            node /= 2;
+        }
+        const int t = t0 + tl;
+        if (!mine || t >= a.n_tok)
+            continue;
         const int pos = a.start_pos + t;
         if (kind == 0)
             rope_pair(lo, hi, 16 * pair + e, DH, pos, a.rope_base);
@@ -232,22 +224,33 @@ PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim) {
     p.token_blocks = std::max(1, cdiv(n_tok, 16 * p.nbt));
     p.units = n_kv_heads * 2 * (head_dim / 32);
     const int chunks = d_in / 32;
-    // enough k-slices to cover the chip, each wave owning 1..8 chunks
-    int ks = std::max(1, cdiv(kPfTargetWorkgroups, p.units * p.token_blocks));
-    ks = std::min(ks, std::max(1, chunks / 4));                   // >= 4 chunks per slice
-    ks = std::max(ks, cdiv(chunks, 4 * kPfMaxChunksPerWave));    // <= 32 chunks per slice
+    // a power-of-two number of k-slices: enough to cover the chip, at least
+    // 4 chunks per slice.  units * token_blocks * (ksplit - 1) < 512, so the
+    // exchange slots stay under 512 * 1024 pairs = the 4 MiB zero block.
+    int ks = 1;
+    while (ks * 2 * p.units * p.token_blocks <= kPfTargetWorkgroups && chunks / (ks * 2) >= 4)
+        ks *= 2;
     p.chunks_per_split = cdiv(chunks, ks);
-    p.ksplit = cdiv(chunks, p.chunks_per_split);
+    p.ksplit = ks;
     return p;
+}
+
+// Exchange slots: (ksplit - 1) internal tree nodes x 16*16*nbt pairs per
+// (unit, token block), inside the workspace's zero block.
+static size_t prefill_slot_bytes(const PrefillPlan &p) {
+    return (size_t)p.units * p.token_blocks * (p.ksplit - 1) * (16 * 16 * p.nbt) *
+           sizeof(unsigned long long);
+}
+
+bool prefill_fits(int n_tok, int d_in, int n_kv_heads, int head_dim) {
+    return prefill_slot_bytes(plan_prefill(n_tok, d_in, n_kv_heads, head_dim)) <= kCounterBytes;
 }
 
 size_t prefill_workspace_bytes(wf_dtype_t dt, int n_tok, int d_in, int n_kv_heads,
                                int head_dim) {
     if (dt != WF_BF16 || n_tok == 0)
         return 0;
-    const PrefillPlan p = plan_prefill(n_tok, d_in, n_kv_heads, head_dim);
-    const size_t part = (size_t)p.units * p.token_blocks * p.ksplit * 2 * 16 * (16 * p.nbt) * sizeof(float);
-    return kCounterBytes + part;
+    return kCounterBytes;
 }
 
 wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
@@ -260,13 +263,11 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
     if (dt == WF_BF16) {
         const PrefillPlan p = plan_prefill(n_tok, d_in, n_kv_heads, head_dim);
         a.chunks_per_split = p.chunks_per_split;
-        a.ws = reinterpret_cast<float *>(static_cast<char *>(workspace) + kCounterBytes);
+        a.slots = static_cast<unsigned long long *>(workspace);
         dim3 grid(p.units, p.ksplit, p.token_blocks), block(256);
-        dim3 fgrid(p.units, p.token_blocks);
 #define WF_PF_CASE(DHV, NBV)                                                        \
     if (head_dim == DHV && p.nbt == NBV) {                                          \
-        prefill_partial_bf16<DHV, NBV><<<grid, block, 0, stream>>>(a);              \
-        prefill_finish_bf16<DHV, NBV><<<fgrid, block, 0, stream>>>(a, p.ksplit);    \
+        prefill_bf16<DHV, NBV><<<grid, block, 0, stream>>>(a);                      \
     } else
         WF_PF_CASE(128, 1) WF_PF_CASE(128, 2) WF_PF_CASE(128, 3) WF_PF_CASE(128, 4)
         WF_PF_CASE(64, 1) WF_PF_CASE(64, 2) WF_PF_CASE(64, 3) WF_PF_CASE(64, 4)

@@ -12,11 +12,12 @@
 
 namespace wf {
 
-// Every workspace starts with a fixed block of arrival counters (the same
-// offset and size for the three kinds of call), followed by that call's
-// partial results.  Calls leave the counters at zero, so a workspace zeroed
-// once can be reused by any later call, whatever its kind or sizes.
-constexpr size_t kCounterBytes = 65536;
+// Every workspace starts with a fixed zero block (the same offset and size
+// for the three kinds of call) holding arrival counters and exchange slots,
+// followed by that call's partial results.  Calls leave the block at zero,
+// so a workspace zeroed once can be reused by any later call, whatever its
+// kind or sizes.
+constexpr size_t kCounterBytes = (size_t)4 << 20;
 constexpr int kCounterSlots = static_cast<int>(kCounterBytes / sizeof(unsigned));
 
 struct AttnPlan {
@@ -59,6 +60,8 @@ struct PrefillPlan {
 PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim);
 size_t prefill_workspace_bytes(wf_dtype_t dt, int n_tok, int d_in, int n_kv_heads,
                                int head_dim);
+// Whether the bf16 plan's exchange slots fit the workspace zero block.
+bool prefill_fits(int n_tok, int d_in, int n_kv_heads, int head_dim);
 wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            const void *w_v, void *k_cache, void *v_cache,
                            int n_tok, int start_pos, int cap, int d_in,

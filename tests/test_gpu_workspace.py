@@ -15,7 +15,7 @@ pytestmark = pytest.mark.gpu
 
 wf = pytest.importorskip("paper_2606_07710_amd")
 DEV = "cuda"
-COUNTER_BLOCK = 65536
+COUNTER_BLOCK = 4 << 20
 
 
 def _lm(h, w, logits, draft, ws):
