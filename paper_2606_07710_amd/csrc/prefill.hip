@@ -16,6 +16,8 @@
 // cache pair.  Tokens are the MFMA N dimension (blocks of 16).
 // RoPE angles are formed in fp64: at positions ~65K an fp32 angle would be
 // off by ~4e-3 rad.
+#include <cmath>
+
 #include "wf_api_internal.h"
 #include "wf_device.h"
 
@@ -24,7 +26,8 @@ namespace wf {
 namespace {
 
 constexpr int kPfMaxChunksPerWave = 8;   // 32-wide chunks per wave per k-slice
-constexpr int kPfTargetWorkgroups = 512;
+constexpr int kPfTargetWorkgroups = 256;
+constexpr int kMaxHalfDim = 64;          // head_dim <= 128
 
 struct PrefillParams {
     const void *x;
@@ -33,18 +36,22 @@ struct PrefillParams {
     void *k_cache;
     void *v_cache;
     int n_tok, start_pos, cap, d_in, n_kv_heads;
-    double rope_base;
+    double theta[kMaxHalfDim];  // RoPE frequencies base^(-2i/D), i < D/2
     unsigned long long *slots; // bf16 path: k-slice exchange slots, zero between calls
     int chunks_per_split;      // 32-wide chunks of d_in per k-slice
 };
 
-__device__ __forceinline__ void rope_pair(float &lo, float &hi, int i, int dh,
-                                          int pos, double base) {
-    const double theta = pow(base, -2.0 * (double)i / (double)dh);
+// Rotation of the pair (lo, hi) = (k_i, k_{i+D/2}) by pos * theta_i, with
+// theta_i = base^(-2i/D) precomputed on the host in fp64.  The angle is
+// formed and reduced modulo 2*pi in fp64 (at pos ~65K an fp32 angle would be
+// off by ~4e-3 rad); the reduced angle, in [-pi, pi], is exact to ~1e-16 and
+// its sine and cosine are taken in fp32 (~1e-7).
+__device__ __forceinline__ void rope_pair(float &lo, float &hi, double theta, int pos) {
+    constexpr double kTwoPi = 6.283185307179586;
     const double phi = (double)pos * theta;
-    double s, c;
-    sincos(phi, &s, &c);
-    const float cf = (float)c, sf = (float)s;
+    const double r = fma(-rint(phi / kTwoPi), kTwoPi, phi);
+    float sf, cf;
+    sincosf((float)r, &sf, &cf);
     const float a = lo, b = hi;
     lo = a * cf - b * sf;
     hi = b * cf + a * sf;
@@ -179,7 +186,7 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
             continue;
         const int pos = a.start_pos + t;
         if (kind == 0)
-            rope_pair(lo, hi, 16 * pair + e, DH, pos, a.rope_base);
+            rope_pair(lo, hi, a.theta[16 * pair + e], pos);
         uint16_t *row = cache + ((size_t)g * a.cap + pos) * DH;
         row[16 * pair + e] = f32_to_bf16(lo);
         row[DH / 2 + 16 * pair + e] = f32_to_bf16(hi);
@@ -208,7 +215,7 @@ __global__ __launch_bounds__(256) void prefill_f32(PrefillParams a, int dh) {
     }
     const int pos = a.start_pos + t;
     if (kind == 0)
-        rope_pair(lo, hi, i, dh, pos, a.rope_base);
+        rope_pair(lo, hi, a.theta[i], pos);
     float *row = static_cast<float *>(kind ? a.v_cache : a.k_cache) + ((size_t)g * a.cap + pos) * dh;
     row[i] = lo;
     row[i + half] = hi;
@@ -259,7 +266,9 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            int n_kv_heads, int head_dim, double rope_base,
                            void *workspace, hipStream_t stream) {
     PrefillParams a{x, w_k, w_v, k_cache, v_cache, n_tok, start_pos, cap, d_in,
-                    n_kv_heads, rope_base, nullptr, 0};
+                    n_kv_heads, {}, nullptr, 0};
+    for (int i = 0; i < head_dim / 2; ++i)
+        a.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
     if (dt == WF_BF16) {
         const PrefillPlan p = plan_prefill(n_tok, d_in, n_kv_heads, head_dim);
         a.chunks_per_split = p.chunks_per_split;
