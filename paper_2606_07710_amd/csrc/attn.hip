@@ -129,8 +129,10 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     constexpr int OST = DH + 4;
     constexpr int REGION_BYTES = ROWS_WG * OST * 4;
     constexpr int MAX_RS = STAGE_BYTES > REGION_BYTES ? STAGE_BYTES : REGION_BYTES;
-    // two regions (one merge round for two streams) when they fit
-    constexpr int NREG = (KS >= 2 && 2 * MAX_RS + (NBUF - 2) * STAGE_BYTES +
+    // Streams 1..KS-1 hand their accumulators to stream 0 through NREG
+    // regions: two (fewer merge rounds) when there are two or more such
+    // streams and the regions fit.
+    constexpr int NREG = (KS >= 3 && 2 * MAX_RS + (NBUF - 2) * STAGE_BYTES +
                           KS * ROWS_WG * 8 + 16 <= 160 * 1024) ? 2 : 1;
     constexpr int RING0_BYTES = STAGE_BYTES > REGION_BYTES ? STAGE_BYTES : REGION_BYTES;
     constexpr int RING1_BYTES = NREG < 2 ? STAGE_BYTES : RING0_BYTES;
@@ -499,9 +501,11 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     }
     __syncthreads();
 
-    // ---- merge the KS streams of each row through LDS ----------------------
-    // Stream s adds into region s % NREG in round s / NREG (round 0 stores),
-    // and the partial write below sums the regions -- a fixed order.
+    // ---- merge the KS streams of each row ------------------------------------
+    // Stream s >= 1 adds its rescaled accumulator into region (s-1) % NREG in
+    // round (s-1) / NREG (round 0 stores); stream 0 then adds the regions to
+    // its own registers, in region order, and writes the partial straight
+    // from registers -- a fixed summation order.
     auto oreg = [&](int r) { return (WF_LDS(float) *)(r ? ring1 : ring0); };
     float fac[NBW];
 #pragma unroll
@@ -514,43 +518,54 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
         const float muse = (mm == -INFINITY) ? 0.f : mm;
         fac[nb] = (mref[nb] == -INFINITY) ? 0.f : fast_exp2((mref[nb] - muse) * sl2);
     }
+    if constexpr (KS > 1) {
+        constexpr int ROUNDS = (KS - 1 + NREG - 1) / NREG;
 #pragma unroll 1
-    for (int round = 0; round < KS / NREG; ++round) {
-        if (stream / NREG == round) {
-            WF_LDS(float) *reg = oreg(stream % NREG);
+        for (int round = 0; round < ROUNDS; ++round) {
+            if (stream >= 1 && (stream - 1) / NREG == round) {
+                WF_LDS(float) *reg = oreg((stream - 1) % NREG);
 #pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
+                for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
-                for (int md = 0; md < MD; ++md) {
-                    WF_LDS(float) *dst = reg + (rgi * ROWS_W + nb * 16 + m16) * OST + md * 16 + 4 * c4;
-                    f32x4 v = o[md][nb] * fac[nb];
-                    if (round > 0)
-                        v += *(WF_LDS(f32x4) *)dst;
-                    *(WF_LDS(f32x4) *)dst = v;
-                }
+                    for (int md = 0; md < MD; ++md) {
+                        WF_LDS(float) *dst = reg + (rgi * ROWS_W + nb * 16 + m16) * OST + md * 16 + 4 * c4;
+                        f32x4 v = o[md][nb] * fac[nb];
+                        if (round > 0)
+                            v += *(WF_LDS(f32x4) *)dst;
+                        *(WF_LDS(f32x4) *)dst = v;
+                    }
+            }
+            __syncthreads();
         }
-        __syncthreads();
     }
+    if (stream != 0)
+        return;
 
-    // ---- write the workgroup partial ----------------------------------------
+    // ---- write the workgroup partial (stream 0 waves) ------------------------
+    // Lane (m16, c4) holds dims md*16 + 4*c4 .. +3 of row nb*16 + m16.
+    constexpr int NR = KS - 1 < NREG ? KS - 1 : NREG;   // regions in use
     const int pairs = a.gamma * a.n_q_heads;
-    for (int idx = threadIdx.x; idx < ROWS_WG * (DH / 4); idx += blockDim.x) {
-        const int rl = idx / (DH / 4);
-        const int d4 = idx % (DH / 4);
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        const int rl = rgi * ROWS_W + nb * 16 + m16;
         const int r = rgw * ROWS_WG + rl;
         if (r >= a.rows)
             continue;
         const int i = r / a.group;
         const int h = g * a.group + (r % a.group);
         const size_t pr = (size_t)split * pairs + (size_t)i * a.n_q_heads + h;
-        f32x4 v = ((WF_LDS(const f32x4) *)(oreg(0) + rl * OST))[d4];
-        if (NREG > 1)
-            v += ((WF_LDS(const f32x4) *)(oreg(1) + rl * OST))[d4];
-        // bf16 partials: the split merge weighs them by at most 1 and the
-        // output is rounded to bf16 anyway
-        const uint2 pk = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-        reinterpret_cast<uint2 *>(static_cast<uint16_t *>(a.ws_o) + pr * DH)[d4] = pk;
-        if (d4 == 0) {
+        uint2 *dst = reinterpret_cast<uint2 *>(static_cast<uint16_t *>(a.ws_o) + pr * DH);
+#pragma unroll
+        for (int md = 0; md < MD; ++md) {
+            f32x4 v = o[md][nb] * fac[nb];
+#pragma unroll
+            for (int rr = 0; rr < NR; ++rr)
+                v += *(WF_LDS(const f32x4) *)(oreg(rr) + rl * OST + md * 16 + 4 * c4);
+            // bf16 partials: the split merge weighs them by at most 1 and
+            // the output is rounded to bf16 anyway
+            dst[md * 4 + c4] = uint2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        }
+        if (c4 == 0) {
             float mm = -INFINITY, ll = 0.f;
 #pragma unroll
             for (int st = 0; st < KS; ++st)
