@@ -17,6 +17,13 @@ Paper: arXiv 2606.07710 (WhiFlash).  What each call computes:
                       H = -sum p log p of the softmax distribution.
   accept           -- greedy acceptance of the longest matching draft prefix
                       plus the Sec. 3.3.1 entropy routing rule (H > tau -> AR).
+  verify_attn_mask -- tree verification (Sec. 3.1 draft trees, Sec. 3.2
+                      parallel verification): row i sees the cache, itself
+                      and the block rows its mask bits name.
+  accept_tree      -- greedy acceptance of the deepest accepted tree node
+                      and its root path, plus the same entropy route.
+  kv_compact_path  -- after tree acceptance, the accepted path's K/V rows
+                      move to consecutive cache rows after the prefix.
   layer_forward    -- a full single attention layer, used to pin that KV-only
                       prefill yields the cache a full forward would.
 """
@@ -55,12 +62,16 @@ def _load():
     lib.wfref_lmhead_rows.argtypes = [_i, _p, _p, _p, _i, _i, _i, _p, _p, _p,
                                       _p]
     lib.wfref_accept.argtypes = [_p, _p, _p, _i, _d, _p, _p]
+    lib.wfref_verify_attn_mask.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i,
+                                           _i, _i, _i, _d]
+    lib.wfref_accept_tree.argtypes = [_p, _p, _p, _p, _i, _d, _p, _p, _p]
     lib.wfref_rope_inplace.argtypes = [_p, _i, _d, _d]
     lib.wfref_rope_inplace.restype = None
     lib.wfref_layer_forward.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i, _i,
                                         _i, _i, _d, _d, _p, _p, _p, _p, _p]
     for name in ("wfref_verify_attn", "wfref_verify_attn_rows",
                  "wfref_kv_only_prefill", "wfref_lmhead_rows", "wfref_accept",
+                 "wfref_verify_attn_mask", "wfref_accept_tree",
                  "wfref_layer_forward"):
         getattr(lib, name).restype = _i
     _lib = lib
@@ -193,6 +204,67 @@ def accept(argmax, entropy, draft, tau):
                           float(tau), _ptr(out3), ctypes.byref(ht))
     _check(rc, "accept")
     return int(out3[0]), int(out3[1]), int(out3[2]), float(ht.value)
+
+
+def verify_attn_mask(q, k_cache, v_cache, ctx_len, mask, scale=None):
+    """Tree verification attention: mask [gamma] uint64, bit j of mask[i]
+    lets row i see block row j (it always sees itself) -> fp64 out."""
+    lib = _load()
+    q, code = _arr(q)
+    k_cache, c2 = _arr(k_cache)
+    v_cache, c3 = _arr(v_cache)
+    if not (code == c2 == c3):
+        raise TypeError("q and caches must share a storage type")
+    gamma, hq, dh = q.shape
+    hkv, cap, dh2 = k_cache.shape
+    if dh2 != dh or v_cache.shape != k_cache.shape:
+        raise ValueError("shape mismatch")
+    m = np.ascontiguousarray(np.asarray(mask, np.uint64))
+    if m.shape != (gamma,):
+        raise ValueError("mask must hold gamma words")
+    if scale is None:
+        scale = 1.0 / np.sqrt(dh)
+    out = np.empty((gamma, hq, dh), np.float64)
+    rc = lib.wfref_verify_attn_mask(code, _ptr(q), _ptr(k_cache),
+                                    _ptr(v_cache), _ptr(out), _ptr(m), gamma,
+                                    int(ctx_len), cap, hq, hkv, dh,
+                                    float(scale))
+    _check(rc, "verify_attn_mask")
+    return out
+
+
+def accept_tree(argmax, entropy, tokens, parents, tau):
+    """-> (n, bonus, route, deepest node, H_t, path [gamma] int32)."""
+    lib = _load()
+    argmax = np.ascontiguousarray(argmax, np.int32)
+    entropy = np.ascontiguousarray(entropy, np.float64)
+    gamma = argmax.shape[0]
+    tok = np.ascontiguousarray(tokens, np.int32)
+    par = np.ascontiguousarray(parents, np.int32)
+    if tok.shape != (gamma,) or par.shape != (gamma,):
+        raise ValueError("tokens and parents must hold gamma entries")
+    out4 = np.empty(4, np.int32)
+    path = np.empty(gamma, np.int32)
+    ht = ctypes.c_double()
+    rc = lib.wfref_accept_tree(_ptr(argmax), _ptr(entropy), _ptr(tok),
+                               _ptr(par), gamma, float(tau), _ptr(out4),
+                               _ptr(path), ctypes.byref(ht))
+    _check(rc, "accept_tree")
+    return (int(out4[0]), int(out4[1]), int(out4[2]), int(out4[3]),
+            float(ht.value), path)
+
+
+def kv_compact_path(k_cache, v_cache, ctx_len, path, n):
+    """Caches [Hkv][cap][D]: block row path[t] (cache row ctx_len + path[t])
+    moves to block row t for t = 0..n; every other row is unchanged.
+    Returns new arrays."""
+    k = np.array(k_cache, copy=True)
+    v = np.array(v_cache, copy=True)
+    src = [ctx_len + int(path[t]) for t in range(n + 1)]
+    dst = [ctx_len + t for t in range(n + 1)]
+    k[:, dst] = np.asarray(k_cache)[:, src]
+    v[:, dst] = np.asarray(v_cache)[:, src]
+    return k, v
 
 
 def rope(v, pos, base):

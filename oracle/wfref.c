@@ -194,6 +194,101 @@ int wfref_verify_attn_rows(int dtype, const void *q, const void *k_cache,
 }
 
 /* ------------------------------------------------------------------------ *
+ * Tree verification.  An autoregressive drafter proposes a tree of
+ * candidates rather than a chain (Sec. 3.1; the EAGLE-3 setting of App. A:
+ * depth 8, top-k 10, 60 draft tokens), and the target checks every node in
+ * the same single parallel pass (Sec. 3.2).
+ *
+ * Block row i is tree node i.  Row 0 is the root (the last committed
+ * token); every other node's parent has a smaller index.  Row i attends to
+ * the ctx_len cached keys and to the block keys ctx_len + j of the nodes j
+ * it may see: j == i, or bit j of mask[i] set (0 <= j < gamma <= 64).
+ * With mask[i] = the ancestors of node i this is ordinary causal attention
+ * along node i's root path; for a chain (node j's parent is j-1) it is the
+ * block-causal verify attention above.
+ *
+ *   keys(i) = {0 .. ctx_len-1} U {ctx_len + j : j == i or mask[i] bit j}
+ *   out[i,h,:] = sum_{j in keys(i)} softmax_j(scale <q[i,h], K[g,j]>) V[g,j]
+ * ------------------------------------------------------------------------ */
+static void attend_mask_one(int dtype, const void *q, const void *k_cache,
+                            const void *v_cache, int ctx_len, int cap,
+                            int gamma, int n_q_heads, int n_kv_heads,
+                            int head_dim, double scale, uint64_t row_mask,
+                            int i, int h, int *keys, double *scores,
+                            double *out_row)
+{
+    const int group = n_q_heads / n_kv_heads;
+    const int g = h / group;
+    const size_t q_off = ((size_t)i * n_q_heads + h) * head_dim;
+    const size_t kv_head_off = (size_t)g * cap * head_dim;
+
+    int n_keys = 0;
+    for (int j = 0; j < ctx_len; ++j)
+        keys[n_keys++] = j;
+    for (int j = 0; j < gamma; ++j)
+        if (j == i || ((row_mask >> j) & 1u))
+            keys[n_keys++] = ctx_len + j;
+
+    double smax = -INFINITY;
+    for (int t = 0; t < n_keys; ++t) {
+        const size_t krow = kv_head_off + (size_t)keys[t] * head_dim;
+        double dot = 0.0;
+        for (int d = 0; d < head_dim; ++d)
+            dot += elem(q, dtype, q_off + d) * elem(k_cache, dtype, krow + d);
+        scores[t] = scale * dot;
+        if (scores[t] > smax)
+            smax = scores[t];
+    }
+    double denom = 0.0;
+    for (int t = 0; t < n_keys; ++t) {
+        scores[t] = exp(scores[t] - smax);
+        denom += scores[t];
+    }
+    for (int d = 0; d < head_dim; ++d)
+        out_row[d] = 0.0;
+    for (int t = 0; t < n_keys; ++t) {
+        const double p = scores[t] / denom;
+        const size_t vrow = kv_head_off + (size_t)keys[t] * head_dim;
+        for (int d = 0; d < head_dim; ++d)
+            out_row[d] += p * elem(v_cache, dtype, vrow + d);
+    }
+}
+
+int wfref_verify_attn_mask(int dtype, const void *q, const void *k_cache,
+                           const void *v_cache, double *out,
+                           const uint64_t *mask, int gamma, int ctx_len,
+                           int cap, int n_q_heads, int n_kv_heads,
+                           int head_dim, double scale)
+{
+    if (!attn_args_ok(dtype, gamma, ctx_len, cap, n_q_heads, n_kv_heads,
+                      head_dim) || gamma > 64 || !mask)
+        return 1;
+    const int n_pairs = gamma * n_q_heads;
+    int fail = 0;
+#pragma omp parallel
+    {
+        double *scores = malloc(sizeof(double) * (size_t)(ctx_len + gamma));
+        int *keys = malloc(sizeof(int) * (size_t)(ctx_len + gamma));
+        if (!scores || !keys) {
+#pragma omp atomic write
+            fail = 1;
+        } else {
+#pragma omp for schedule(dynamic, 1)
+            for (int pr = 0; pr < n_pairs; ++pr) {
+                const int i = pr / n_q_heads, h = pr % n_q_heads;
+                attend_mask_one(dtype, q, k_cache, v_cache, ctx_len, cap,
+                                gamma, n_q_heads, n_kv_heads, head_dim, scale,
+                                mask[i], i, h, keys, scores,
+                                out + (size_t)pr * head_dim);
+            }
+        }
+        free(scores);
+        free(keys);
+    }
+    return fail ? 2 : 0;
+}
+
+/* ------------------------------------------------------------------------ *
  * Rotary position embedding, rotate-half pairing (the paper names no
  * variant; this is the pairing of the Qwen3 / Llama-3.1 targets it uses).
  * For i < head_dim/2, theta_i = base^(-2i/head_dim), phi = pos * theta_i:
@@ -351,6 +446,61 @@ int wfref_accept(const int32_t *argmax, const double *entropy,
     out3[2] = (entropy[n] > tau) ? 1 : 0;
     if (h_t)
         *h_t = entropy[n];
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ *
+ * Greedy acceptance on a draft tree and the entropy route (the tree of
+ * Sec. 3.1 verified as in Sec. 3.2; rule of Sec. 3.3.1).
+ *   The root (node 0) is accepted.  Node j >= 1 with parent p = parents[j]
+ *   is accepted iff 0 <= p < j, p is accepted and tokens[j] == argmax[p]
+ *   (the target, having seen p's path, would itself emit tokens[j]).  A node
+ *   whose parent index is out of range is never accepted.
+ *   depth(0) = 0, depth(j) = depth(parents[j]) + 1.
+ *   b     = the accepted node of greatest depth (lowest index among equals)
+ *   n     = depth(b), the number of accepted drafts
+ *   bonus = argmax[b]; H_t = entropy[b]; route = H_t > tau (1 = AR)
+ * out4 = {n, bonus, route, b}; path[t] = the node at depth t on b's root
+ * path for t <= n, -1 for t > n; *h_t receives H_t.  tokens[0] and
+ * parents[0] are not read.
+ * ------------------------------------------------------------------------ */
+int wfref_accept_tree(const int32_t *argmax, const double *entropy,
+                      const int32_t *tokens, const int32_t *parents,
+                      int gamma, double tau, int32_t *out4, int32_t *path,
+                      double *h_t)
+{
+    if (gamma < 1 || gamma > 64 || (gamma > 1 && (!tokens || !parents)))
+        return 1;
+    int accepted[64], depth[64];
+    accepted[0] = 1;
+    depth[0] = 0;
+    for (int j = 1; j < gamma; ++j) {
+        const int p = parents[j];
+        if (p < 0 || p >= j) {
+            accepted[j] = 0;
+            depth[j] = 0;
+            continue;
+        }
+        depth[j] = depth[p] + 1;
+        accepted[j] = accepted[p] && tokens[j] == argmax[p];
+    }
+    int b = 0;
+    for (int j = 1; j < gamma; ++j)
+        if (accepted[j] && depth[j] > depth[b])
+            b = j;
+    const int n = depth[b];
+    for (int t = 0; t < gamma; ++t)
+        path[t] = -1;
+    for (int v = b, t = n; t >= 0; --t) {
+        path[t] = v;
+        v = (t > 0) ? parents[v] : v;
+    }
+    out4[0] = n;
+    out4[1] = argmax[b];
+    out4[2] = (entropy[b] > tau) ? 1 : 0;
+    out4[3] = b;
+    if (h_t)
+        *h_t = entropy[b];
     return 0;
 }
 

@@ -67,3 +67,41 @@ def test_to_oracle_keeps_bf16_bits():
     assert a.dtype == np.uint16
     back = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16)
     assert torch.equal(back, t)
+
+
+def test_draft_tree_shape():
+    """EAGLE-3 shape (App. A): 60 drafts below the root, depth 8, at most 10
+    children per node, breadth-first order (every parent precedes its
+    children, depths never decrease)."""
+    par = W.draft_tree(seed=W.stream_seed(6000, "tree"))
+    assert par.shape == (61,) and par[0] == -1
+    depth = np.zeros(61, np.int64)
+    for j in range(1, 61):
+        assert 0 <= par[j] < j
+        depth[j] = depth[par[j]] + 1
+    assert np.all(np.diff(depth) >= 0)
+    assert [int((depth == d).sum()) for d in range(1, 9)] == list(W.EAGLE_LEVELS)
+    counts = np.bincount(par[1:], minlength=61)
+    assert counts.max() <= W.EAGLE_TOP_K
+
+
+def test_ancestor_masks_mark_root_paths():
+    par = np.array([-1, 0, 0, 1, 3, 2], np.int32)
+    m = W.ancestor_masks(par)
+    assert [bin(int(x))[2:][::-1] for x in m] == [
+        "1", "11", "101", "1101", "11011", "101001"]
+
+
+def test_tree_tokens_accept_exactly_k():
+    par = W.draft_tree(seed=5)
+    ref = np.arange(61, dtype=np.int32) * 7 % 1000
+    for k in (0, 2, 5, 9):
+        tok = W.tree_tokens(ref, par, k, 1000, seed=k)
+        accepted = {0}
+        for j in range(1, 61):
+            if par[j] in accepted and tok[j] == ref[par[j]]:
+                accepted.add(j)
+        depth = {0: 0}
+        for j in range(1, 61):
+            depth[j] = depth[int(par[j])] + 1
+        assert max(depth[j] for j in accepted) == min(k, 8)

@@ -62,6 +62,13 @@ class Workload:
     fixed_prefix: int | None
     router_logits: bool      # config with logits-only router rows
     description: str = field(default="", compare=False)
+    # draft-tree verification: nodes per depth below the root (empty: the
+    # block is a chain or a diffusion block, verified block-causally)
+    tree_levels: tuple = ()
+
+    @property
+    def is_tree(self) -> bool:
+        return len(self.tree_levels) > 0
 
     @property
     def cap(self) -> int:
@@ -111,7 +118,7 @@ class Workload:
 
 
 def _qwen_like(cfg, name, n_layers, hidden, hq, ctx, gamma, n_pre, p, desc,
-               router=False):
+               router=False, tree_levels=()):
     return Workload(cfg=cfg, name=name, dtype="bf16", n_layers=n_layers,
                     hidden=hidden, n_q_heads=hq, n_kv_heads=8, head_dim=128,
                     ctx_len=ctx, gamma=gamma, vocab=151936, rope_base=1e6,
@@ -119,7 +126,15 @@ def _qwen_like(cfg, name, n_layers, hidden, hq, ctx, gamma, n_pre, p, desc,
                     prefill_cap=ctx + gamma + n_pre,
                     separate_drafter_cache=False, act_std=1.0, w_std=0.02,
                     qkv_std=0.02 * math.sqrt(hidden), accept_p=p,
-                    fixed_prefix=None, router_logits=router, description=desc)
+                    fixed_prefix=None, router_logits=router, description=desc,
+                    tree_levels=tuple(tree_levels))
+
+
+# Nodes per depth of the synthetic EAGLE-3-shaped draft tree: depth 8 and
+# 60 draft tokens (App. A drafter settings), at most 10 children per node
+# (top-k 10), thinning with depth as a top-scored expansion does.
+EAGLE_LEVELS = (10, 10, 10, 8, 8, 6, 4, 4)
+EAGLE_TOP_K = 10
 
 
 CONFIGS = {
@@ -144,13 +159,19 @@ CONFIGS = {
     5: _qwen_like(5, "32b-block16-ctx64k", 64, 5120, 64, 65536, 16, 32, 0.3,
                   "32B shapes, 64 layers, ctx 65536, gamma 16 block-causal, "
                   "32 catch-up tokens per layer, vocab 151936"),
+    6: _qwen_like(6, "8b-tree61-ctx8k", 36, 4096, 32, 8192,
+                  1 + sum(EAGLE_LEVELS), 0, 0.3,
+                  "8B shapes, 36 layers, ctx 8192, EAGLE-3-shaped draft tree "
+                  "(root + 60 nodes, depth 8, top-k 10) verified with an "
+                  "ancestor mask, vocab 151936", tree_levels=EAGLE_LEVELS),
 }
 
 # Fixed tensor identifiers: each named tensor (and layer) gets its own stream.
 TENSOR_IDS = {"q": 1, "k_cache": 2, "v_cache": 3, "x": 4, "w_k": 5, "w_v": 6,
               "h": 7, "w_lm": 8, "router_logits": 9, "router_rows": 10,
               "router_boost": 11, "drafts": 12, "prefix": 13,
-              "drafter_k_cache": 14, "drafter_v_cache": 15}
+              "drafter_k_cache": 14, "drafter_v_cache": 15, "tree": 16,
+              "tree_tokens": 17}
 
 
 def stream_seed(master: int, tensor: str | int, layer: int = 0) -> int:
@@ -228,6 +249,84 @@ def make_drafts(ref_argmax, k: int, vocab: int, seed: int) -> np.ndarray:
         r = int(rng.integers(0, vocab - 1))
         d[k] = r if r < ref[k] else r + 1   # uniform over ids != ref[k]
     return d.astype(np.int32)
+
+
+def draft_tree(levels=EAGLE_LEVELS, top_k=EAGLE_TOP_K, seed=0) -> np.ndarray:
+    """Parents [1 + sum(levels)] int32 of a draft tree in breadth-first
+    order: node 0 is the root (parent -1) and depth d holds levels[d-1]
+    nodes, each the child of a depth d-1 node with at most top_k children
+    per node.  A node's children are numbered consecutively, in the order of
+    their parents, so every parent precedes its children.  Parents are drawn
+    with weights 1/(rank+1) over the previous depth, favouring its earlier
+    (higher-ranked) nodes."""
+    rng = np.random.default_rng(seed)
+    parents = [-1]
+    prev = [0]
+    for count in levels:
+        if count > top_k * len(prev):
+            raise ValueError("level larger than top_k children per node allow")
+        load = np.zeros(len(prev), np.int64)
+        picks = []
+        for _ in range(count):
+            wts = np.array([0.0 if load[r] >= top_k else 1.0 / (r + 1)
+                            for r in range(len(prev))])
+            r = int(rng.choice(len(prev), p=wts / wts.sum()))
+            load[r] += 1
+            picks.append(r)
+        picks.sort()
+        first = len(parents)
+        parents.extend(prev[r] for r in picks)
+        prev = list(range(first, len(parents)))
+    return np.asarray(parents, np.int32)
+
+
+def ancestor_masks(parents) -> np.ndarray:
+    """mask[i] (uint64): bit j set iff node j is node i or one of its
+    ancestors -- the rows of the block that node i's query may see."""
+    parents = np.asarray(parents, np.int64)
+    gamma = parents.shape[0]
+    if gamma > 64:
+        raise ValueError("at most 64 nodes")
+    masks = np.zeros(gamma, np.uint64)
+    for i in range(gamma):
+        m, v = 0, i
+        while v >= 0:
+            m |= 1 << v
+            v = int(parents[v]) if v > 0 else -1
+        masks[i] = np.uint64(m)
+    return masks
+
+
+def tree_tokens(ref_argmax, parents, k: int, vocab: int, seed: int) -> np.ndarray:
+    """Node tokens [gamma] int32 for a tree whose accepted path has exactly
+    min(k, depth of the designated path) drafts.  The designated path starts
+    at the root and follows the lowest-index child down to a leaf.  Its
+    first k nodes carry the reference argmax of their parent; every other
+    child of the root and of those k nodes carries an id different from its
+    parent's reference argmax; all remaining nodes carry uniform ids.
+    tokens[0] (the root) is 0."""
+    ref = np.asarray(ref_argmax, np.int64)
+    parents = np.asarray(parents, np.int64)
+    gamma = parents.shape[0]
+    rng = np.random.default_rng(seed)
+    tok = rng.integers(0, vocab, size=gamma, dtype=np.int64)
+    tok[0] = 0
+    children = [[] for _ in range(gamma)]
+    for j in range(1, gamma):
+        children[int(parents[j])].append(j)
+    path = [0]
+    while children[path[-1]]:
+        path.append(min(children[path[-1]]))
+    k = min(k, len(path) - 1)
+    for t in range(k + 1):
+        node = path[t]
+        for c in children[node]:
+            if t < k and c == path[t + 1]:
+                tok[c] = ref[node]
+            else:
+                r = int(rng.integers(0, vocab - 1))
+                tok[c] = r if r < ref[node] else r + 1
+    return tok.astype(np.int32)
 
 
 def prefix_len(w: Workload, draft_seed: int) -> int:
