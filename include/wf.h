@@ -18,6 +18,15 @@
  *   wf_lmhead_accept_entropy  LM head reduced to argmax and entropy per row,
  *                             then greedy acceptance and the entropy route
  *
+ * and the tree-shaped variant of the step, for autoregressive drafters that
+ * propose a tree of candidates (Sec. 3.1; EAGLE-3 trees of depth 8, top-k
+ * 10, 60 draft tokens, App. A):
+ *
+ *   wf_verify_attn_tree       verify attention under a per-row ancestor mask
+ *   wf_lmhead_accept_tree     LM head as above, then the deepest accepted
+ *                             tree node, its root path and the route
+ *   wf_kv_compact_path        moves the accepted path's K/V rows together
+ *
  * Conventions shared by every call
  *   - Every tensor pointer is DEVICE memory owned by the caller, 16-byte
  *     aligned, densely packed in the layout stated.  The library never
@@ -32,9 +41,8 @@
  *     Each starts with a 4 MiB zero block of arrival counters and exchange
  *     slots, through which workgroups of one call combine results; partial
  *     results follow that block.  Every call leaves the zero block at zero
- *     again, so a workspace zeroed once serves any later call, of any of the
- *     three kinds and any sizes.  Two calls that overlap in time must not
- *     share one.
+ *     again, so a workspace zeroed once serves any later call, of any kind
+ *     and any sizes.  Two calls that overlap in time must not share one.
  *   - Reductions use a fixed order, so repeated calls on the same inputs and
  *     the same split count return bit-identical results.
  *   - Row-major throughout; "[a][b][c]" lists dimensions slowest first.
@@ -108,11 +116,39 @@ wf_status_t wf_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
                            void *workspace, size_t workspace_bytes,
                            void *stream);
 
-/* Workspace for wf_verify_attn (0 for invalid arguments). */
+/* Workspace for wf_verify_attn and wf_verify_attn_tree (0 for invalid
+ * arguments). */
 size_t wf_verify_attn_workspace_bytes(wf_dtype_t dt, int32_t gamma,
                                       int32_t ctx_len, int32_t n_q_heads,
                                       int32_t n_kv_heads, int32_t head_dim,
                                       int32_t num_splits);
+
+/* ------------------------------------------------------------------------
+ * wf_verify_attn_tree -- target attention over a draft tree (Sec. 3.1: an
+ * autoregressive drafter proposes a tree of candidates; Sec. 3.2: the target
+ * verifies them all in one parallel pass).
+ *
+ * Block row i is tree node i: row 0 is the root (the last committed token)
+ * and every node's parent has a smaller index.  Node i's K/V sit at cache
+ * row ctx_len + i (its RoPE position, ctx_len + depth(i), is the caller's).
+ * Row i attends to the ctx_len cached keys and to the block keys
+ * ctx_len + j for j == i and for every j with bit j of tree_mask[i] set;
+ * with tree_mask[i] = the ancestors of i this is causal attention along
+ * node i's root path, and a chain (parent of j = j-1) gives exactly
+ * wf_verify_attn.  Bits at or above gamma are ignored.
+ *
+ * tree_mask  [gamma] uint64, device memory, 16-byte aligned.
+ * Everything else as for wf_verify_attn (same limits, same workspace
+ * query); block rows a row does not see still have to hold finite values.
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_verify_attn_tree(wf_dtype_t dt, const void *q,
+                                const void *k_cache, const void *v_cache,
+                                void *out, const uint64_t *tree_mask,
+                                int32_t gamma, int32_t ctx_len, int32_t cap,
+                                int32_t n_q_heads, int32_t n_kv_heads,
+                                int32_t head_dim, float softmax_scale,
+                                int32_t num_splits, void *workspace,
+                                size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * wf_kv_only_prefill -- lazy catch-up of a drafter's KV cache (Sec. 3.4).
@@ -191,8 +227,59 @@ wf_status_t wf_lmhead_accept_entropy(wf_dtype_t dt, const void *h,
                                      void *workspace, size_t workspace_bytes,
                                      void *stream);
 
-/* Workspace for wf_lmhead_accept_entropy (0 for invalid arguments). */
+/* Workspace for wf_lmhead_accept_entropy and wf_lmhead_accept_tree (0 for
+ * invalid arguments). */
 size_t wf_lmhead_workspace_bytes(int32_t gamma, int32_t vocab);
+
+/* ------------------------------------------------------------------------
+ * wf_lmhead_accept_tree -- LM head and greedy acceptance on a draft tree
+ * (the tree of Sec. 3.1 verified as in Sec. 3.2; route rule of Sec. 3.3.1).
+ *
+ * argmax_out and entropy_out per row (tree node) exactly as for
+ * wf_lmhead_accept_entropy.  Then: the root (node 0) is accepted; node
+ * j >= 1 is accepted iff its parent p = parents[j] satisfies 0 <= p < j, p
+ * is accepted and tokens[j] == argmax[p] (a node with an out-of-range parent
+ * is never accepted).  The accepted node b of greatest depth (lowest index
+ * among equals) ends the accepted path:
+ *   accept_out = { n = depth(b) (accepted drafts), bonus = argmax[b],
+ *                  route = entropy[b] > tau_entropy (1 = AR), b }
+ *   path_out[t] = node at depth t on b's root path for t <= n, -1 after.
+ *
+ * tokens    [gamma] int32: the drafted token of each node (tokens[0], the
+ *           root's, is not compared).
+ * parents   [gamma] int32: parent index of each node (parents[0] ignored).
+ * accept_out [4] int32; path_out [gamma] int32.  Other arguments, limits
+ * and the workspace as for wf_lmhead_accept_entropy.
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_lmhead_accept_tree(wf_dtype_t dt, const void *h,
+                                  const void *w_lm, const float *logits,
+                                  const int32_t *tokens, const int32_t *parents,
+                                  int32_t gamma, int32_t d, int32_t vocab,
+                                  float tau_entropy, int32_t *argmax_out,
+                                  float *entropy_out, int32_t *accept_out,
+                                  int32_t *path_out, void *workspace,
+                                  size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * wf_kv_compact_path -- after tree acceptance, move the accepted path's K/V
+ * rows to consecutive cache rows after the prefix, so the cache again holds
+ * the committed sequence in order (one layer's cache per call):
+ *   K[g][ctx_len + t] <- K[g][ctx_len + path[t]]   (and V), t = 0..n
+ * with n = accept[0].  Both are read on the device (accept_out and path_out
+ * of wf_lmhead_accept_tree), so the call can follow it on the same stream
+ * without a host round trip.  A path entry outside [t, gamma) leaves row t
+ * unchanged; rows other than ctx_len .. ctx_len+n are never written.
+ *
+ * k_cache, v_cache  [n_kv_heads][cap][head_dim], dtype dt.
+ * accept  device int32, at least 1 entry; path  [gamma] device int32.
+ * Limits: 1 <= gamma <= 64; ctx_len >= 0; ctx_len + gamma <= cap;
+ *         head_dim in {64, 128}.
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
+                               const int32_t *accept, const int32_t *path,
+                               int32_t gamma, int32_t ctx_len, int32_t cap,
+                               int32_t n_kv_heads, int32_t head_dim,
+                               void *stream);
 
 #ifdef __cplusplus
 }

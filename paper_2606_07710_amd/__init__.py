@@ -22,7 +22,8 @@ EXPORTED_SYMBOLS = (
     "wf_abi_version", "wf_status_string", "wf_verify_attn",
     "wf_verify_attn_workspace_bytes", "wf_kv_only_prefill",
     "wf_lmhead_accept_entropy", "wf_lmhead_workspace_bytes",
-    "wf_kv_only_prefill_workspace_bytes",
+    "wf_kv_only_prefill_workspace_bytes", "wf_verify_attn_tree",
+    "wf_lmhead_accept_tree", "wf_kv_compact_path",
 )
 
 
@@ -59,6 +60,15 @@ def _load():
     lib.wf_lmhead_accept_entropy.restype = i32
     lib.wf_lmhead_workspace_bytes.argtypes = [i32, i32]
     lib.wf_lmhead_workspace_bytes.restype = sz
+    lib.wf_verify_attn_tree.argtypes = [i32, p, p, p, p, p, i32, i32, i32,
+                                        i32, i32, i32, f32, i32, p, sz, p]
+    lib.wf_verify_attn_tree.restype = i32
+    lib.wf_lmhead_accept_tree.argtypes = [i32, p, p, p, p, p, i32, i32, i32,
+                                          f32, p, p, p, p, p, sz, p]
+    lib.wf_lmhead_accept_tree.restype = i32
+    lib.wf_kv_compact_path.argtypes = [i32, p, p, p, p, i32, i32, i32, i32,
+                                       i32, p]
+    lib.wf_kv_compact_path.restype = i32
     return lib
 
 
@@ -199,3 +209,75 @@ def wf_lmhead_accept_entropy(h, w_lm, logits, draft, tau, argmax_out,
         _dev(accept_out, "accept_out"), _dev(workspace, "workspace"),
         workspace.numel(), _stream(stream))
     _check(st, "wf_lmhead_accept_entropy")
+
+
+def wf_verify_attn_tree(q, k_cache, v_cache, out, ctx_len, tree_mask,
+                        softmax_scale=None, num_splits=0, workspace=None,
+                        stream=None):
+    """Tree verification attention: tree_mask [gamma] int64/uint64 device
+    tensor (bit j of row i: row i sees block row j); else as wf_verify_attn."""
+    gamma, hq, dh = q.shape
+    hkv, cap, dh2 = k_cache.shape
+    if dh2 != dh or tuple(v_cache.shape) != tuple(k_cache.shape):
+        raise ValueError("cache shapes do not match q")
+    if tuple(out.shape) != tuple(q.shape) or out.dtype != q.dtype:
+        raise ValueError("out must match q in shape and dtype")
+    if tree_mask.numel() != gamma or tree_mask.element_size() != 8:
+        raise ValueError("tree_mask must hold gamma 64-bit words")
+    code = _dtype_code(q)
+    if softmax_scale is None:
+        softmax_scale = dh ** -0.5
+    need = wf_verify_attn_workspace_bytes(code, gamma, ctx_len, hq, hkv, dh,
+                                          num_splits)
+    if workspace is None:
+        workspace = alloc_workspace(need, q.device)
+    st = lib.wf_verify_attn_tree(code, _dev(q, "q"), _dev(k_cache, "k_cache"),
+                                 _dev(v_cache, "v_cache"), _dev(out, "out"),
+                                 _dev(tree_mask, "tree_mask"), gamma,
+                                 int(ctx_len), cap, hq, hkv, dh,
+                                 float(softmax_scale), int(num_splits),
+                                 _dev(workspace, "workspace"),
+                                 workspace.numel(), _stream(stream))
+    _check(st, "wf_verify_attn_tree")
+    return out
+
+
+def wf_lmhead_accept_tree(h, w_lm, logits, tokens, parents, tau, argmax_out,
+                          entropy_out, accept_out, path_out, workspace=None,
+                          stream=None):
+    """Either (h [gamma][d], w_lm [vocab][d]) or logits [gamma][vocab] fp32;
+    tokens, parents [gamma] int32; outputs int32 [gamma], fp32 [gamma],
+    int32 [4], int32 [gamma]."""
+    if logits is not None:
+        gamma, vocab = logits.shape
+        d, code = 0, WF_F32
+    else:
+        gamma, d = h.shape
+        vocab = w_lm.shape[0]
+        code = _dtype_code(h)
+    need = wf_lmhead_workspace_bytes(gamma, vocab)
+    dev = (logits if logits is not None else h).device
+    if workspace is None:
+        workspace = alloc_workspace(need, dev)
+    st = lib.wf_lmhead_accept_tree(
+        code, _dev(h, "h"), _dev(w_lm, "w_lm"), _dev(logits, "logits"),
+        _dev(tokens, "tokens"), _dev(parents, "parents"), gamma, d, vocab,
+        float(tau), _dev(argmax_out, "argmax_out"),
+        _dev(entropy_out, "entropy_out"), _dev(accept_out, "accept_out"),
+        _dev(path_out, "path_out"), _dev(workspace, "workspace"),
+        workspace.numel(), _stream(stream))
+    _check(st, "wf_lmhead_accept_tree")
+
+
+def wf_kv_compact_path(k_cache, v_cache, accept, path, ctx_len, stream=None):
+    """Caches [Hkv][cap][D]; accept (n at [0]) and path [gamma] int32 device
+    tensors, as written by wf_lmhead_accept_tree."""
+    hkv, cap, dh = k_cache.shape
+    if tuple(v_cache.shape) != tuple(k_cache.shape) or v_cache.dtype != k_cache.dtype:
+        raise ValueError("k_cache and v_cache must match")
+    gamma = path.numel()
+    st = lib.wf_kv_compact_path(_dtype_code(k_cache), _dev(k_cache, "k_cache"),
+                                _dev(v_cache, "v_cache"), _dev(accept, "accept"),
+                                _dev(path, "path"), gamma, int(ctx_len), cap,
+                                hkv, dh, _stream(stream))
+    _check(st, "wf_kv_compact_path")

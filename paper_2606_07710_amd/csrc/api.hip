@@ -42,7 +42,7 @@ wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
 
 extern "C" {
 
-int32_t wf_abi_version(void) { return 3; }
+int32_t wf_abi_version(void) { return 4; }
 
 const char *wf_status_string(wf_status_t s) {
     switch (s) {
@@ -67,13 +67,15 @@ size_t wf_verify_attn_workspace_bytes(wf_dtype_t dt, int32_t gamma,
     return wf::attn_workspace_bytes(p, gamma, n_q_heads, head_dim);
 }
 
-wf_status_t wf_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
-                           const void *v_cache, void *out, int32_t gamma,
-                           int32_t ctx_len, int32_t cap, int32_t n_q_heads,
-                           int32_t n_kv_heads, int32_t head_dim,
-                           float softmax_scale, int32_t num_splits,
-                           void *workspace, size_t workspace_bytes,
-                           void *stream) {
+namespace {
+wf_status_t verify_attn_common(wf_dtype_t dt, const void *q, const void *k_cache,
+                               const void *v_cache, void *out,
+                               const uint64_t *tree_mask, int32_t gamma,
+                               int32_t ctx_len, int32_t cap, int32_t n_q_heads,
+                               int32_t n_kv_heads, int32_t head_dim,
+                               float softmax_scale, int32_t num_splits,
+                               void *workspace, size_t workspace_bytes,
+                               void *stream) {
     wf_status_t st = check_attn(dt, gamma, ctx_len, n_q_heads, n_kv_heads,
                                 head_dim, num_splits);
     if (st != WF_OK)
@@ -93,8 +95,39 @@ wf_status_t wf_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
     if (!workspace || workspace_bytes < need || !aligned16(workspace))
         return WF_ERR_WORKSPACE;
     return wf::launch_attn(dt, q, k_cache, v_cache, out, gamma, ctx_len, cap,
-                           n_q_heads, n_kv_heads, head_dim, softmax_scale, p,
-                           workspace, static_cast<hipStream_t>(stream));
+                           n_q_heads, n_kv_heads, head_dim, softmax_scale,
+                           tree_mask, p, workspace,
+                           static_cast<hipStream_t>(stream));
+}
+}  // namespace
+
+wf_status_t wf_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
+                           const void *v_cache, void *out, int32_t gamma,
+                           int32_t ctx_len, int32_t cap, int32_t n_q_heads,
+                           int32_t n_kv_heads, int32_t head_dim,
+                           float softmax_scale, int32_t num_splits,
+                           void *workspace, size_t workspace_bytes,
+                           void *stream) {
+    return verify_attn_common(dt, q, k_cache, v_cache, out, nullptr, gamma,
+                              ctx_len, cap, n_q_heads, n_kv_heads, head_dim,
+                              softmax_scale, num_splits, workspace,
+                              workspace_bytes, stream);
+}
+
+wf_status_t wf_verify_attn_tree(wf_dtype_t dt, const void *q,
+                                const void *k_cache, const void *v_cache,
+                                void *out, const uint64_t *tree_mask,
+                                int32_t gamma, int32_t ctx_len, int32_t cap,
+                                int32_t n_q_heads, int32_t n_kv_heads,
+                                int32_t head_dim, float softmax_scale,
+                                int32_t num_splits, void *workspace,
+                                size_t workspace_bytes, void *stream) {
+    if (!tree_mask || !aligned16(tree_mask))
+        return WF_ERR_INVALID_ARG;
+    return verify_attn_common(dt, q, k_cache, v_cache, out, tree_mask, gamma,
+                              ctx_len, cap, n_q_heads, n_kv_heads, head_dim,
+                              softmax_scale, num_splits, workspace,
+                              workspace_bytes, stream);
 }
 
 namespace {
@@ -159,14 +192,15 @@ size_t wf_lmhead_workspace_bytes(int32_t gamma, int32_t vocab) {
     return wf::lmhead_workspace_bytes(gamma, vocab);
 }
 
-wf_status_t wf_lmhead_accept_entropy(wf_dtype_t dt, const void *h,
-                                     const void *w_lm, const float *logits,
-                                     const int32_t *draft, int32_t gamma,
-                                     int32_t d, int32_t vocab,
-                                     float tau_entropy, int32_t *argmax_out,
-                                     float *entropy_out, int32_t *accept_out,
-                                     void *workspace, size_t workspace_bytes,
-                                     void *stream) {
+namespace {
+// Shared checks of the two LM-head entry points (the head/logits inputs,
+// outputs and workspace); the caller checks its own draft arguments.
+wf_status_t check_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
+                         const float *logits, int32_t gamma, int32_t d,
+                         int32_t vocab, float tau_entropy,
+                         const int32_t *argmax_out, const float *entropy_out,
+                         const int32_t *accept_out, const void *workspace,
+                         size_t workspace_bytes) {
     if (gamma < 1 || gamma > kMaxGamma || vocab < 1 || vocab > (1 << 30))
         return WF_ERR_INVALID_ARG;
     if (std::isnan(tau_entropy))
@@ -182,16 +216,75 @@ wf_status_t wf_lmhead_accept_entropy(wf_dtype_t dt, const void *h,
         if (dt == WF_BF16 && d % 32 != 0)
             return WF_ERR_UNSUPPORTED;
     }
-    if (gamma > 1 && !draft)
-        return WF_ERR_INVALID_ARG;
     if (!argmax_out || !entropy_out || !accept_out)
         return WF_ERR_INVALID_ARG;
     const size_t need = wf::lmhead_workspace_bytes(gamma, vocab);
     if (!workspace || workspace_bytes < need || !aligned16(workspace))
         return WF_ERR_WORKSPACE;
-    return wf::launch_lmhead(dt, h, w_lm, logits, draft, gamma, d, vocab,
-                             tau_entropy, argmax_out, entropy_out, accept_out,
-                             workspace, static_cast<hipStream_t>(stream));
+    return WF_OK;
+}
+}  // namespace
+
+wf_status_t wf_lmhead_accept_entropy(wf_dtype_t dt, const void *h,
+                                     const void *w_lm, const float *logits,
+                                     const int32_t *draft, int32_t gamma,
+                                     int32_t d, int32_t vocab,
+                                     float tau_entropy, int32_t *argmax_out,
+                                     float *entropy_out, int32_t *accept_out,
+                                     void *workspace, size_t workspace_bytes,
+                                     void *stream) {
+    const wf_status_t st = check_lmhead(dt, h, w_lm, logits, gamma, d, vocab,
+                                        tau_entropy, argmax_out, entropy_out,
+                                        accept_out, workspace, workspace_bytes);
+    if (st != WF_OK)
+        return st;
+    if (gamma > 1 && !draft)
+        return WF_ERR_INVALID_ARG;
+    return wf::launch_lmhead(dt, h, w_lm, logits, draft, nullptr, gamma, d,
+                             vocab, tau_entropy, argmax_out, entropy_out,
+                             accept_out, nullptr, workspace,
+                             static_cast<hipStream_t>(stream));
+}
+
+wf_status_t wf_lmhead_accept_tree(wf_dtype_t dt, const void *h,
+                                  const void *w_lm, const float *logits,
+                                  const int32_t *tokens, const int32_t *parents,
+                                  int32_t gamma, int32_t d, int32_t vocab,
+                                  float tau_entropy, int32_t *argmax_out,
+                                  float *entropy_out, int32_t *accept_out,
+                                  int32_t *path_out, void *workspace,
+                                  size_t workspace_bytes, void *stream) {
+    const wf_status_t st = check_lmhead(dt, h, w_lm, logits, gamma, d, vocab,
+                                        tau_entropy, argmax_out, entropy_out,
+                                        accept_out, workspace, workspace_bytes);
+    if (st != WF_OK)
+        return st;
+    if (!tokens || !parents || !path_out)
+        return WF_ERR_INVALID_ARG;
+    return wf::launch_lmhead(dt, h, w_lm, logits, tokens, parents, gamma, d,
+                             vocab, tau_entropy, argmax_out, entropy_out,
+                             accept_out, path_out, workspace,
+                             static_cast<hipStream_t>(stream));
+}
+
+wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
+                               const int32_t *accept, const int32_t *path,
+                               int32_t gamma, int32_t ctx_len, int32_t cap,
+                               int32_t n_kv_heads, int32_t head_dim,
+                               void *stream) {
+    if (!dtype_ok(dt) || gamma < 1 || gamma > kMaxGamma || ctx_len < 0 ||
+        (long long)ctx_len + gamma > cap || n_kv_heads < 1 ||
+        n_kv_heads > kMaxQHeads)
+        return WF_ERR_INVALID_ARG;
+    if (!k_cache || !v_cache || !accept || !path)
+        return WF_ERR_INVALID_ARG;
+    if (!aligned16(k_cache) || !aligned16(v_cache))
+        return WF_ERR_INVALID_ARG;
+    if (!head_dim_ok(head_dim))
+        return WF_ERR_UNSUPPORTED;
+    return wf::launch_compact(dt, k_cache, v_cache, accept, path, gamma,
+                              ctx_len, cap, n_kv_heads, head_dim,
+                              static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

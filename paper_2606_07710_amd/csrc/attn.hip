@@ -40,6 +40,9 @@ struct AttnParams {
     void *ws_o;               // [splits][gamma*n_q_heads][head_dim], unnormalised
                               // partial outputs: bf16 (bf16 path) or fp32
     float *ws_ml;             // [splits][gamma*n_q_heads][2]: running max, sum
+    // Tree verification: bit j of tree_mask[i] lets block row i see block
+    // row j (row i always sees itself); nullptr = block-causal.
+    const uint64_t *tree_mask;
     int gamma, ctx_len, cap, n_q_heads, n_kv_heads, group, rows, n_keys;
     int splits, keys_per_split, n_row_groups;
     float sl2;                // softmax_scale * log2(e)
@@ -231,8 +234,11 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
 
     // ---- Q^T operands and causal limits of this wave's rows ------------------
     const int row0 = rgw * ROWS_WG + rgi * ROWS_W;
+    const bool tree = a.tree_mask != nullptr;   // kernel argument: uniform
+    const uint64_t gbits = a.gamma >= 64 ? ~0ull : (1ull << a.gamma) - 1ull;
     bf16x8 qf[NBW][KC];
     int lim[NBW];
+    uint64_t tm[NBW];                 // tree mode: block rows the row sees
     auto load_q = [&]() {
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb) {
@@ -247,6 +253,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             // padding rows (r >= rows) reuse a real row's query and are never
             // stored; they must not be masked harder than it
             lim[nb] = a.ctx_len + i;
+            tm[nb] = tree ? ((a.tree_mask[i] | (1ull << i)) & gbits) : 0ull;
         }
     };
 
@@ -307,9 +314,23 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                 for (int nb = 0; nb < NBW; ++nb)
                     s[mb][nb] = mfma16x16x32(kop[mb][kk], qf[nb][kk], s[mb][nb]);
         }
-        // causal mask: only tiles reaching past ctx_len
+        // mask: only tiles reaching into the block (block-causal: past its
+        // first row, which every row sees; tree: from its first row on)
         const int kb = k_begin + t * kTileKeys;
-        if (kb + kTileKeys - 1 > a.ctx_len) {
+        if (tree) {
+            if (kb + kTileKeys - 1 >= a.ctx_len) {
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+                    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int j = kb + 16 * mb + 4 * c4 + i - a.ctx_len;
+                            const bool vis = j < 0 || (j < a.gamma && ((tm[nb] >> j) & 1ull));
+                            s[mb][nb][i] = vis ? s[mb][nb][i] : -INFINITY;
+                        }
+            }
+        } else if (kb + kTileKeys - 1 > a.ctx_len) {
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
@@ -602,7 +623,11 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
     __syncthreads();
 
     const int k_begin = split * a.keys_per_split;
-    const int k_end = min(min(a.n_keys, k_begin + a.keys_per_split), a.ctx_len + i + 1);
+    const bool tree = a.tree_mask != nullptr;
+    const uint64_t gbits = a.gamma >= 64 ? ~0ull : (1ull << a.gamma) - 1ull;
+    const uint64_t tm = tree ? ((a.tree_mask[i] | (1ull << i)) & gbits) : 0ull;
+    const int k_end = min(min(a.n_keys, k_begin + a.keys_per_split),
+                          tree ? a.n_keys : a.ctx_len + i + 1);
     const float *kbase = a.k32 + (size_t)g * a.cap * DH;
     const float *vbase = a.v32 + (size_t)g * a.cap * DH;
 
@@ -613,8 +638,10 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
 
     for (int kb = k_begin; kb < k_end; kb += kWave) {
         const int j = kb + lane;
+        const int jb = j - a.ctx_len;
+        const bool vis = j < k_end && (!tree || jb < 0 || ((tm >> jb) & 1ull));
         float sc = -INFINITY;
-        if (j < k_end) {
+        if (vis) {
             const float *kr = kbase + (size_t)j * DH;
             float dot = 0.f;
             for (int d = 0; d < DH; ++d)
@@ -623,7 +650,7 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
         }
         const float mnew = fmaxf(m, wave_max(sc));
         const float alpha = (m == -INFINITY) ? 0.f : exp2f((m - mnew) * a.sl2);
-        const float p = (j < k_end) ? exp2f((sc - mnew) * a.sl2) : 0.f;
+        const float p = vis ? exp2f((sc - mnew) * a.sl2) : 0.f;
         l = fmaf(l, alpha, wave_sum(p));
 #pragma unroll
         for (int e = 0; e < E; ++e)
@@ -631,6 +658,8 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
         const int cnt = min(kWave, k_end - kb);
         for (int tt = 0; tt < cnt; ++tt) {
             const float pt = __shfl(p, tt, kWave);
+            if (pt == 0.f)              // masked key (uniform: broadcast value)
+                continue;
             const float *vr = vbase + (size_t)(kb + tt) * DH;
 #pragma unroll
             for (int e = 0; e < E; ++e)
@@ -810,9 +839,10 @@ size_t attn_workspace_bytes(const AttnPlan &p, int gamma, int n_q_heads, int hea
 wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
                         const void *v_cache, void *out, int gamma, int ctx_len,
                         int cap, int n_q_heads, int n_kv_heads, int head_dim,
-                        float softmax_scale, const AttnPlan &p, void *workspace,
-                        hipStream_t stream) {
+                        float softmax_scale, const uint64_t *tree_mask,
+                        const AttnPlan &p, void *workspace, hipStream_t stream) {
     AttnParams a{};
+    a.tree_mask = tree_mask;
     const size_t pairs = (size_t)gamma * n_q_heads;
     a.ws_ml = reinterpret_cast<float *>(static_cast<char *>(workspace) + kCounterBytes);
     a.ws_o = a.ws_ml + (size_t)p.splits * pairs * 2;

@@ -59,13 +59,61 @@ constexpr int kFinishBatch = 16;
 struct LmFinish {
     RowState *states;        // [gamma][n_tiles]
     unsigned *fcnt;          // ticket counter, zero between calls
-    const int32_t *draft;
+    const int32_t *draft;    // chain: [gamma-1] drafts; tree: [gamma] node tokens
+    const int32_t *parents;  // tree: [gamma] parent of each node; chain: nullptr
+    int32_t *path_out;       // tree: [gamma] accepted root path
     int32_t *argmax_out;
     float *entropy_out;
     int32_t *accept_out;
     int gamma, n_tiles;
     float tau;
 };
+
+// Greedy acceptance on a draft tree, run by the last row workgroup once
+// every row's argmax is out.  Node j (one lane each, gamma <= 64) walks its
+// root path: it is accepted iff every node v on it has a parent p < v whose
+// argmax equals v's token.  The accepted node of greatest depth (lowest
+// index among equals) ends the accepted path; it gives the accept length,
+// bonus token and route, and lane 0 writes its root path.
+__device__ __forceinline__ void tree_accept(const LmFinish &f, int wave, int lane) {
+    __shared__ int s_par[kMaxGamma], s_tok[kMaxGamma], s_am[kMaxGamma];
+    if (wave == 0 && lane < f.gamma) {
+        s_par[lane] = f.parents[lane];
+        s_tok[lane] = f.draft[lane];
+        s_am[lane] = f.argmax_out[lane];
+    }
+    __syncthreads();
+    if (wave != 0)
+        return;
+    bool ok = lane < f.gamma;
+    int depth = 0;
+    // indices fall strictly along the walk, so it ends within `lane` steps
+    for (int v = lane; ok && v > 0; ++depth) {
+        const int p = s_par[v];
+        if (p < 0 || p >= v || s_tok[v] != s_am[p])
+            ok = false;
+        v = p;
+    }
+    int key = ok ? (depth << 6) | (63 - lane) : -1;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        key = max(key, __shfl_xor(key, off, kWave));
+    const int b = 63 - (key & 63);      // the root is always accepted: key >= 0
+    const int n = key >> 6;
+    if (lane > n && lane < f.gamma)
+        f.path_out[lane] = -1;
+    if (lane == 0) {
+        for (int t = n, v = b; t >= 0; --t) {
+            f.path_out[t] = v;
+            v = s_par[v];
+        }
+        f.accept_out[0] = n;
+        f.accept_out[1] = s_am[b];
+        f.accept_out[2] = (f.entropy_out[b] > f.tau) ? 1 : 0;
+        f.accept_out[3] = b;
+        *f.fcnt = 0u;
+    }
+}
 
 __global__ __launch_bounds__(kFinishThreads) void lm_finish_rows(LmFinish f) {
     __shared__ RowState ws[kFinishThreads / kWave];
@@ -100,6 +148,10 @@ __global__ __launch_bounds__(kFinishThreads) void lm_finish_rows(LmFinish f) {
     }
     if (!arrive_last(f.fcnt, (unsigned)f.gamma))
         return;
+    if (f.parents) {
+        tree_accept(f, wave, lane);
+        return;
+    }
     if (threadIdx.x == 0) {
         int n = 0;
         while (n < f.gamma - 1 && f.draft[n] == f.argmax_out[n])
@@ -412,15 +464,18 @@ size_t lmhead_workspace_bytes(int gamma, int vocab) {
 
 
 wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
-                          const float *logits, const int32_t *draft, int gamma,
-                          int d, int vocab, float tau, int32_t *argmax_out,
-                          float *entropy_out, int32_t *accept_out,
+                          const float *logits, const int32_t *draft,
+                          const int32_t *parents, int gamma, int d, int vocab,
+                          float tau, int32_t *argmax_out, float *entropy_out,
+                          int32_t *accept_out, int32_t *path_out,
                           void *workspace, hipStream_t stream) {
     char *ws = static_cast<char *>(workspace);
     LmFinish f;
     f.states = reinterpret_cast<RowState *>(ws + kCounterBytes);
     f.fcnt = reinterpret_cast<unsigned *>(ws);
     f.draft = draft;
+    f.parents = parents;
+    f.path_out = path_out;
     f.argmax_out = argmax_out;
     f.entropy_out = entropy_out;
     f.accept_out = accept_out;

@@ -39,15 +39,25 @@ size_t attn_workspace_bytes(const AttnPlan &p, int gamma, int n_q_heads,
 wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
                         const void *v_cache, void *out, int gamma, int ctx_len,
                         int cap, int n_q_heads, int n_kv_heads, int head_dim,
-                        float softmax_scale, const AttnPlan &p, void *workspace,
-                        hipStream_t stream);
+                        float softmax_scale, const uint64_t *tree_mask,
+                        const AttnPlan &p, void *workspace, hipStream_t stream);
 
 size_t lmhead_workspace_bytes(int gamma, int vocab);
+// Chain mode: draft [gamma-1], parents == path_out == nullptr, accept_out
+// [3].  Tree mode: draft = node tokens [gamma], parents [gamma], accept_out
+// [4], path_out [gamma].
 wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
-                          const float *logits, const int32_t *draft, int gamma,
-                          int d, int vocab, float tau, int32_t *argmax_out,
-                          float *entropy_out, int32_t *accept_out,
+                          const float *logits, const int32_t *draft,
+                          const int32_t *parents, int gamma, int d, int vocab,
+                          float tau, int32_t *argmax_out, float *entropy_out,
+                          int32_t *accept_out, int32_t *path_out,
                           void *workspace, hipStream_t stream);
+
+// Path compaction after tree acceptance: block rows path[t] -> t, t <= n.
+wf_status_t launch_compact(wf_dtype_t dt, void *k_cache, void *v_cache,
+                           const int32_t *accept, const int32_t *path,
+                           int gamma, int ctx_len, int cap, int n_kv_heads,
+                           int head_dim, hipStream_t stream);
 
 struct PrefillPlan {
     int nbt;             // 16-token blocks per workgroup

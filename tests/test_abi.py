@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert wf.abi_version() == 3
+    assert wf.abi_version() == 4
     assert wf.status_string(wf.WF_OK) == "ok"
     assert "workspace" in wf.status_string(wf.WF_ERR_WORKSPACE)
     assert wf.status_string(99) == "unknown status"
@@ -137,3 +137,61 @@ def _lm(**kw):
 ])
 def test_lmhead_rejects(kw, status):
     assert _lm(**kw) == status
+
+
+def _attn_tree(**kw):
+    a = dict(dt=1, q=FAKE, k=FAKE, v=FAKE, out=FAKE, mask=FAKE, gamma=61,
+             ctx=100, cap=161, hq=32, hkv=8, dh=128, scale=0.088, splits=0,
+             ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return wf.lib.wf_verify_attn_tree(
+        a["dt"], a["q"], a["k"], a["v"], a["out"], a["mask"], a["gamma"],
+        a["ctx"], a["cap"], a["hq"], a["hkv"], a["dh"], a["scale"],
+        a["splits"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(mask=None), 1), (dict(mask=ODD), 1), (dict(q=None), 1),
+    (dict(gamma=65), 1), (dict(cap=160), 1), (dict(dh=96), 2),
+    (dict(ws_bytes=100), 3),
+])
+def test_verify_attn_tree_rejects(kw, status):
+    assert _attn_tree(**kw) == status
+
+
+def _lm_tree(**kw):
+    a = dict(dt=1, h=FAKE, w=FAKE, logits=None, tok=FAKE, par=FAKE, gamma=61,
+             d=4096, vocab=151936, tau=1.0, am=FAKE, ent=FAKE, acc=FAKE,
+             path=FAKE, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return wf.lib.wf_lmhead_accept_tree(
+        a["dt"], a["h"], a["w"], a["logits"], a["tok"], a["par"], a["gamma"],
+        a["d"], a["vocab"], a["tau"], a["am"], a["ent"], a["acc"], a["path"],
+        a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(tok=None), 1), (dict(par=None), 1), (dict(path=None), 1),
+    (dict(gamma=65), 1), (dict(h=None), 1), (dict(d=100), 2),
+    (dict(ws_bytes=100), 3), (dict(tau=float("nan")), 1),
+])
+def test_lmhead_tree_rejects(kw, status):
+    assert _lm_tree(**kw) == status
+
+
+def _compact(**kw):
+    a = dict(dt=1, k=FAKE, v=FAKE, acc=FAKE, path=FAKE, gamma=61, ctx=100,
+             cap=161, hkv=8, dh=128)
+    a.update(kw)
+    return wf.lib.wf_kv_compact_path(a["dt"], a["k"], a["v"], a["acc"],
+                                     a["path"], a["gamma"], a["ctx"],
+                                     a["cap"], a["hkv"], a["dh"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=None), 1), (dict(acc=None), 1), (dict(path=None), 1),
+    (dict(gamma=0), 1), (dict(gamma=65), 1), (dict(cap=160), 1),
+    (dict(k=ODD), 1), (dict(dh=96), 2), (dict(dt=7), 1),
+])
+def test_compact_rejects(kw, status):
+    assert _compact(**kw) == status
