@@ -65,10 +65,13 @@ class Step:
     """Pre-marshalled C-ABI calls of one verification step."""
 
     def __init__(self, w, layers, head, outs, lmouts, draft, tau, ws_attn,
-                 ws_pre, ws_lm, wf):
+                 ws_pre, ws_lm, wf, tree=None):
         self.w, self.layers, self.head = w, layers, head
         self.outs, self.lmouts, self.draft, self.tau = outs, lmouts, draft, tau
         self.ws_attn, self.ws_pre, self.ws_lm, self.wf = ws_attn, ws_pre, ws_lm, wf
+        # draft-tree workloads: {"mask", "parents", "path", "k_all", "v_all"}
+        # (draft then holds the node tokens)
+        self.tree = tree
 
     def build(self, stream, catchup=None):
         """Marshal every call for `stream`; with `catchup` (a second stream),
@@ -86,9 +89,14 @@ class Step:
         self.join = torch.cuda.Event()
         self.attn = []
         self.pre = []
+        self.compact = []
+        tr = self.tree
+        self.attn_fn = wf.lib.wf_verify_attn_tree if tr else wf.lib.wf_verify_attn
         for l, t in enumerate(self.layers):
+            mask = (P(tr["mask"]),) if tr else ()
             self.attn.append((code, P(t["q"]), P(t["k_cache"]), P(t["v_cache"]),
-                              P(self.outs[l]), w.gamma, w.ctx_len, w.cap,
+                              P(self.outs[l])) + mask +
+                             (w.gamma, w.ctx_len, w.cap,
                               w.n_q_heads, w.n_kv_heads, w.head_dim,
                               w.softmax_scale, 0, P(self.ws_attn),
                               self.ws_attn.numel(), s))
@@ -101,6 +109,18 @@ class Step:
                                  w.head_dim, w.rope_base, P(self.ws_pre),
                                  self.ws_pre.numel(), s2))
         am, ent, acc = self.lmouts[0]
+        if tr:
+            self.lm_fn = wf.lib.wf_lmhead_accept_tree
+            self.lm = [(code, P(self.head["h"]), P(self.head["w_lm"]), None,
+                        P(self.draft), P(tr["parents"]), w.gamma, w.hidden,
+                        w.vocab, self.tau, P(am), P(ent), P(acc), P(tr["path"]),
+                        P(self.ws_lm), self.ws_lm.numel(), s)]
+            ka, va = tr["k_all"], tr["v_all"]
+            self.compact = [(code, P(ka), P(va), P(acc), P(tr["path"]), w.gamma,
+                             w.ctx_len, w.cap, w.n_kv_heads, w.head_dim,
+                             ka.shape[0], ka[0].numel(), s)]
+            return
+        self.lm_fn = wf.lib.wf_lmhead_accept_entropy
         self.lm = [(code, P(self.head["h"]), P(self.head["w_lm"]), None,
                     P(self.draft), w.gamma, w.hidden, w.vocab, self.tau, P(am),
                     P(ent), P(acc), P(self.ws_lm), self.ws_lm.numel(), s)]
@@ -117,9 +137,9 @@ class Step:
             self.fork.record(self.stream)
             self.catchup.wait_event(self.fork)
         for l, a in enumerate(self.attn):
-            rc = lib.wf_verify_attn(*a)
+            rc = self.attn_fn(*a)
             if check and rc:
-                raise RuntimeError(f"wf_verify_attn: {self.wf.status_string(rc)}")
+                raise RuntimeError(f"verify attention: {self.wf.status_string(rc)}")
             if self.catchup is not None and l < len(self.pre):
                 rc = lib.wf_kv_only_prefill(*self.pre[l])
                 if check and rc:
@@ -133,18 +153,26 @@ class Step:
             self.join.record(self.catchup)
             self.stream.wait_event(self.join)
         for a in self.lm:
-            rc = lib.wf_lmhead_accept_entropy(*a)
+            rc = self.lm_fn(*a)
             if check and rc:
-                raise RuntimeError(f"wf_lmhead_accept_entropy: {self.wf.status_string(rc)}")
+                raise RuntimeError(f"LM head: {self.wf.status_string(rc)}")
+        for a in self.compact:
+            rc = lib.wf_kv_compact_path(*a)
+            if check and rc:
+                raise RuntimeError(f"wf_kv_compact_path: {self.wf.status_string(rc)}")
 
     def phases(self):
         """(name, C function, argument tuples, stream) of the step's three
         phases."""
         lib = self.wf.lib
-        return [("attention", lib.wf_verify_attn, self.attn, self.stream),
-                ("prefill", lib.wf_kv_only_prefill, self.pre,
-                 self.catchup or self.stream),
-                ("lmhead", lib.wf_lmhead_accept_entropy, self.lm, self.stream)]
+        ph = [("attention", self.attn_fn, self.attn, self.stream),
+              ("prefill", lib.wf_kv_only_prefill, self.pre,
+               self.catchup or self.stream),
+              ("lmhead", self.lm_fn, self.lm, self.stream)]
+        if self.compact:
+            ph.append(("compaction", lib.wf_kv_compact_path, self.compact,
+                       self.stream))
+        return ph
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "verify_attn_8b_ctx32k_hbm_traffic.md")
@@ -172,7 +200,7 @@ def measured_traffic():
         return None
 
 
-def cpu_baseline(w, layers, head, budget_s, max_layers=None):
+def cpu_baseline(w, layers, head, budget_s, max_layers=None, tree_mask=None):
     """The oracle as it stands, on host cores, over a bounded sample of the
     step: the LM head, then as many layers of attention and prefill as fit
     in about `budget_s` seconds (all of them if they fit); scaled to one
@@ -200,7 +228,10 @@ def cpu_baseline(w, layers, head, budget_s, max_layers=None):
         k = W.to_oracle(t["k_cache"][:, :n].contiguous())
         v = W.to_oracle(t["v_cache"][:, :n].contiguous())
         t0 = time.perf_counter()
-        oracle.verify_attn(q, k, v, w.ctx_len)
+        if tree_mask is None:
+            oracle.verify_attn(q, k, v, w.ctx_len)
+        else:
+            oracle.verify_attn_mask(q, k, v, w.ctx_len, tree_mask)
         t_attn += time.perf_counter() - t0
         del q, k, v
         if w.n_prefill:
@@ -223,7 +254,8 @@ def cpu_baseline(w, layers, head, budget_s, max_layers=None):
         "kind": "oracle",
         "sample": ("the whole step: " if whole else
                    f"{done} of {w.n_layers} layers, scaled to one step: ")
-                  + f"attention over all {w.gamma * w.n_q_heads} rows x heads"
+                  + f"{'tree ' if tree_mask is not None else ''}attention over all "
+                    f"{w.gamma * w.n_q_heads} rows x heads"
                   + (", KV-only prefill" if w.n_prefill else "")
                   + ", full LM head",
         "measured_s": round(t_attn + t_pre + t_lm, 2),
@@ -256,6 +288,20 @@ def main():
     t0 = time.perf_counter()
     layers = [W.generate_layer(w, l, device=dev) for l in range(w.n_layers)]
     head = W.generate_head(w, device=dev)
+    tree = None
+    if w.is_tree:
+        # one [layers][heads][cap][D] cache per K and V, so the path
+        # compaction covers every layer in one call
+        tree = {"k_all": torch.stack([t.pop("k_cache") for t in layers]),
+                "v_all": torch.stack([t.pop("v_cache") for t in layers])}
+        for l, t in enumerate(layers):
+            t["k_cache"], t["v_cache"] = tree["k_all"][l], tree["v_all"][l]
+        par = W.draft_tree(seed=W.stream_seed(W.master_seed(w.cfg), "tree"))
+        tree["parents_np"] = par
+        tree["parents"] = torch.from_numpy(par).to(dev)
+        tree["mask"] = torch.from_numpy(
+            W.ancestor_masks(par).view(np.int64).copy()).to(dev)
+        tree["path"] = torch.empty(w.gamma, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
     log(f"inputs generated in {time.perf_counter() - t0:.1f}s")
 
@@ -271,7 +317,8 @@ def main():
     ws_lm = wf.alloc_workspace(wf.wf_lmhead_workspace_bytes(w.gamma, w.vocab), dev)
     lmouts = [(torch.empty(w.gamma, dtype=torch.int32, device=dev),
                torch.empty(w.gamma, dtype=torch.float32, device=dev),
-               torch.empty(3, dtype=torch.int32, device=dev)) for _ in range(2)]
+               torch.empty(4 if tree else 3, dtype=torch.int32, device=dev))
+              for _ in range(2)]
 
     # drafts: the workload's accept prefix, built from this GPU's own argmax
     # (the timed work does not depend on draft content)
@@ -282,12 +329,17 @@ def main():
                                 0.0, am, ent, acc, workspace=ws_lm)
     torch.cuda.synchronize()
     k = W.prefix_len(w, 0)
-    draft = torch.as_tensor(W.make_drafts(am.cpu().numpy(), k, w.vocab, 1),
-                            device=dev)
+    if tree:
+        # node tokens: the accepted root path has min(k, its depth) drafts
+        draft = torch.as_tensor(W.tree_tokens(am.cpu().numpy(), tree["parents_np"],
+                                              k, w.vocab, 1), device=dev)
+    else:
+        draft = torch.as_tensor(W.make_drafts(am.cpu().numpy(), k, w.vocab, 1),
+                                device=dev)
     tau = float(np.median(ent.cpu().numpy()))
 
     step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_pre,
-                ws_lm, wf)
+                ws_lm, wf, tree)
     stream = torch.cuda.current_stream()
     catchup = torch.cuda.Stream() if args.overlap else None
     step.build(stream, catchup)
@@ -380,7 +432,8 @@ def main():
     if not args.no_cpu_baseline:
         log(f"cpu baseline: about {args.cpu_budget_s:.0f}s of oracle work ...")
         cpu = cpu_baseline(w, layers, head, args.cpu_budget_s,
-                           args.cpu_sample_layers)
+                           args.cpu_sample_layers,
+                           W.ancestor_masks(tree["parents_np"]) if tree else None)
 
     line = {
         "metric": "verify-step us and achieved HBM GB/s (gamma=16, 32K ctx, "
@@ -405,12 +458,17 @@ def main():
                    "catch_up_tokens": w.n_prefill, "vocab": w.vocab,
                    "graph": bool(graph is not None),
                    "schedule": "one stream, model order" if catchup is None else
-                               "catch-up prefill on a second stream"},
+                               "catch-up prefill on a second stream"}
+                  | ({"draft_tree": {"nodes": w.gamma - 1,
+                                     "depth": len(w.tree_levels),
+                                     "nodes_per_depth": list(w.tree_levels)}}
+                     if tree else {}),
         "step_hbm_gbps": round(step_gbps, 1),
         "step_algorithmic_bytes": by["total"],
         "breakdown_us": breakdown,   # each phase run alone, back to back
         "roofline": {
-            "kernel": "wf_verify_attn, one layer (attn_partial_bf16 + attn_merge)",
+            "kernel": ("wf_verify_attn_tree" if tree else "wf_verify_attn")
+                      + ", one layer (attn_partial_bf16 + attn_merge)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": PEAK_HBM_GBPS,

@@ -263,22 +263,26 @@ wf_status_t wf_lmhead_accept_tree(wf_dtype_t dt, const void *h,
 /* ------------------------------------------------------------------------
  * wf_kv_compact_path -- after tree acceptance, move the accepted path's K/V
  * rows to consecutive cache rows after the prefix, so the cache again holds
- * the committed sequence in order (one layer's cache per call):
- *   K[g][ctx_len + t] <- K[g][ctx_len + path[t]]   (and V), t = 0..n
+ * the committed sequence in order, in every layer at once:
+ *   K_l[g][ctx_len + t] <- K_l[g][ctx_len + path[t]]   (and V), t = 0..n
  * with n = accept[0].  Both are read on the device (accept_out and path_out
  * of wf_lmhead_accept_tree), so the call can follow it on the same stream
  * without a host round trip.  A path entry outside [t, gamma) leaves row t
  * unchanged; rows other than ctx_len .. ctx_len+n are never written.
  *
- * k_cache, v_cache  [n_kv_heads][cap][head_dim], dtype dt.
+ * k_cache, v_cache  layer 0's [n_kv_heads][cap][head_dim] cache, dtype dt;
+ *          layer l's starts l * layer_stride elements further on.
  * accept  device int32, at least 1 entry; path  [gamma] device int32.
  * Limits: 1 <= gamma <= 64; ctx_len >= 0; ctx_len + gamma <= cap;
- *         head_dim in {64, 128}.
+ *         head_dim in {64, 128}; 1 <= n_layers <= 1024; for n_layers > 1,
+ *         layer_stride >= n_kv_heads * cap * head_dim and a multiple of 16
+ *         bytes (ignored when n_layers == 1).
  * ---------------------------------------------------------------------- */
 wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
                                const int32_t *accept, const int32_t *path,
                                int32_t gamma, int32_t ctx_len, int32_t cap,
                                int32_t n_kv_heads, int32_t head_dim,
+                               int32_t n_layers, size_t layer_stride,
                                void *stream);
 
 #ifdef __cplusplus

@@ -67,7 +67,7 @@ def _load():
                                           f32, p, p, p, p, p, sz, p]
     lib.wf_lmhead_accept_tree.restype = i32
     lib.wf_kv_compact_path.argtypes = [i32, p, p, p, p, i32, i32, i32, i32,
-                                       i32, p]
+                                       i32, i32, sz, p]
     lib.wf_kv_compact_path.restype = i32
     return lib
 
@@ -270,14 +270,19 @@ def wf_lmhead_accept_tree(h, w_lm, logits, tokens, parents, tau, argmax_out,
 
 
 def wf_kv_compact_path(k_cache, v_cache, accept, path, ctx_len, stream=None):
-    """Caches [Hkv][cap][D]; accept (n at [0]) and path [gamma] int32 device
-    tensors, as written by wf_lmhead_accept_tree."""
-    hkv, cap, dh = k_cache.shape
+    """Caches [Hkv][cap][D] (one layer) or [L][Hkv][cap][D] (all layers);
+    accept (n at [0]) and path [gamma] int32 device tensors, as written by
+    wf_lmhead_accept_tree."""
     if tuple(v_cache.shape) != tuple(k_cache.shape) or v_cache.dtype != k_cache.dtype:
         raise ValueError("k_cache and v_cache must match")
+    if k_cache.dim() == 4:
+        n_layers, hkv, cap, dh = k_cache.shape
+        stride = hkv * cap * dh
+    else:
+        (hkv, cap, dh), n_layers, stride = k_cache.shape, 1, 0
     gamma = path.numel()
     st = lib.wf_kv_compact_path(_dtype_code(k_cache), _dev(k_cache, "k_cache"),
                                 _dev(v_cache, "v_cache"), _dev(accept, "accept"),
                                 _dev(path, "path"), gamma, int(ctx_len), cap,
-                                hkv, dh, _stream(stream))
+                                hkv, dh, n_layers, stride, _stream(stream))
     _check(st, "wf_kv_compact_path")

@@ -11,6 +11,7 @@ constexpr int kMaxGamma = 64;
 constexpr int kMaxQHeads = 256;
 constexpr int kMaxSplits = 1024;
 constexpr int kMaxPrefillTokens = 4096;
+constexpr int kMaxLayers = 1024;
 
 inline bool aligned16(const void *p) {
     return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
@@ -271,10 +272,16 @@ wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
                                const int32_t *accept, const int32_t *path,
                                int32_t gamma, int32_t ctx_len, int32_t cap,
                                int32_t n_kv_heads, int32_t head_dim,
+                               int32_t n_layers, size_t layer_stride,
                                void *stream) {
     if (!dtype_ok(dt) || gamma < 1 || gamma > kMaxGamma || ctx_len < 0 ||
         (long long)ctx_len + gamma > cap || n_kv_heads < 1 ||
-        n_kv_heads > kMaxQHeads)
+        n_kv_heads > kMaxQHeads || n_layers < 1 || n_layers > kMaxLayers)
+        return WF_ERR_INVALID_ARG;
+    if (n_layers > 1 &&
+        layer_stride < (size_t)n_kv_heads * (size_t)cap * (size_t)head_dim)
+        return WF_ERR_INVALID_ARG;
+    if (n_layers > 1 && (layer_stride * (dt == WF_BF16 ? 2 : 4)) % 16 != 0)
         return WF_ERR_INVALID_ARG;
     if (!k_cache || !v_cache || !accept || !path)
         return WF_ERR_INVALID_ARG;
@@ -283,7 +290,8 @@ wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
     if (!head_dim_ok(head_dim))
         return WF_ERR_UNSUPPORTED;
     return wf::launch_compact(dt, k_cache, v_cache, accept, path, gamma,
-                              ctx_len, cap, n_kv_heads, head_dim,
+                              ctx_len, cap, n_kv_heads, head_dim, n_layers,
+                              n_layers > 1 ? layer_stride : 0,
                               static_cast<hipStream_t>(stream));
 }
 

@@ -53,11 +53,13 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
                           int32_t *accept_out, int32_t *path_out,
                           void *workspace, hipStream_t stream);
 
-// Path compaction after tree acceptance: block rows path[t] -> t, t <= n.
+// Path compaction after tree acceptance: block rows path[t] -> t, t <= n,
+// in n_layers caches layer_stride elements apart.
 wf_status_t launch_compact(wf_dtype_t dt, void *k_cache, void *v_cache,
                            const int32_t *accept, const int32_t *path,
                            int gamma, int ctx_len, int cap, int n_kv_heads,
-                           int head_dim, hipStream_t stream);
+                           int head_dim, int n_layers, size_t layer_stride,
+                           hipStream_t stream);
 
 struct PrefillPlan {
     int nbt;             // 16-token blocks per workgroup

@@ -181,17 +181,20 @@ def test_lmhead_tree_rejects(kw, status):
 
 def _compact(**kw):
     a = dict(dt=1, k=FAKE, v=FAKE, acc=FAKE, path=FAKE, gamma=61, ctx=100,
-             cap=161, hkv=8, dh=128)
+             cap=161, hkv=8, dh=128, layers=36, stride=8 * 161 * 128)
     a.update(kw)
     return wf.lib.wf_kv_compact_path(a["dt"], a["k"], a["v"], a["acc"],
                                      a["path"], a["gamma"], a["ctx"],
-                                     a["cap"], a["hkv"], a["dh"], None)
+                                     a["cap"], a["hkv"], a["dh"], a["layers"],
+                                     a["stride"], None)
 
 
 @pytest.mark.parametrize("kw,status", [
     (dict(k=None), 1), (dict(acc=None), 1), (dict(path=None), 1),
     (dict(gamma=0), 1), (dict(gamma=65), 1), (dict(cap=160), 1),
     (dict(k=ODD), 1), (dict(dh=96), 2), (dict(dt=7), 1),
+    (dict(layers=0), 1), (dict(stride=8 * 161 * 128 - 1), 1),
+    (dict(layers=1025), 1),
 ])
 def test_compact_rejects(kw, status):
     assert _compact(**kw) == status

@@ -214,26 +214,31 @@ def test_tree_accept_invalid_parents_never_accepted():
 
 # ---- compaction --------------------------------------------------------------
 
-@pytest.mark.parametrize("dt,dh", [("bf16", 128), ("bf16", 64), ("f32", 128)])
-def test_compaction_matches_oracle(dt, dh):
-    print(f"compaction {dt} D={dh}", flush=True)
+@pytest.mark.parametrize("dt,dh,layers", [("bf16", 128, 1), ("bf16", 64, 1),
+                                          ("f32", 128, 1), ("bf16", 128, 5)])
+def test_compaction_matches_oracle(dt, dh, layers):
+    print(f"compaction {dt} D={dh} layers={layers}", flush=True)
     gamma, ctx, hkv = 61, 500, 8
     cap = ctx + gamma + 7
-    k = W.normal((hkv, cap, dh), 1.0, W.stream_seed(3, "k_cache"), DT[dt], DEV)
-    v = W.normal((hkv, cap, dh), 1.0, W.stream_seed(3, "v_cache"), DT[dt], DEV)
+    shape = (hkv, cap, dh) if layers == 1 else (layers, hkv, cap, dh)
+    k = W.normal(shape, 1.0, W.stream_seed(3, "k_cache"), DT[dt], DEV)
+    v = W.normal(shape, 1.0, W.stream_seed(3, "v_cache"), DT[dt], DEV)
     par = W.draft_tree(seed=4)
     rng = np.random.default_rng(5)
     am = rng.integers(0, 1000, gamma).astype(np.int32)
     tok = W.tree_tokens(am, par, 6, 1000, seed=6)
     n, _, _, b, _, path = oracle.accept_tree(am, np.zeros(gamma), tok, par, 0.0)
     assert n == 6
-    kref, vref = oracle.kv_compact_path(W.to_oracle(k), W.to_oracle(v), ctx,
-                                        path, n)
+    k0, v0 = W.to_oracle(k), W.to_oracle(v)
     acc = torch.tensor([n, 0, 0, b], dtype=torch.int32, device=DEV)
     wf.wf_kv_compact_path(k, v, acc, torch.from_numpy(path).to(DEV), ctx)
     torch.cuda.synchronize()
-    assert np.array_equal(W.to_oracle(k), kref)
-    assert np.array_equal(W.to_oracle(v), vref)
+    k1, v1 = W.to_oracle(k), W.to_oracle(v)
+    for l in range(layers):
+        sl = (slice(None),) if layers == 1 else (l,)
+        kref, vref = oracle.kv_compact_path(k0[sl], v0[sl], ctx, path, n)
+        assert np.array_equal(k1[sl], kref)
+        assert np.array_equal(v1[sl], vref)
 
 
 # ---- the EAGLE-3-shaped workload at full size ----------------------------------
