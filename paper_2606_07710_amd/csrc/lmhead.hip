@@ -395,6 +395,170 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
     }
 }
 
+// Persistent bf16 LM head for up to 64 verify rows (NBL groups of 16) and
+// a hidden size that is a multiple of 512.  Workgroup b owns the 16-row
+// vocabulary blocks [b0, b1); wave w owns blocks b0 + w + 8j, j < MBW (a
+// block past the run re-reads the run's last block and is masked out of the
+// states).  The hidden dimension is walked in K-blocks of 512 dims: each
+// K-block of h, all rows, is staged in LDS (double-buffered; the 16-byte
+// granules of a row are XOR-swizzled by the row so the MFMA operand reads
+// are bank-conflict free) and shared by the 8 waves, so h leaves L2 once per
+// workgroup and K-block, while W streams from HBM straight into registers P
+// chunks ahead, across K-block boundaries (the last K-block is peeled).  The
+// logits of all of a wave's blocks stay in registers for the whole K loop,
+// and each row's state over the run is formed once at the end: lane values
+// in ascending vocabulary order, then the 4 lanes of a row, then the 8 waves
+// in order.
+constexpr int kWideK = 512;                 // hidden dims per staged K-block
+constexpr int kWideGran = kWideK / 8;       // 16-byte granules per row per K-block
+constexpr int kWideMaxBlocksPerWave = 5;
+
+template <int NBL, int MBW, int P>
+__global__ __launch_bounds__(512) void lm_wide_bf16(const uint16_t *__restrict__ h,
+                                                    const uint16_t *__restrict__ w,
+                                                    LmFinish f, int d, int vocab) {
+    constexpr int ROWS = 16 * NBL;
+    constexpr int CPB = kWideK / 32;                   // chunks per K-block
+    constexpr int HLOADS = ROWS * kWideGran / 512;     // h granules per thread per K-block
+    static_assert(CPB % P == 0, "prefetch depth must divide the K-block");
+    __shared__ __attribute__((aligned(16))) u32x4 hs[2][ROWS][kWideGran];
+    __shared__ RowState wst[kLmWaves][ROWS];
+
+    const int gamma = f.gamma;
+    const int wave = wave_id();
+    const int lane = threadIdx.x % kWave;
+    const int m16 = lane & 15;
+    const int c4 = lane >> 4;
+    const int nblk = (vocab + 15) / 16;
+    const int b0 = (int)((long long)blockIdx.x * nblk / gridDim.x);
+    const int b1 = (int)((long long)(blockIdx.x + 1) * nblk / gridDim.x);
+    const int nkb = d / kWideK;
+
+    const uint16_t *wrow[MBW];
+#pragma unroll
+    for (int j = 0; j < MBW; ++j) {
+        const int blk = max(min(b0 + wave + 8 * j, b1 - 1), 0);
+        wrow[j] = w + (size_t)min(blk * 16 + m16, vocab - 1) * d + c4 * 8;
+    }
+    // h staging: granule idx = threadIdx.x + 512 q of the K-block is row
+    // idx / kWideGran, granule idx % kWideGran (rows past gamma repeat the
+    // last row; their logits are never used)
+    // (staged in two halves, q in [half*HH, (half+1)*HH), to keep few
+    // registers in flight)
+    constexpr int HH = HLOADS / 2;
+    static_assert(HLOADS % 2 == 0, "h staging halves");
+    auto hload = [&](int kb, int half, u32x4 (&hr)[HH]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < HH; ++q) {
+            const int idx = threadIdx.x + 512 * (half * HH + q);
+            const int row = idx / kWideGran, g = idx % kWideGran;
+            hr[q] = *reinterpret_cast<const u32x4 *>(
+                h + (size_t)min(row, gamma - 1) * d + kb * kWideK + 8 * g);
+        }
+    };
+    auto hstore = [&](int buf, int half, const u32x4 (&hr)[HH]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < HH; ++q) {
+            const int idx = threadIdx.x + 512 * (half * HH + q);
+            const int row = idx / kWideGran, g = idx % kWideGran;
+            hs[buf][row][g ^ (row & 15)] = hr[q];
+        }
+    };
+
+    f32x4 acc[MBW][NBL];
+#pragma unroll
+    for (int j = 0; j < MBW; ++j)
+#pragma unroll
+        for (int nb = 0; nb < NBL; ++nb)
+            acc[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    bf16x8 wb[P][MBW];
+    {
+        u32x4 hr[HH];
+        hload(0, 0, hr);
+        hstore(0, 0, hr);
+        hload(0, 1, hr);
+        hstore(0, 1, hr);
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+#pragma unroll
+            for (int j = 0; j < MBW; ++j)
+                wb[p][j] = load_bf16x8(wrow[j] + p * 32);
+        __syncthreads();
+    }
+
+    // One K-block; all but the last also stage the next K-block of h and
+    // refill W from the next K-block's first chunks.
+    auto kblock = [&](int kb, auto last_tag) __attribute__((always_inline)) {
+        constexpr bool LAST = decltype(last_tag)::value;
+        const int buf = kb & 1;
+        u32x4 hr[HH];
+        if (!LAST)
+            hload(kb + 1, 0, hr);
+        const int cbase = kb * CPB;
+#pragma unroll
+        for (int u = 0; u < CPB; ++u) {
+            const int p = u % P;
+            if (!LAST && u == CPB / 2) {
+                hstore(buf ^ 1, 0, hr);
+                hload(kb + 1, 1, hr);
+            }
+            bf16x8 hop[NBL];
+#pragma unroll
+            for (int nb = 0; nb < NBL; ++nb)
+                hop[nb] = __builtin_bit_cast(bf16x8, hs[buf][nb * 16 + m16][(4 * u + c4) ^ m16]);
+#pragma unroll
+            for (int j = 0; j < MBW; ++j)
+#pragma unroll
+                for (int nb = 0; nb < NBL; ++nb)
+                    acc[j][nb] = mfma16x16x32(wb[p][j], hop[nb], acc[j][nb]);
+            if (!LAST || u + P < CPB) {
+#pragma unroll
+                for (int j = 0; j < MBW; ++j)
+                    wb[p][j] = load_bf16x8(wrow[j] + (cbase + u + P) * 32);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (!LAST) {
+            hstore(buf ^ 1, 1, hr);
+            asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        }
+    };
+    for (int kb = 0; kb + 1 < nkb; ++kb)
+        kblock(kb, std::false_type{});
+    kblock(nkb - 1, std::true_type{});
+
+    // row states: lane values in ascending vocabulary order, then the four
+    // lanes of a row (fixed butterfly), then the waves in order
+#pragma unroll
+    for (int nb = 0; nb < NBL; ++nb) {
+        RowState st = state_empty();
+#pragma unroll
+        for (int j = 0; j < MBW; ++j) {
+            const int blk = b0 + wave + 8 * j;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int v = blk * 16 + 4 * c4 + i;
+                if (blk < b1 && v < vocab)
+                    st = state_merge(st, state_single(acc[j][nb][i], v));
+            }
+        }
+        st = state_merge(st, shfl_xor_state(st, 16));
+        st = state_merge(st, shfl_xor_state(st, 32));
+        if (c4 == 0)
+            wst[wave][nb * 16 + m16] = st;
+    }
+    __syncthreads();
+    const int r = threadIdx.x;
+    if (r < gamma) {
+        RowState m = wst[0][r];
+#pragma unroll
+        for (int ww = 1; ww < kLmWaves; ++ww)
+            m = state_merge(m, wst[ww][r]);
+        f.states[(size_t)r * f.n_tiles + blockIdx.x] = m;
+    }
+}
+
 __global__ __launch_bounds__(256) void lm_tiles_f32(const float *__restrict__ h,
                                                     const float *__restrict__ w,
                                                     LmFinish f, int d, int vocab) {
@@ -493,6 +657,24 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
             lm_stream_bf16<16><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, vocab);
         else
             lm_stream_bf16<20><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, vocab);
+    } else if (dt == WF_BF16 && d % kWideK == 0) {
+        // persistent: about one workgroup per CU, each wave at most
+        // kWideMaxBlocksPerWave 16-row vocabulary blocks
+        const int nblk = cdiv(vocab, 16);
+        const int per_wg = kLmWaves * kWideMaxBlocksPerWave;
+        f.n_tiles = std::max(std::min(kLmStreamGrid, cdiv(nblk, kLmWaves)), cdiv(nblk, per_wg));
+        const int mbw = cdiv(cdiv(nblk, f.n_tiles), kLmWaves);
+        const uint16_t *hb = static_cast<const uint16_t *>(h);
+        const uint16_t *wb = static_cast<const uint16_t *>(w_lm);
+        const int nbl = cdiv(gamma, 16);
+#define WF_WIDE(NBLV, MBWV, PV)                                                              \
+    if (nbl == NBLV && mbw <= MBWV) {                                                      \
+        lm_wide_bf16<NBLV, MBWV, PV><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, d, vocab);  \
+    } else
+        WF_WIDE(1, 2, 4) WF_WIDE(1, 5, 4) WF_WIDE(2, 2, 4) WF_WIDE(2, 5, 4)
+        WF_WIDE(3, 2, 4) WF_WIDE(3, 5, 2) WF_WIDE(4, 2, 4) WF_WIDE(4, 5, 2)
+        { return WF_ERR_UNSUPPORTED; }
+#undef WF_WIDE
     } else if (dt == WF_BF16) {
         f.n_tiles = cdiv(vocab, kLmTile);
         const uint16_t *hb = static_cast<const uint16_t *>(h);

@@ -40,6 +40,13 @@ CASES = [
     ("bf16", 17, 1024, 3000, 1.0, 0.05),
     ("bf16", 64, 256, 2000, 1.0, 0.1),
     ("bf16", 8, 4096, 151936, 1.0, 0.02),
+    # the wide-row kernel (hidden size a multiple of 512): every row-group
+    # count, runs of one to five blocks per wave, ragged vocabularies
+    ("bf16", 24, 1024, 2000, 1.0, 0.05),
+    ("bf16", 40, 512, 70001, 1.0, 0.05),
+    ("bf16", 61, 4096, 151936, 1.0, 0.02),
+    ("bf16", 64, 512, 300000, 1.0, 0.05),
+    ("bf16", 33, 512, 15, 1.0, 0.05),
     ("f32", 8, 512, 4096, 0.02, 0.02),
     ("f32", 3, 100, 1001, 1.0, 0.1),
     ("f32", 1, 64, 77, 1.0, 0.3),
