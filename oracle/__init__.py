@@ -24,6 +24,9 @@ Paper: arXiv 2606.07710 (WhiFlash).  What each call computes:
                       and its root path, plus the same entropy route.
   kv_compact_path  -- after tree acceptance, the accepted path's K/V rows
                       move to consecutive cache rows after the prefix.
+  router_mlp       -- the neural routing policy (Sec. 3.3.2 and its
+                      appendix): delta = w2 . GELU(W1 h + b1) + b2 per row;
+                      route = delta > tau_neural.
   layer_forward    -- a full single attention layer, used to pin that KV-only
                       prefill yields the cache a full forward would.
 """
@@ -65,6 +68,7 @@ def _load():
     lib.wfref_verify_attn_mask.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i,
                                            _i, _i, _i, _d]
     lib.wfref_accept_tree.argtypes = [_p, _p, _p, _p, _i, _d, _p, _p, _p]
+    lib.wfref_router_mlp.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i, _p]
     lib.wfref_rope_inplace.argtypes = [_p, _i, _d, _d]
     lib.wfref_rope_inplace.restype = None
     lib.wfref_layer_forward.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i, _i,
@@ -72,6 +76,7 @@ def _load():
     for name in ("wfref_verify_attn", "wfref_verify_attn_rows",
                  "wfref_kv_only_prefill", "wfref_lmhead_rows", "wfref_accept",
                  "wfref_verify_attn_mask", "wfref_accept_tree",
+                 "wfref_router_mlp",
                  "wfref_layer_forward"):
         getattr(lib, name).restype = _i
     _lib = lib
@@ -265,6 +270,34 @@ def kv_compact_path(k_cache, v_cache, ctx_len, path, n):
     k[:, dst] = np.asarray(k_cache)[:, src]
     v[:, dst] = np.asarray(v_cache)[:, src]
     return k, v
+
+
+def router_mlp(h, w1, b1, w2, b2):
+    """h [gamma][d]; w1 [m][d]; b1, w2 [m]; b2 [1] (one storage type)
+    -> delta [gamma] fp64."""
+    lib = _load()
+    h, code = _arr(h)
+    arrs = []
+    for a in (w1, b1, w2, b2):
+        a, c = _arr(a)
+        if c != code:
+            raise TypeError("router inputs must share a storage type")
+        arrs.append(a)
+    w1, b1, w2, b2 = arrs
+    gamma, d = h.shape
+    m = w1.shape[0]
+    if w1.shape != (m, d) or b1.shape != (m,) or w2.shape != (m,) or b2.shape != (1,):
+        raise ValueError("router shapes")
+    out = np.empty(gamma, np.float64)
+    rc = lib.wfref_router_mlp(code, _ptr(h), _ptr(w1), _ptr(b1), _ptr(w2),
+                              _ptr(b2), gamma, d, m, _ptr(out))
+    _check(rc, "router_mlp")
+    return out
+
+
+def route_neural(delta, row, tau):
+    """Sec. 3.3.2 decision: 1 (autoregressive) iff delta[row] > tau."""
+    return int(float(delta[row]) > float(tau))
 
 
 def rope(v, pos, base):

@@ -505,6 +505,40 @@ int wfref_accept_tree(const int32_t *argmax, const double *entropy,
 }
 
 /* ------------------------------------------------------------------------ *
+ * Neural routing policy (Sec. 3.3.2; architecture in the appendix on the
+ * neural router): a two-layer MLP regressor on the target's final hidden
+ * state predicts the acceptance-length gain of the autoregressive drafter
+ * over the diffusion drafter,
+ *   delta = w2 . GELU(W1 h + b1) + b2,   GELU(x) = x * Phi(x)
+ *         = 0.5 x (1 + erf(x / sqrt 2))   (exact form; dropout is off at
+ *                                          inference),
+ * with W1 [m][d], m = d/8, and the route is the autoregressive drafter iff
+ * delta > tau_neural.  Evaluated here for every row of h [gamma][d];
+ * storage code dtype for h, W1, b1, w2 and b2 alike.  delta_out [gamma].
+ * ------------------------------------------------------------------------ */
+int wfref_router_mlp(int dtype, const void *h, const void *w1, const void *b1,
+                     const void *w2, const void *b2, int gamma, int d, int m,
+                     double *delta_out)
+{
+    if (!valid_dtype(dtype) || gamma < 1 || d < 1 || m < 1)
+        return 1;
+#pragma omp parallel for schedule(static)
+    for (int r = 0; r < gamma; ++r) {
+        double acc = elem(b2, dtype, 0);
+        for (int i = 0; i < m; ++i) {
+            double z = elem(b1, dtype, i);
+            for (int k = 0; k < d; ++k)
+                z += elem(w1, dtype, (size_t)i * d + k) *
+                     elem(h, dtype, (size_t)r * d + k);
+            const double g = 0.5 * z * (1.0 + erf(z / sqrt(2.0)));
+            acc += elem(w2, dtype, i) * g;
+        }
+        delta_out[r] = acc;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ *
  * One full decoder attention layer over a fresh sequence of T tokens
  * (positions pos0 .. pos0+T-1), used only to pin the KV-only prefill: the
  * keys and values it records must equal what KV-only prefill produces for

@@ -171,7 +171,8 @@ TENSOR_IDS = {"q": 1, "k_cache": 2, "v_cache": 3, "x": 4, "w_k": 5, "w_v": 6,
               "h": 7, "w_lm": 8, "router_logits": 9, "router_rows": 10,
               "router_boost": 11, "drafts": 12, "prefix": 13,
               "drafter_k_cache": 14, "drafter_v_cache": 15, "tree": 16,
-              "tree_tokens": 17}
+              "tree_tokens": 17, "router_w1": 18, "router_b1": 19,
+              "router_w2": 20, "router_b2": 21}
 
 
 def stream_seed(master: int, tensor: str | int, layer: int = 0) -> int:
@@ -383,6 +384,28 @@ def generate_layer(w: Workload, layer: int, device="cpu", seed=None):
                 (w.n_kv_heads, w.prefill_cap, w.head_dim), w.qkv_std,
                 stream_seed(m, "drafter_v_cache", layer), dt, device)
     return out
+
+
+def router_hidden(hidden: int) -> int:
+    """Width of the neural router's hidden layer: d/8 (appendix on the
+    neural router)."""
+    return hidden // 8
+
+
+def generate_router(w: Workload, device="cpu", seed=None):
+    """Neural-router weights with random values (the trained router is not
+    available): W1 [d/8][d] and b1 [d/8] ~ N(0, w_std), w2 [d/8] and b2 [1]
+    ~ N(0, 0.05), which spreads the predicted gain over about +-1 token for
+    post-norm activations, the range of the paper's thresholds."""
+    m_seed = master_seed(w.cfg) if seed is None else seed
+    dt = w.torch_dtype
+    m = router_hidden(w.hidden)
+    return {
+        "w1": normal((m, w.hidden), w.w_std, stream_seed(m_seed, "router_w1"), dt, device),
+        "b1": normal((m,), w.w_std, stream_seed(m_seed, "router_b1"), dt, device),
+        "w2": normal((m,), 0.05, stream_seed(m_seed, "router_w2"), dt, device),
+        "b2": normal((1,), 0.05, stream_seed(m_seed, "router_b2"), dt, device),
+    }
 
 
 def generate_head(w: Workload, device="cpu", seed=None):
