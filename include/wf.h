@@ -27,6 +27,11 @@
  *                             tree node, its root path and the route
  *   wf_kv_compact_path        moves the accepted path's K/V rows together
  *
+ * and the learned routing policy, the alternative to the entropy rule:
+ *
+ *   wf_router_neural          two-layer MLP on the final hidden state ->
+ *                             predicted acceptance-length gain and route
+ *
  * Conventions shared by every call
  *   - Every tensor pointer is DEVICE memory owned by the caller, 16-byte
  *     aligned, densely packed in the layout stated.  The library never
@@ -284,6 +289,40 @@ wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
                                int32_t n_kv_heads, int32_t head_dim,
                                int32_t n_layers, size_t layer_stride,
                                void *stream);
+
+/* ------------------------------------------------------------------------
+ * wf_router_neural -- the neural routing policy (Sec. 3.3.2; architecture
+ * in the appendix on the neural router).  A two-layer MLP regressor on the
+ * target's final hidden state predicts the acceptance-length gain of the
+ * autoregressive drafter over the diffusion drafter, and the next round uses
+ * the autoregressive drafter iff the gain exceeds tau_neural:
+ *   delta_out[r] = w2 . GELU(W1 h[r] + b1) + b2   for every row r,
+ *   GELU(x) = 0.5 x (1 + erf(x / sqrt 2))  (exact form; no dropout),
+ *   route_out[0] = delta_out[row[0]] > tau_neural   (1 = AR, 0 = diffusion).
+ *
+ * h        [gamma][d] final-norm hidden states of the verify rows (the
+ *          LM head's input).
+ * w1 [m][d], b1 [m], w2 [m], b2 [1]: the router's weights, dtype dt like h
+ *          (the paper's router has m = d/8).
+ * row      device int32: the row to route on, usually the final accepted
+ *          position written by the acceptance call (accept_out + 0 for
+ *          chains and blocks, accept_out + 3 for trees); clamped to
+ *          [0, gamma).
+ * delta_out [gamma] fp32; route_out [1] int32.
+ * Limits:  1 <= gamma <= 64; d >= 1 and m >= 1 (m <= 65536); for WF_BF16
+ *          d % 32 == 0 and m % 16 == 0.  h and w1 16-byte aligned.
+ * workspace >= wf_router_workspace_bytes(dt, gamma, d, m) bytes.
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_router_neural(wf_dtype_t dt, const void *h, const void *w1,
+                             const void *b1, const void *w2, const void *b2,
+                             const int32_t *row, int32_t gamma, int32_t d,
+                             int32_t m, float tau_neural, float *delta_out,
+                             int32_t *route_out, void *workspace,
+                             size_t workspace_bytes, void *stream);
+
+/* Workspace for wf_router_neural (0 for invalid arguments). */
+size_t wf_router_workspace_bytes(wf_dtype_t dt, int32_t gamma, int32_t d,
+                                 int32_t m);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,8 @@ EXPORTED_SYMBOLS = (
     "wf_verify_attn_workspace_bytes", "wf_kv_only_prefill",
     "wf_lmhead_accept_entropy", "wf_lmhead_workspace_bytes",
     "wf_kv_only_prefill_workspace_bytes", "wf_verify_attn_tree",
-    "wf_lmhead_accept_tree", "wf_kv_compact_path",
+    "wf_lmhead_accept_tree", "wf_kv_compact_path", "wf_router_neural",
+    "wf_router_workspace_bytes",
 )
 
 
@@ -69,6 +70,11 @@ def _load():
     lib.wf_kv_compact_path.argtypes = [i32, p, p, p, p, i32, i32, i32, i32,
                                        i32, i32, sz, p]
     lib.wf_kv_compact_path.restype = i32
+    lib.wf_router_neural.argtypes = [i32, p, p, p, p, p, p, i32, i32, i32, f32,
+                                     p, p, p, sz, p]
+    lib.wf_router_neural.restype = i32
+    lib.wf_router_workspace_bytes.argtypes = [i32, i32, i32, i32]
+    lib.wf_router_workspace_bytes.restype = sz
     return lib
 
 
@@ -286,3 +292,23 @@ def wf_kv_compact_path(k_cache, v_cache, accept, path, ctx_len, stream=None):
                                 _dev(path, "path"), gamma, int(ctx_len), cap,
                                 hkv, dh, n_layers, stride, _stream(stream))
     _check(st, "wf_kv_compact_path")
+
+
+def wf_router_neural(h, w1, b1, w2, b2, row, tau, delta_out, route_out,
+                     workspace=None, stream=None):
+    """h [gamma][d]; w1 [m][d]; b1, w2 [m]; b2 [1] (one dtype); row: int32
+    device tensor holding the row to route on; outputs fp32 [gamma] and
+    int32 [1]."""
+    gamma, d = h.shape
+    m = w1.shape[0]
+    code = _dtype_code(h)
+    need = int(lib.wf_router_workspace_bytes(code, gamma, d, m))
+    if workspace is None:
+        workspace = alloc_workspace(need, h.device)
+    st = lib.wf_router_neural(code, _dev(h, "h"), _dev(w1, "w1"), _dev(b1, "b1"),
+                              _dev(w2, "w2"), _dev(b2, "b2"), _dev(row, "row"),
+                              gamma, d, m, float(tau), _dev(delta_out, "delta_out"),
+                              _dev(route_out, "route_out"),
+                              _dev(workspace, "workspace"), workspace.numel(),
+                              _stream(stream))
+    _check(st, "wf_router_neural")

@@ -12,6 +12,7 @@ constexpr int kMaxQHeads = 256;
 constexpr int kMaxSplits = 1024;
 constexpr int kMaxPrefillTokens = 4096;
 constexpr int kMaxLayers = 1024;
+constexpr int kMaxRouterHidden = 1 << 16;
 
 inline bool aligned16(const void *p) {
     return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
@@ -265,6 +266,47 @@ wf_status_t wf_lmhead_accept_tree(wf_dtype_t dt, const void *h,
     return wf::launch_lmhead(dt, h, w_lm, logits, tokens, parents, gamma, d,
                              vocab, tau_entropy, argmax_out, entropy_out,
                              accept_out, path_out, workspace,
+                             static_cast<hipStream_t>(stream));
+}
+
+namespace {
+wf_status_t check_router(wf_dtype_t dt, int gamma, int d, int m) {
+    if (!dtype_ok(dt) || gamma < 1 || gamma > kMaxGamma || d < 1 || m < 1 ||
+        m > kMaxRouterHidden)
+        return WF_ERR_INVALID_ARG;
+    if (dt == WF_BF16 && (d % 32 != 0 || m % 16 != 0))
+        return WF_ERR_UNSUPPORTED;
+    return WF_OK;
+}
+}  // namespace
+
+size_t wf_router_workspace_bytes(wf_dtype_t dt, int32_t gamma, int32_t d,
+                                 int32_t m) {
+    if (check_router(dt, gamma, d, m) != WF_OK)
+        return 0;
+    return wf::router_workspace_bytes(gamma, m);
+}
+
+wf_status_t wf_router_neural(wf_dtype_t dt, const void *h, const void *w1,
+                             const void *b1, const void *w2, const void *b2,
+                             const int32_t *row, int32_t gamma, int32_t d,
+                             int32_t m, float tau_neural, float *delta_out,
+                             int32_t *route_out, void *workspace,
+                             size_t workspace_bytes, void *stream) {
+    const wf_status_t st = check_router(dt, gamma, d, m);
+    if (st != WF_OK)
+        return st;
+    if (std::isnan(tau_neural))
+        return WF_ERR_INVALID_ARG;
+    if (!h || !w1 || !b1 || !w2 || !b2 || !row || !delta_out || !route_out)
+        return WF_ERR_INVALID_ARG;
+    if (!aligned16(h) || !aligned16(w1))
+        return WF_ERR_INVALID_ARG;
+    const size_t need = wf::router_workspace_bytes(gamma, m);
+    if (!workspace || workspace_bytes < need || !aligned16(workspace))
+        return WF_ERR_WORKSPACE;
+    return wf::launch_router(dt, h, w1, b1, w2, b2, row, gamma, d, m, tau_neural,
+                             delta_out, route_out, workspace,
                              static_cast<hipStream_t>(stream));
 }
 

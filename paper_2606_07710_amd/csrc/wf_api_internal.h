@@ -53,6 +53,15 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
                           int32_t *accept_out, int32_t *path_out,
                           void *workspace, hipStream_t stream);
 
+// Neural routing policy: delta = w2 . GELU(W1 h + b1) + b2 for every row,
+// route at the row *row names.
+size_t router_workspace_bytes(int gamma, int m);
+wf_status_t launch_router(wf_dtype_t dt, const void *h, const void *w1,
+                          const void *b1, const void *w2, const void *b2,
+                          const int32_t *row, int gamma, int d, int m, float tau,
+                          float *delta_out, int32_t *route_out, void *workspace,
+                          hipStream_t stream);
+
 // Path compaction after tree acceptance: block rows path[t] -> t, t <= n,
 // in n_layers caches layer_stride elements apart.
 wf_status_t launch_compact(wf_dtype_t dt, void *k_cache, void *v_cache,

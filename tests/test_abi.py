@@ -198,3 +198,31 @@ def _compact(**kw):
 ])
 def test_compact_rejects(kw, status):
     assert _compact(**kw) == status
+
+
+def _router(**kw):
+    a = dict(dt=1, h=FAKE, w1=FAKE, b1=FAKE, w2=FAKE, b2=FAKE, row=FAKE,
+             gamma=16, d=4096, m=512, tau=1.0, delta=FAKE, route=FAKE,
+             ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return wf.lib.wf_router_neural(
+        a["dt"], a["h"], a["w1"], a["b1"], a["w2"], a["b2"], a["row"],
+        a["gamma"], a["d"], a["m"], a["tau"], a["delta"], a["route"], a["ws"],
+        a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(h=None), 1), (dict(row=None), 1), (dict(delta=None), 1),
+    (dict(gamma=0), 1), (dict(gamma=65), 1), (dict(m=0), 1), (dict(d=0), 1),
+    (dict(d=100), 2), (dict(m=40), 2), (dict(tau=float("nan")), 1),
+    (dict(w1=ODD), 1), (dict(ws_bytes=100), 3), (dict(ws=None), 3),
+])
+def test_router_rejects(kw, status):
+    assert _router(**kw) == status
+
+
+def test_router_workspace_query():
+    need = wf.lib.wf_router_workspace_bytes(1, 16, 4096, 512)
+    assert need == COUNTER_BLOCK + 16 * 512 * 4
+    assert wf.lib.wf_router_workspace_bytes(1, 16, 4096, 40) == 0
+    assert wf.lib.wf_router_workspace_bytes(0, 3, 100, 40) == COUNTER_BLOCK + 3 * 40 * 4
