@@ -46,6 +46,11 @@ def parse():
                          "default: in a round the catch-up follows the route "
                          "decision and reads the target's features of the "
                          "accepted tokens, so it depends on the verification")
+    ap.add_argument("--router", choices=("entropy", "neural"), default="entropy",
+                    help="routing policy: the entropy rule evaluated with the "
+                         "LM head (default), or the neural policy (a two-layer "
+                         "MLP on the final accepted row's hidden state) as "
+                         "one more call per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0,
                     help="approximate seconds of oracle work for cpu_baseline")
@@ -65,13 +70,15 @@ class Step:
     """Pre-marshalled C-ABI calls of one verification step."""
 
     def __init__(self, w, layers, head, outs, lmouts, draft, tau, ws_attn,
-                 ws_pre, ws_lm, wf, tree=None):
+                 ws_pre, ws_lm, wf, tree=None, router=None):
         self.w, self.layers, self.head = w, layers, head
         self.outs, self.lmouts, self.draft, self.tau = outs, lmouts, draft, tau
         self.ws_attn, self.ws_pre, self.ws_lm, self.wf = ws_attn, ws_pre, ws_lm, wf
         # draft-tree workloads: {"mask", "parents", "path", "k_all", "v_all"}
         # (draft then holds the node tokens)
         self.tree = tree
+        # neural routing policy: {"w1", "b1", "w2", "b2", "delta", "route", "ws"}
+        self.router = router
 
     def build(self, stream, catchup=None):
         """Marshal every call for `stream`; with `catchup` (a second stream),
@@ -109,6 +116,15 @@ class Step:
                                  w.head_dim, w.rope_base, P(self.ws_pre),
                                  self.ws_pre.numel(), s2))
         am, ent, acc = self.lmouts[0]
+        self.route = []
+        rt = self.router
+        if rt:
+            m = rt["w1"].shape[0]
+            row = ctypes.c_void_p(acc.data_ptr() + (12 if tr else 0))
+            self.route = [(code, P(self.head["h"]), P(rt["w1"]), P(rt["b1"]),
+                           P(rt["w2"]), P(rt["b2"]), row, w.gamma, w.hidden, m,
+                           1.0, P(rt["delta"]), P(rt["route"]), P(rt["ws"]),
+                           rt["ws"].numel(), s)]
         if tr:
             self.lm_fn = wf.lib.wf_lmhead_accept_tree
             self.lm = [(code, P(self.head["h"]), P(self.head["w_lm"]), None,
@@ -160,6 +176,10 @@ class Step:
             rc = lib.wf_kv_compact_path(*a)
             if check and rc:
                 raise RuntimeError(f"wf_kv_compact_path: {self.wf.status_string(rc)}")
+        for a in self.route:
+            rc = lib.wf_router_neural(*a)
+            if check and rc:
+                raise RuntimeError(f"wf_router_neural: {self.wf.status_string(rc)}")
 
     def phases(self):
         """(name, C function, argument tuples, stream) of the step's three
@@ -172,6 +192,8 @@ class Step:
         if self.compact:
             ph.append(("compaction", lib.wf_kv_compact_path, self.compact,
                        self.stream))
+        if self.route:
+            ph.append(("router", lib.wf_router_neural, self.route, self.stream))
         return ph
 
 
@@ -338,8 +360,16 @@ def main():
                                 device=dev)
     tau = float(np.median(ent.cpu().numpy()))
 
+    router = None
+    if args.router == "neural":
+        router = W.generate_router(w, device=dev)
+        m = router["w1"].shape[0]
+        router["delta"] = torch.empty(w.gamma, dtype=torch.float32, device=dev)
+        router["route"] = torch.empty(1, dtype=torch.int32, device=dev)
+        router["ws"] = wf.alloc_workspace(int(wf.lib.wf_router_workspace_bytes(
+            1 if w.dtype == "bf16" else 0, w.gamma, w.hidden, m)), dev)
     step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_pre,
-                ws_lm, wf, tree)
+                ws_lm, wf, tree, router)
     stream = torch.cuda.current_stream()
     catchup = torch.cuda.Stream() if args.overlap else None
     step.build(stream, catchup)
@@ -416,6 +446,11 @@ def main():
                                        for k, v in per_call_ms.items()))
 
     by = w.algorithmic_bytes()
+    if router is not None:
+        # the router reads its weights and the verify rows' hidden states
+        m = router["w1"].shape[0]
+        by["router"] = (m * w.hidden + 2 * m + 1 + w.gamma * w.hidden) * w.elem_bytes
+        by["total"] += by["router"]
     achieved = by["attn_per_layer"] / (attn_avg_ms * 1e-3) / 1e9
     step_gbps = by["total"] / (ms_per_step * 1e-3) / 1e9
 
@@ -459,6 +494,7 @@ def main():
                    "graph": bool(graph is not None),
                    "schedule": "one stream, model order" if catchup is None else
                                "catch-up prefill on a second stream"}
+                  | {"router": args.router}
                   | ({"draft_tree": {"nodes": w.gamma - 1,
                                      "depth": len(w.tree_levels),
                                      "nodes_per_depth": list(w.tree_levels)}}

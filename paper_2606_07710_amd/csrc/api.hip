@@ -284,7 +284,7 @@ size_t wf_router_workspace_bytes(wf_dtype_t dt, int32_t gamma, int32_t d,
                                  int32_t m) {
     if (check_router(dt, gamma, d, m) != WF_OK)
         return 0;
-    return wf::router_workspace_bytes(gamma, m);
+    return wf::router_workspace_bytes(dt, gamma, d, m);
 }
 
 wf_status_t wf_router_neural(wf_dtype_t dt, const void *h, const void *w1,
@@ -302,7 +302,7 @@ wf_status_t wf_router_neural(wf_dtype_t dt, const void *h, const void *w1,
         return WF_ERR_INVALID_ARG;
     if (!aligned16(h) || !aligned16(w1))
         return WF_ERR_INVALID_ARG;
-    const size_t need = wf::router_workspace_bytes(gamma, m);
+    const size_t need = wf::router_workspace_bytes(dt, gamma, d, m);
     if (!workspace || workspace_bytes < need || !aligned16(workspace))
         return WF_ERR_WORKSPACE;
     return wf::launch_router(dt, h, w1, b1, w2, b2, row, gamma, d, m, tau_neural,

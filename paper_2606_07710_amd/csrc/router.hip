@@ -13,13 +13,16 @@
 // accepted position from the acceptance call), so no host round trip sits
 // between acceptance and routing.
 //
-// Kernel 1: workgroup g owns hidden units 16g .. 16g+15.  bf16: the 8 waves
-// split the input dimension into interleaved 32-wide chunks, z = W1 h runs
-// on 16x16x32 MFMA (A = 16 units x 32 dims, B = 32 dims x 16 rows), the
-// waves' partial sums meet in LDS in wave order, and each row's 16 units
-// are folded into one partial of delta in unit order.  fp32: one thread per
-// (unit, row) and a plain dot product; one partial per unit.
-// Kernel 2 (one workgroup): delta[r] = b2 + the partials in order, then the
+// Kernel 1 forms z = W1 h without the bias, split over the input dimension
+// so the few hundred hidden units still spread over the chip: workgroup
+// (g, k) owns hidden units 16g .. 16g+15 and the k-th slice of d.  bf16: the
+// 8 waves take interleaved 32-wide chunks of the slice, z runs on 16x16x32
+// MFMA (A = 16 units x 32 dims, B = 32 dims x 16 rows) and the waves'
+// partial sums meet in LDS in wave order.  fp32: one thread per (unit, row),
+// a plain dot product over all of d (one slice).
+// Kernel 2 (one workgroup per 16 hidden units): z = b1 + the slices in
+// order, GELU, times w2, and the 16 units of each row summed in unit order.
+// Kernel 3 (one workgroup): delta = b2 + the unit groups in order, then the
 // route.
 #include "wf_api_internal.h"
 #include "wf_device.h"
@@ -39,33 +42,34 @@ __device__ __forceinline__ float gelu_exact(float x) {
 template <int NBL>
 __global__ __launch_bounds__(kRouterWaves * kWave) void router_hidden_bf16(
     const uint16_t *__restrict__ h, const uint16_t *__restrict__ w1,
-    const uint16_t *__restrict__ b1, const uint16_t *__restrict__ w2,
-    float *__restrict__ parts, int gamma, int d) {
+    float *__restrict__ zpart, int gamma, int d, int m, int chunks_per_slice) {
     __shared__ float zs[kRouterWaves][16][16 * NBL + 1];
     const int u0 = 16 * blockIdx.x;
+    const int ks = blockIdx.y;
     const int wave = wave_id();
     const int lane = threadIdx.x % kWave;
     const int m16 = lane & 15;
     const int c4 = lane >> 4;
-    const int nchunks = d / 32;
+    const int c_begin = ks * chunks_per_slice;
+    const int n_c = max(0, min(chunks_per_slice, d / 32 - c_begin));
 
-    const uint16_t *wp = w1 + (size_t)(u0 + m16) * d + c4 * 8;
+    const uint16_t *wp = w1 + (size_t)(u0 + m16) * d + (size_t)c_begin * 32 + c4 * 8;
     // rows past gamma read row gamma-1: their columns are never used
     const uint16_t *hp[NBL];
 #pragma unroll
     for (int nb = 0; nb < NBL; ++nb)
-        hp[nb] = h + (size_t)min(16 * nb + m16, gamma - 1) * d + c4 * 8;
+        hp[nb] = h + (size_t)min(16 * nb + m16, gamma - 1) * d + (size_t)c_begin * 32 + c4 * 8;
 
     f32x4 acc[NBL];
 #pragma unroll
     for (int nb = 0; nb < NBL; ++nb)
         acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int cb = wave; cb < nchunks; cb += kRouterWaves * kRouterBatch) {
+    for (int cb = wave; cb < n_c; cb += kRouterWaves * kRouterBatch) {
         bf16x8 wr[kRouterBatch], hr[kRouterBatch][NBL];
 #pragma unroll
         for (int u = 0; u < kRouterBatch; ++u) {
             const int c = cb + kRouterWaves * u;
-            if (c < nchunks) {
+            if (c < n_c) {
                 wr[u] = load_bf16x8(wp + c * 32);
 #pragma unroll
                 for (int nb = 0; nb < NBL; ++nb)
@@ -74,7 +78,7 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_hidden_bf16(
         }
 #pragma unroll
         for (int u = 0; u < kRouterBatch; ++u) {
-            if (cb + kRouterWaves * u < nchunks) {
+            if (cb + kRouterWaves * u < n_c) {
 #pragma unroll
                 for (int nb = 0; nb < NBL; ++nb)
                     acc[nb] = mfma16x16x32(wr[u], hr[u][nb], acc[nb]);
@@ -88,48 +92,100 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_hidden_bf16(
         for (int i = 0; i < 4; ++i)
             zs[wave][4 * c4 + i][16 * nb + m16] = acc[nb][i];
     __syncthreads();
-    const int r = threadIdx.x;
-    if (r < gamma) {
-        float p = 0.f;
-        for (int u = 0; u < 16; ++u) {
-            float z = zs[0][u][r];
+    // zpart [ks][m][gamma]
+    for (int idx = threadIdx.x; idx < 16 * gamma; idx += blockDim.x) {
+        const int u = idx / gamma, r = idx % gamma;
+        float z = zs[0][u][r];
 #pragma unroll
-            for (int ww = 1; ww < kRouterWaves; ++ww)
-                z += zs[ww][u][r];
-            z += bf16_to_f32(b1[u0 + u]);
-            p = fmaf(bf16_to_f32(w2[u0 + u]), gelu_exact(z), p);
-        }
-        parts[(size_t)blockIdx.x * gamma + r] = p;
+        for (int ww = 1; ww < kRouterWaves; ++ww)
+            z += zs[ww][u][r];
+        zpart[((size_t)ks * m + u0 + u) * gamma + r] = z;
     }
 }
 
 __global__ __launch_bounds__(256) void router_hidden_f32(
     const float *__restrict__ h, const float *__restrict__ w1,
-    const float *__restrict__ b1, const float *__restrict__ w2,
-    float *__restrict__ parts, int gamma, int d, int m) {
+    float *__restrict__ zpart, int gamma, int d, int m) {
     const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= (long long)m * gamma)
         return;
     const int u = (int)(idx / gamma), r = (int)(idx % gamma);
     const float *wr = w1 + (size_t)u * d;
     const float *hr = h + (size_t)r * d;
-    float z = b1[u];
+    float z = 0.f;
     for (int k = 0; k < d; ++k)
         z = fmaf(wr[k], hr[k], z);
-    parts[(size_t)u * gamma + r] = w2[u] * gelu_exact(z);
+    zpart[(size_t)u * gamma + r] = z;
+}
+
+template <bool BF16>
+__device__ __forceinline__ float ld_param(const void *p, int i) {
+    return BF16 ? bf16_to_f32(static_cast<const uint16_t *>(p)[i])
+                : static_cast<const float *>(p)[i];
+}
+
+constexpr int kMaxSlices = 16;
+
+// part [cdiv(m,16)][gamma]: w2 . GELU(z) over the group's 16 units
+template <bool BF16>
+__global__ __launch_bounds__(256) void router_units(const float *__restrict__ zpart,
+                                                    const void *b1, const void *w2,
+                                                    float *__restrict__ part, int gamma,
+                                                    int m, int n_slices) {
+    __shared__ float cs[16][kRouterMaxGamma + 1];
+    const int u0 = 16 * blockIdx.x;
+    const int u = threadIdx.x / 16;
+    const int rr = threadIdx.x % 16;
+    const bool unit_ok = u0 + u < m;
+    const float bias = unit_ok ? ld_param<BF16>(b1, u0 + u) : 0.f;
+    const float w2u = unit_ok ? ld_param<BF16>(w2, u0 + u) : 0.f;
+#pragma unroll
+    for (int q = 0; q < kRouterMaxGamma / 16; ++q) {
+        const int r = rr + 16 * q;
+        if (r < gamma) {
+            float zs[kMaxSlices];
+#pragma unroll
+            for (int k = 0; k < kMaxSlices; ++k)
+                zs[k] = (unit_ok && k < n_slices)
+                            ? zpart[((size_t)k * m + u0 + u) * gamma + r] : 0.f;
+            float z = bias;
+#pragma unroll
+            for (int k = 0; k < kMaxSlices; ++k)
+                if (k < n_slices)
+                    z += zs[k];
+            cs[u][r] = unit_ok ? w2u * gelu_exact(z) : 0.f;
+        }
+    }
+    __syncthreads();
+    const int r = threadIdx.x;
+    if (r < gamma) {
+        float p = 0.f;
+#pragma unroll
+        for (int uu = 0; uu < 16; ++uu)
+            p += cs[uu][r];
+        part[(size_t)blockIdx.x * gamma + r] = p;
+    }
 }
 
 template <bool BF16>
 __global__ __launch_bounds__(kRouterMaxGamma) void router_finish(
-    const float *__restrict__ parts, const void *b2, const int32_t *row,
-    float tau, float *delta_out, int32_t *route_out, int gamma, int n_parts) {
+    const float *__restrict__ part, const void *b2, const int32_t *row, float tau,
+    float *delta_out, int32_t *route_out, int gamma, int n_groups) {
+    constexpr int kBatch = 16;
     __shared__ float ds[kRouterMaxGamma];
     const int r = threadIdx.x;
     if (r < gamma) {
-        float s = BF16 ? bf16_to_f32(*static_cast<const uint16_t *>(b2))
-                       : *static_cast<const float *>(b2);
-        for (int g = 0; g < n_parts; ++g)
-            s += parts[(size_t)g * gamma + r];
+        float s = ld_param<BF16>(b2, 0);
+        for (int g0 = 0; g0 < n_groups; g0 += kBatch) {
+            float v[kBatch];
+#pragma unroll
+            for (int b = 0; b < kBatch; ++b)
+                v[b] = (g0 + b < n_groups) ? part[(size_t)(g0 + b) * gamma + r] : 0.f;
+#pragma unroll
+            for (int b = 0; b < kBatch; ++b)
+                if (g0 + b < n_groups)
+                    s += v[b];
+        }
         delta_out[r] = s;
         ds[r] = s;
     }
@@ -144,8 +200,21 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
-size_t router_workspace_bytes(int gamma, int m) {
-    return kCounterBytes + (size_t)gamma * m * sizeof(float);
+// Split of the input dimension for the bf16 hidden kernel: enough
+// workgroups to cover the chip, at least four 32-wide chunks per slice.
+static int router_slices(int d, int m) {
+    const int chunks = d / 32;
+    int ks = 1;
+    while ((m / 16) * ks * 2 <= 256 && chunks / (ks * 2) >= 4 && ks * 2 <= kMaxSlices)
+        ks *= 2;
+    return ks;
+}
+
+// Workspace after the zero block: z slices [ks][m][gamma], then the unit
+// group sums [cdiv(m, 16)][gamma].
+size_t router_workspace_bytes(wf_dtype_t dt, int gamma, int d, int m) {
+    const int ks = dt == WF_BF16 ? router_slices(d, m) : 1;
+    return kCounterBytes + ((size_t)ks * m + (size_t)cdiv(m, 16)) * gamma * sizeof(float);
 }
 
 wf_status_t launch_router(wf_dtype_t dt, const void *h, const void *w1,
@@ -153,31 +222,35 @@ wf_status_t launch_router(wf_dtype_t dt, const void *h, const void *w1,
                           const int32_t *row, int gamma, int d, int m, float tau,
                           float *delta_out, int32_t *route_out, void *workspace,
                           hipStream_t stream) {
-    float *parts = reinterpret_cast<float *>(static_cast<char *>(workspace) + kCounterBytes);
-    int n_parts;
+    float *zpart = reinterpret_cast<float *>(static_cast<char *>(workspace) + kCounterBytes);
+    const int groups = cdiv(m, 16);
+    int ks = 1;
     if (dt == WF_BF16) {
-        n_parts = m / 16;
+        ks = router_slices(d, m);
+        const int cps = cdiv(d / 32, ks);
+        const dim3 grid(m / 16, ks);
         const auto *hh = static_cast<const uint16_t *>(h);
         const auto *ww1 = static_cast<const uint16_t *>(w1);
-        const auto *bb1 = static_cast<const uint16_t *>(b1);
-        const auto *ww2 = static_cast<const uint16_t *>(w2);
         switch (cdiv(gamma, 16)) {
-        case 1: router_hidden_bf16<1><<<n_parts, kRouterWaves * kWave, 0, stream>>>(hh, ww1, bb1, ww2, parts, gamma, d); break;
-        case 2: router_hidden_bf16<2><<<n_parts, kRouterWaves * kWave, 0, stream>>>(hh, ww1, bb1, ww2, parts, gamma, d); break;
-        case 3: router_hidden_bf16<3><<<n_parts, kRouterWaves * kWave, 0, stream>>>(hh, ww1, bb1, ww2, parts, gamma, d); break;
-        default: router_hidden_bf16<4><<<n_parts, kRouterWaves * kWave, 0, stream>>>(hh, ww1, bb1, ww2, parts, gamma, d); break;
+        case 1: router_hidden_bf16<1><<<grid, kRouterWaves * kWave, 0, stream>>>(hh, ww1, zpart, gamma, d, m, cps); break;
+        case 2: router_hidden_bf16<2><<<grid, kRouterWaves * kWave, 0, stream>>>(hh, ww1, zpart, gamma, d, m, cps); break;
+        case 3: router_hidden_bf16<3><<<grid, kRouterWaves * kWave, 0, stream>>>(hh, ww1, zpart, gamma, d, m, cps); break;
+        default: router_hidden_bf16<4><<<grid, kRouterWaves * kWave, 0, stream>>>(hh, ww1, zpart, gamma, d, m, cps); break;
         }
-        router_finish<true><<<1, kRouterMaxGamma, 0, stream>>>(parts, b2, row, tau, delta_out,
-                                                               route_out, gamma, n_parts);
     } else {
-        n_parts = m;
         const long long threads = (long long)m * gamma;
         router_hidden_f32<<<(unsigned)((threads + 255) / 256), 256, 0, stream>>>(
-            static_cast<const float *>(h), static_cast<const float *>(w1),
-            static_cast<const float *>(b1), static_cast<const float *>(w2), parts, gamma,
-            d, m);
-        router_finish<false><<<1, kRouterMaxGamma, 0, stream>>>(parts, b2, row, tau, delta_out,
-                                                                route_out, gamma, n_parts);
+            static_cast<const float *>(h), static_cast<const float *>(w1), zpart, gamma, d, m);
+    }
+    float *part = zpart + (size_t)ks * m * gamma;
+    if (dt == WF_BF16) {
+        router_units<true><<<groups, 256, 0, stream>>>(zpart, b1, w2, part, gamma, m, ks);
+        router_finish<true><<<1, kRouterMaxGamma, 0, stream>>>(part, b2, row, tau, delta_out,
+                                                               route_out, gamma, groups);
+    } else {
+        router_units<false><<<groups, 256, 0, stream>>>(zpart, b1, w2, part, gamma, m, ks);
+        router_finish<false><<<1, kRouterMaxGamma, 0, stream>>>(part, b2, row, tau, delta_out,
+                                                                route_out, gamma, groups);
     }
     if (hipGetLastError() != hipSuccess)
         return WF_ERR_HIP;

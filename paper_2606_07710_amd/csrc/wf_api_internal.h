@@ -55,7 +55,7 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
 
 // Neural routing policy: delta = w2 . GELU(W1 h + b1) + b2 for every row,
 // route at the row *row names.
-size_t router_workspace_bytes(int gamma, int m);
+size_t router_workspace_bytes(wf_dtype_t dt, int gamma, int d, int m);
 wf_status_t launch_router(wf_dtype_t dt, const void *h, const void *w1,
                           const void *b1, const void *w2, const void *b2,
                           const int32_t *row, int gamma, int d, int m, float tau,

@@ -222,7 +222,8 @@ def test_router_rejects(kw, status):
 
 
 def test_router_workspace_query():
+    # z in 8 slices of d, then 32 unit-group sums, per row
     need = wf.lib.wf_router_workspace_bytes(1, 16, 4096, 512)
-    assert need == COUNTER_BLOCK + 16 * 512 * 4
+    assert need == COUNTER_BLOCK + (8 * 512 + 32) * 16 * 4
     assert wf.lib.wf_router_workspace_bytes(1, 16, 4096, 40) == 0
-    assert wf.lib.wf_router_workspace_bytes(0, 3, 100, 40) == COUNTER_BLOCK + 3 * 40 * 4
+    assert wf.lib.wf_router_workspace_bytes(0, 3, 100, 40) == COUNTER_BLOCK + (40 + 3) * 3 * 4
