@@ -27,6 +27,12 @@ Paper: arXiv 2606.07710 (WhiFlash).  What each call computes:
   router_mlp       -- the neural routing policy (Sec. 3.3.2 and its
                       appendix): delta = w2 . GELU(W1 h + b1) + b2 per row;
                       route = delta > tau_neural.
+  decoder_forward  -- one full drafter layer (attention + SwiGLU MLP) for
+                      tokens against a cache: what lazy catch-up (Sec. 3.4)
+                      still runs for the last backlog token.
+  catchup          -- lazy catch-up of a drafter's cache: KV-only prefill of
+                      the backlog but its last token, which runs the full
+                      layer.
   layer_forward    -- a full single attention layer, used to pin that KV-only
                       prefill yields the cache a full forward would.
 """
@@ -69,6 +75,9 @@ def _load():
                                            _i, _i, _i, _d]
     lib.wfref_accept_tree.argtypes = [_p, _p, _p, _p, _i, _d, _p, _p, _p]
     lib.wfref_router_mlp.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i, _p]
+    lib.wfref_rmsnorm.argtypes = [_i, _p, _p, _i, _i, _d, _p]
+    lib.wfref_decoder_forward.argtypes = [_i, _p, _i, _i] + [_p] * 9 + [_i] * 5 + \
+        [_d, _d, _p, _p, _i, _p]
     lib.wfref_rope_inplace.argtypes = [_p, _i, _d, _d]
     lib.wfref_rope_inplace.restype = None
     lib.wfref_layer_forward.argtypes = [_i, _p, _p, _p, _p, _p, _i, _i, _i, _i,
@@ -76,7 +85,7 @@ def _load():
     for name in ("wfref_verify_attn", "wfref_verify_attn_rows",
                  "wfref_kv_only_prefill", "wfref_lmhead_rows", "wfref_accept",
                  "wfref_verify_attn_mask", "wfref_accept_tree",
-                 "wfref_router_mlp",
+                 "wfref_router_mlp", "wfref_rmsnorm", "wfref_decoder_forward",
                  "wfref_layer_forward"):
         getattr(lib, name).restype = _i
     _lib = lib
@@ -298,6 +307,81 @@ def router_mlp(h, w1, b1, w2, b2):
 def route_neural(delta, row, tau):
     """Sec. 3.3.2 decision: 1 (autoregressive) iff delta[row] > tau."""
     return int(float(delta[row]) > float(tau))
+
+
+DECODER_WEIGHTS = ("attn_norm", "w_q", "w_k", "w_v", "w_o", "mlp_norm",
+                   "w_gate", "w_up", "w_down")
+
+
+def rmsnorm(x, gain, eps):
+    """x [M][d], gain [d] (one storage type) -> fp64 [M][d]."""
+    lib = _load()
+    x, code = _arr(x)
+    gain, c2 = _arr(gain)
+    if code != c2:
+        raise TypeError("x and gain must share a storage type")
+    M, d = x.shape
+    y = np.empty((M, d), np.float64)
+    _check(lib.wfref_rmsnorm(code, _ptr(x), _ptr(gain), M, d, float(eps), _ptr(y)),
+           "rmsnorm")
+    return y
+
+
+def decoder_forward(r, pos, layer, k_cache, v_cache, n_q_heads, n_kv_heads,
+                    rms_eps, rope_base):
+    """r [M][d]; layer: dict of DECODER_WEIGHTS arrays (storage as r);
+    k_cache, v_cache [Hkv][cap][D] (any storage; rows [0, pos) used).
+    Returns (out [M][d], k_cache, v_cache) in fp64, the caches with rows
+    pos .. pos+M-1 written."""
+    lib = _load()
+    r, code = _arr(r)
+    ws = []
+    for name in DECODER_WEIGHTS:
+        a, c = _arr(layer[name])
+        if c != code:
+            raise TypeError(f"{name} must share r's storage type")
+        ws.append(a)
+    M, d = r.shape
+    hkv, cap, dh = np.asarray(k_cache).shape
+    inter = ws[6].shape[0]
+    kc = _decode64(k_cache)
+    vc = _decode64(v_cache)
+    out = np.empty((M, d), np.float64)
+    rc = lib.wfref_decoder_forward(code, _ptr(r), M, int(pos), *[_ptr(a) for a in ws],
+                                   d, n_q_heads, n_kv_heads, dh, inter,
+                                   float(rms_eps), float(rope_base), _ptr(kc),
+                                   _ptr(vc), cap, _ptr(out))
+    _check(rc, "decoder_forward")
+    return out, kc, vc
+
+
+def catchup(r, pos, layer, k_cache, v_cache, n_q_heads, n_kv_heads, rms_eps,
+            rope_base):
+    """Lazy catch-up over a backlog r [n][d] starting at cache row pos: the
+    first n-1 tokens get K/V only (KV-only prefill of RMSNorm(r) * g1), the
+    last runs the full layer.  Returns (out [d], k_cache, v_cache) fp64."""
+    r = np.asarray(r)
+    n = r.shape[0]
+    kc = _decode64(k_cache)
+    vc = _decode64(v_cache)
+    hkv, cap, dh = kc.shape
+    if n > 1:
+        xn = rmsnorm(r[:n - 1], layer["attn_norm"], rms_eps)
+        k, v = kv_only_prefill(xn, _decode64(layer["w_k"]), _decode64(layer["w_v"]),
+                               pos, hkv, dh, rope_base)
+        kc[:, pos:pos + n - 1] = k
+        vc[:, pos:pos + n - 1] = v
+    out, kc, vc = decoder_forward(r[n - 1:], pos + n - 1, layer, kc, vc, n_q_heads,
+                                  n_kv_heads, rms_eps, rope_base)
+    return out[0], kc, vc
+
+
+def _decode64(a):
+    """fp64 copy of an oracle array (bf16 bit patterns decoded exactly)."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return np.ascontiguousarray(a, np.float64).copy()
 
 
 def rope(v, pos, base):

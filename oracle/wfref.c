@@ -539,6 +539,171 @@ int wfref_router_mlp(int dtype, const void *h, const void *w1, const void *b1,
 }
 
 /* ------------------------------------------------------------------------ *
+ * RMSNorm of M rows: y = x / sqrt(mean(x^2) + eps) * gain (fp64).
+ * ------------------------------------------------------------------------ */
+int wfref_rmsnorm(int dtype, const void *x, const void *gain, int M, int d,
+                  double eps, double *y)
+{
+    if (!valid_dtype(dtype) || M < 1 || d < 1)
+        return 1;
+    for (int m = 0; m < M; ++m) {
+        double ss = 0.0;
+        for (int c = 0; c < d; ++c) {
+            const double xv = elem(x, dtype, (size_t)m * d + c);
+            ss += xv * xv;
+        }
+        const double inv = 1.0 / sqrt(ss / d + eps);
+        for (int c = 0; c < d; ++c)
+            y[(size_t)m * d + c] =
+                elem(x, dtype, (size_t)m * d + c) * inv * elem(gain, dtype, c);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ *
+ * One full decoder layer of a drafter for M tokens at positions
+ * pos .. pos+M-1, against a cache whose rows [0, pos) hold the earlier
+ * tokens.  Lazy catch-up (Sec. 3.4) runs it only for the last backlog
+ * token -- the one whose hidden state the next draft needs -- and forms the
+ * other backlog tokens' K/V alone; a full catch-up runs it for all of them.
+ *   xn  = RMSNorm(r) * g1
+ *   q, k, v = Wq xn, Wk xn, Wv xn; RoPE on q and k at the token's position
+ *   cache rows pos + t <- (k, v)
+ *   a   = causal grouped-query attention of q over cache rows [0, pos + t]
+ *   h1  = r + Wo a
+ *   xn2 = RMSNorm(h1) * g2
+ *   out = h1 + Wd (SiLU(Wg xn2) * (Wu xn2)),  SiLU(x) = x / (1 + exp(-x))
+ * r [M][d], weights in nn.Linear layout (Wq [Hq*D][d], Wk/Wv [Hkv*D][d],
+ * Wo [d][Hq*D], Wg/Wu [inter][d], Wd [d][inter]) and the gains share the
+ * storage code; k_cache, v_cache are fp64 [Hkv][cap][D] and are updated
+ * in place; out [M][d] fp64.
+ * ------------------------------------------------------------------------ */
+int wfref_decoder_forward(int dtype, const void *r, int M, int pos,
+                          const void *g1, const void *wq, const void *wk,
+                          const void *wv, const void *wo, const void *g2,
+                          const void *wg, const void *wu, const void *wd,
+                          int d, int n_q_heads, int n_kv_heads, int head_dim,
+                          int inter, double rms_eps, double rope_base,
+                          double *k_cache, double *v_cache, int cap,
+                          double *out)
+{
+    if (!valid_dtype(dtype) || M < 1 || pos < 0 || pos + M > cap || d < 1 ||
+        n_kv_heads < 1 || n_q_heads % n_kv_heads != 0 || head_dim % 2 != 0 ||
+        inter < 1)
+        return 1;
+    const int qd = n_q_heads * head_dim;
+    const int group = n_q_heads / n_kv_heads;
+    const double scale = 1.0 / sqrt((double)head_dim);
+    double *xn = malloc(sizeof(double) * (size_t)M * d);
+    double *q = malloc(sizeof(double) * (size_t)M * qd);
+    double *a = malloc(sizeof(double) * (size_t)M * qd);
+    double *h1 = malloc(sizeof(double) * (size_t)M * d);
+    double *xn2 = malloc(sizeof(double) * (size_t)d);
+    double *act = malloc(sizeof(double) * (size_t)inter);
+    double *s = malloc(sizeof(double) * (size_t)(pos + M));
+    int rc = 0;
+    if (!xn || !q || !a || !h1 || !xn2 || !act || !s) {
+        rc = 2;
+        goto done;
+    }
+    wfref_rmsnorm(dtype, r, g1, M, d, rms_eps, xn);
+    for (int t = 0; t < M; ++t) {
+        const double *x = xn + (size_t)t * d;
+        for (int o = 0; o < qd; ++o) {
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c)
+                acc += elem(wq, dtype, (size_t)o * d + c) * x[c];
+            q[(size_t)t * qd + o] = acc;
+        }
+        for (int h = 0; h < n_q_heads; ++h)
+            wfref_rope_inplace(q + (size_t)t * qd + (size_t)h * head_dim, head_dim,
+                               (double)(pos + t), rope_base);
+        for (int g = 0; g < n_kv_heads; ++g) {
+            double *kr = k_cache + ((size_t)g * cap + pos + t) * head_dim;
+            double *vr = v_cache + ((size_t)g * cap + pos + t) * head_dim;
+            for (int e = 0; e < head_dim; ++e) {
+                double ak = 0.0, av = 0.0;
+                for (int c = 0; c < d; ++c) {
+                    ak += elem(wk, dtype, ((size_t)g * head_dim + e) * d + c) * x[c];
+                    av += elem(wv, dtype, ((size_t)g * head_dim + e) * d + c) * x[c];
+                }
+                kr[e] = ak;
+                vr[e] = av;
+            }
+            wfref_rope_inplace(kr, head_dim, (double)(pos + t), rope_base);
+        }
+    }
+    for (int t = 0; t < M; ++t)
+        for (int h = 0; h < n_q_heads; ++h) {
+            const int g = h / group;
+            const double *qr = q + (size_t)t * qd + (size_t)h * head_dim;
+            const int n = pos + t + 1;
+            double smax = -INFINITY;
+            for (int j = 0; j < n; ++j) {
+                const double *kr = k_cache + ((size_t)g * cap + j) * head_dim;
+                double dot = 0.0;
+                for (int e = 0; e < head_dim; ++e)
+                    dot += qr[e] * kr[e];
+                s[j] = scale * dot;
+                if (s[j] > smax)
+                    smax = s[j];
+            }
+            double denom = 0.0;
+            for (int j = 0; j < n; ++j) {
+                s[j] = exp(s[j] - smax);
+                denom += s[j];
+            }
+            double *ar = a + (size_t)t * qd + (size_t)h * head_dim;
+            for (int e = 0; e < head_dim; ++e)
+                ar[e] = 0.0;
+            for (int j = 0; j < n; ++j) {
+                const double *vr = v_cache + ((size_t)g * cap + j) * head_dim;
+                for (int e = 0; e < head_dim; ++e)
+                    ar[e] += (s[j] / denom) * vr[e];
+            }
+        }
+    for (int t = 0; t < M; ++t) {
+        const double *ar = a + (size_t)t * qd;
+        double *hr = h1 + (size_t)t * d;
+        for (int o = 0; o < d; ++o) {
+            double acc = 0.0;
+            for (int c = 0; c < qd; ++c)
+                acc += elem(wo, dtype, (size_t)o * qd + c) * ar[c];
+            hr[o] = elem(r, dtype, (size_t)t * d + o) + acc;
+        }
+        double ss = 0.0;
+        for (int c = 0; c < d; ++c)
+            ss += hr[c] * hr[c];
+        const double inv = 1.0 / sqrt(ss / d + rms_eps);
+        for (int c = 0; c < d; ++c)
+            xn2[c] = hr[c] * inv * elem(g2, dtype, c);
+        for (int i = 0; i < inter; ++i) {
+            double zg = 0.0, zu = 0.0;
+            for (int c = 0; c < d; ++c) {
+                zg += elem(wg, dtype, (size_t)i * d + c) * xn2[c];
+                zu += elem(wu, dtype, (size_t)i * d + c) * xn2[c];
+            }
+            act[i] = zg / (1.0 + exp(-zg)) * zu;
+        }
+        for (int o = 0; o < d; ++o) {
+            double acc = 0.0;
+            for (int i = 0; i < inter; ++i)
+                acc += elem(wd, dtype, (size_t)o * inter + i) * act[i];
+            out[(size_t)t * d + o] = hr[o] + acc;
+        }
+    }
+done:
+    free(xn);
+    free(q);
+    free(a);
+    free(h1);
+    free(xn2);
+    free(act);
+    free(s);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ *
  * One full decoder attention layer over a fresh sequence of T tokens
  * (positions pos0 .. pos0+T-1), used only to pin the KV-only prefill: the
  * keys and values it records must equal what KV-only prefill produces for
