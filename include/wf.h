@@ -32,6 +32,14 @@
  *   wf_router_neural          two-layer MLP on the final hidden state ->
  *                             predicted acceptance-length gain and route
  *
+ * and the drafter side of a switch (Sec. 3.4):
+ *
+ *   wf_drafter_catchup        lazy catch-up of a drafter's KV cache over the
+ *                             backlog: KV-only prefill, then the full layer
+ *                             for the last backlog token
+ *   wf_drafter_forward        the drafter's full layer (attention + SwiGLU
+ *                             MLP) for a few tokens
+ *
  * Conventions shared by every call
  *   - Every tensor pointer is DEVICE memory owned by the caller, 16-byte
  *     aligned, densely packed in the layout stated.  The library never
@@ -323,6 +331,77 @@ wf_status_t wf_router_neural(wf_dtype_t dt, const void *h, const void *w1,
 /* Workspace for wf_router_neural (0 for invalid arguments). */
 size_t wf_router_workspace_bytes(wf_dtype_t dt, int32_t gamma, int32_t d,
                                  int32_t m);
+
+/* ------------------------------------------------------------------------
+ * Drafter layer and lazy catch-up (Sec. 3.4: "Lazy Catch-up" defers the
+ * inactive drafter's cache updates until the router switches to it, then
+ * processes the backlog in one batch; "KV-only Prefill" forms only the
+ * attention layer's K/V for the backlog -- all of it but the last token,
+ * whose hidden state the next draft starts from).
+ *
+ * A drafter layer (one pre-norm decoder layer, bf16 weights in nn.Linear
+ * layout; pointers are device memory, the struct itself host memory read
+ * during the call):
+ *   xn  = RMSNorm(r) * attn_norm;  q, k, v = W_q xn, W_k xn, W_v xn with
+ *   rotate-half RoPE on q and k at the token's position (theta_i =
+ *   rope_base^(-2i/D), angles in fp64);  k, v -> cache rows;
+ *   a   = causal grouped-query attention over the cache (scale 1/sqrt(D));
+ *   h1  = r + W_o a;  xn2 = RMSNorm(h1) * mlp_norm;
+ *   out = h1 + W_down (SiLU(W_gate xn2) * (W_up xn2)).
+ * Activations are stored in bf16 between these steps.
+ * ---------------------------------------------------------------------- */
+typedef struct wf_decoder_layer {
+    const void *attn_norm;   /* [hidden] */
+    const void *w_q;         /* [n_q_heads*head_dim][hidden] */
+    const void *w_k;         /* [n_kv_heads*head_dim][hidden] */
+    const void *w_v;         /* [n_kv_heads*head_dim][hidden] */
+    const void *w_o;         /* [hidden][n_q_heads*head_dim] */
+    const void *mlp_norm;    /* [hidden] */
+    const void *w_gate;      /* [inter][hidden] */
+    const void *w_up;        /* [inter][hidden] */
+    const void *w_down;      /* [hidden][inter] */
+    int32_t hidden, n_q_heads, n_kv_heads, head_dim, inter;
+    float rms_eps;
+    double rope_base;
+} wf_decoder_layer_t;
+
+/* The full layer for n_tok tokens at positions pos .. pos+n_tok-1 (causal
+ * among them).  r [n_tok][hidden] is the layer input (pre-norm residual
+ * stream); the tokens' K/V are written to cache rows pos .. pos+n_tok-1 and
+ * attention reads rows [0, pos + t]; out [n_tok][hidden].
+ * Limits: dt == WF_BF16 (else WF_ERR_UNSUPPORTED); 1 <= n_tok <= 64;
+ *         pos >= 0; pos + n_tok <= cap; head_dim in {64, 128};
+ *         n_q_heads % n_kv_heads == 0; hidden, inter and
+ *         n_q_heads*head_dim multiples of 32; weights, r, out and the
+ *         caches 16-byte aligned.
+ * workspace >= wf_drafter_forward_workspace_bytes(...) bytes, zero-filled
+ *         before first use like every workspace (its zero block comes
+ *         first). */
+wf_status_t wf_drafter_forward(wf_dtype_t dt, const wf_decoder_layer_t *layer,
+                               const void *r, int32_t n_tok, int32_t pos,
+                               void *k_cache, void *v_cache, int32_t cap,
+                               void *out, void *workspace,
+                               size_t workspace_bytes, void *stream);
+size_t wf_drafter_forward_workspace_bytes(wf_dtype_t dt,
+                                          const wf_decoder_layer_t *layer,
+                                          int32_t n_tok, int32_t pos);
+
+/* Lazy catch-up over a backlog of n_backlog tokens whose layer inputs are
+ * r [n_backlog][hidden], starting at cache row pos: KV-only prefill of
+ * RMSNorm(r[t]) * attn_norm for t < n_backlog - 1 (cache rows pos ..), then
+ * the full layer for the last token; out [hidden] is its output.  The cache
+ * rows and out equal those of wf_drafter_forward over the whole backlog
+ * (to rounding).  Limits as for wf_drafter_forward, with
+ * 1 <= n_backlog <= 4097 and pos + n_backlog <= cap.
+ * workspace >= wf_drafter_catchup_workspace_bytes(...) bytes. */
+wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer,
+                               const void *r, int32_t n_backlog, int32_t pos,
+                               void *k_cache, void *v_cache, int32_t cap,
+                               void *out, void *workspace,
+                               size_t workspace_bytes, void *stream);
+size_t wf_drafter_catchup_workspace_bytes(wf_dtype_t dt,
+                                          const wf_decoder_layer_t *layer,
+                                          int32_t n_backlog, int32_t pos);
 
 #ifdef __cplusplus
 }

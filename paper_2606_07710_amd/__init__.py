@@ -24,8 +24,23 @@ EXPORTED_SYMBOLS = (
     "wf_lmhead_accept_entropy", "wf_lmhead_workspace_bytes",
     "wf_kv_only_prefill_workspace_bytes", "wf_verify_attn_tree",
     "wf_lmhead_accept_tree", "wf_kv_compact_path", "wf_router_neural",
-    "wf_router_workspace_bytes",
+    "wf_router_workspace_bytes", "wf_drafter_forward",
+    "wf_drafter_forward_workspace_bytes", "wf_drafter_catchup",
+    "wf_drafter_catchup_workspace_bytes",
 )
+
+DECODER_WEIGHTS = ("attn_norm", "w_q", "w_k", "w_v", "w_o", "mlp_norm",
+                   "w_gate", "w_up", "w_down")
+
+
+class DecoderLayer(ctypes.Structure):
+    """wf_decoder_layer_t: device pointers of a drafter layer's weights and
+    its shape."""
+    _fields_ = [(n, ctypes.c_void_p) for n in DECODER_WEIGHTS] + [
+        ("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("inter", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+        ("rope_base", ctypes.c_double)]
 
 
 class WfError(RuntimeError):
@@ -75,6 +90,13 @@ def _load():
     lib.wf_router_neural.restype = i32
     lib.wf_router_workspace_bytes.argtypes = [i32, i32, i32, i32]
     lib.wf_router_workspace_bytes.restype = sz
+    for name in ("wf_drafter_forward", "wf_drafter_catchup"):
+        fn = getattr(lib, name)
+        fn.argtypes = [i32, p, p, i32, i32, p, p, i32, p, p, sz, p]
+        fn.restype = i32
+        q = getattr(lib, name + "_workspace_bytes")
+        q.argtypes = [i32, p, i32, i32]
+        q.restype = sz
     return lib
 
 
@@ -312,3 +334,62 @@ def wf_router_neural(h, w1, b1, w2, b2, row, tau, delta_out, route_out,
                               _dev(workspace, "workspace"), workspace.numel(),
                               _stream(stream))
     _check(st, "wf_router_neural")
+
+
+def decoder_layer(weights, n_q_heads, n_kv_heads, rms_eps, rope_base):
+    """DecoderLayer from a dict of DECODER_WEIGHTS device tensors (bf16)."""
+    w_q, w_k, w_gate = weights["w_q"], weights["w_k"], weights["w_gate"]
+    head_dim = w_q.shape[0] // n_q_heads
+    if w_k.shape[0] != n_kv_heads * head_dim:
+        raise ValueError("w_k rows must be n_kv_heads * head_dim")
+    return DecoderLayer(*[_dev(weights[n], n).value for n in DECODER_WEIGHTS],
+                        w_q.shape[1], n_q_heads, n_kv_heads, head_dim,
+                        w_gate.shape[0], float(rms_eps), float(rope_base))
+
+
+def wf_drafter_forward_workspace_bytes(layer, n_tok, pos) -> int:
+    """Workspace of a bf16 wf_drafter_forward call (0: shapes rejected)."""
+    return int(lib.wf_drafter_forward_workspace_bytes(WF_BF16, ctypes.byref(layer),
+                                                      int(n_tok), int(pos)))
+
+
+def wf_drafter_catchup_workspace_bytes(layer, n_backlog, pos) -> int:
+    """Workspace of a bf16 wf_drafter_catchup call (0: shapes rejected)."""
+    return int(lib.wf_drafter_catchup_workspace_bytes(WF_BF16, ctypes.byref(layer),
+                                                      int(n_backlog), int(pos)))
+
+
+def wf_drafter_forward(layer, r, pos, k_cache, v_cache, out, workspace=None,
+                       stream=None):
+    """layer: DecoderLayer; r, out [n_tok][hidden]; caches [Hkv][cap][D]."""
+    n_tok = r.shape[0]
+    code = _dtype_code(r)
+    need = int(lib.wf_drafter_forward_workspace_bytes(code, ctypes.byref(layer), n_tok,
+                                                      int(pos)))
+    if workspace is None:
+        workspace = alloc_workspace(need, r.device)
+    st = lib.wf_drafter_forward(code, ctypes.byref(layer), _dev(r, "r"), n_tok, int(pos),
+                                _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+                                k_cache.shape[1], _dev(out, "out"),
+                                _dev(workspace, "workspace"), workspace.numel(),
+                                _stream(stream))
+    _check(st, "wf_drafter_forward")
+    return out
+
+
+def wf_drafter_catchup(layer, r, pos, k_cache, v_cache, out, workspace=None,
+                       stream=None):
+    """layer: DecoderLayer; r [n_backlog][hidden]; out [hidden]."""
+    n = r.shape[0]
+    code = _dtype_code(r)
+    need = int(lib.wf_drafter_catchup_workspace_bytes(code, ctypes.byref(layer), n,
+                                                      int(pos)))
+    if workspace is None:
+        workspace = alloc_workspace(need, r.device)
+    st = lib.wf_drafter_catchup(code, ctypes.byref(layer), _dev(r, "r"), n, int(pos),
+                                _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+                                k_cache.shape[1], _dev(out, "out"),
+                                _dev(workspace, "workspace"), workspace.numel(),
+                                _stream(stream))
+    _check(st, "wf_drafter_catchup")
+    return out

@@ -310,6 +310,97 @@ wf_status_t wf_router_neural(wf_dtype_t dt, const void *h, const void *w1,
                              static_cast<hipStream_t>(stream));
 }
 
+namespace {
+// Shapes and pointers of a drafter layer call (the backlog or token count
+// is checked by the caller).
+wf_status_t check_drafter(wf_dtype_t dt, const wf_decoder_layer_t *L, int pos, int last_row,
+                          int cap) {
+    if (!dtype_ok(dt) || !L)
+        return WF_ERR_INVALID_ARG;
+    if (L->hidden < 1 || L->inter < 1 || L->n_kv_heads < 1 || L->n_q_heads < 1 ||
+        L->n_q_heads > kMaxQHeads || L->n_q_heads % L->n_kv_heads != 0)
+        return WF_ERR_INVALID_ARG;
+    if (pos < 0 || (long long)last_row >= cap || cap < 1)
+        return WF_ERR_INVALID_ARG;
+    if (!std::isfinite(L->rope_base) || L->rope_base <= 0.0 || !std::isfinite(L->rms_eps) ||
+        L->rms_eps <= 0.f)
+        return WF_ERR_INVALID_ARG;
+    const void *ws[] = {L->attn_norm, L->w_q, L->w_k, L->w_v, L->w_o,
+                        L->mlp_norm, L->w_gate, L->w_up, L->w_down};
+    for (const void *p : ws)
+        if (!p || !aligned16(p))
+            return WF_ERR_INVALID_ARG;
+    if (dt != WF_BF16 || !head_dim_ok(L->head_dim))
+        return WF_ERR_UNSUPPORTED;
+    if (L->hidden % 32 != 0 || L->inter % 32 != 0 || (L->n_q_heads * L->head_dim) % 32 != 0)
+        return WF_ERR_UNSUPPORTED;
+    return WF_OK;
+}
+}  // namespace
+
+size_t wf_drafter_forward_workspace_bytes(wf_dtype_t dt, const wf_decoder_layer_t *layer,
+                                          int32_t n_tok, int32_t pos) {
+    if (n_tok < 1 || n_tok > kMaxGamma ||
+        check_drafter(dt, layer, pos, pos + n_tok - 1, pos + n_tok) != WF_OK ||
+        !wf::prefill_fits(n_tok, layer->hidden, layer->n_kv_heads, layer->head_dim))
+        return 0;
+    return wf::drafter_forward_workspace_bytes(*layer, n_tok, pos);
+}
+
+wf_status_t wf_drafter_forward(wf_dtype_t dt, const wf_decoder_layer_t *layer, const void *r,
+                               int32_t n_tok, int32_t pos, void *k_cache, void *v_cache,
+                               int32_t cap, void *out, void *workspace,
+                               size_t workspace_bytes, void *stream) {
+    if (n_tok < 1 || n_tok > kMaxGamma)
+        return WF_ERR_INVALID_ARG;
+    const wf_status_t st = check_drafter(dt, layer, pos, pos + n_tok - 1, cap);
+    if (st != WF_OK)
+        return st;
+    if (!r || !k_cache || !v_cache || !out || !aligned16(r) || !aligned16(k_cache) ||
+        !aligned16(v_cache) || !aligned16(out))
+        return WF_ERR_INVALID_ARG;
+    if (!wf::prefill_fits(n_tok, layer->hidden, layer->n_kv_heads, layer->head_dim))
+        return WF_ERR_UNSUPPORTED;
+    const size_t need = wf::drafter_forward_workspace_bytes(*layer, n_tok, pos);
+    if (!workspace || workspace_bytes < need || !aligned16(workspace))
+        return WF_ERR_WORKSPACE;
+    return wf::launch_drafter_forward(*layer, r, n_tok, pos, k_cache, v_cache, cap, out,
+                                      workspace, static_cast<hipStream_t>(stream));
+}
+
+size_t wf_drafter_catchup_workspace_bytes(wf_dtype_t dt, const wf_decoder_layer_t *layer,
+                                          int32_t n_backlog, int32_t pos) {
+    if (n_backlog < 1 || n_backlog > kMaxPrefillTokens + 1 ||
+        check_drafter(dt, layer, pos, pos + n_backlog - 1, pos + n_backlog) != WF_OK)
+        return 0;
+    if (n_backlog > 1 &&
+        !wf::prefill_fits(n_backlog - 1, layer->hidden, layer->n_kv_heads, layer->head_dim))
+        return 0;
+    return wf::drafter_catchup_workspace_bytes(*layer, n_backlog, pos);
+}
+
+wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer, const void *r,
+                               int32_t n_backlog, int32_t pos, void *k_cache, void *v_cache,
+                               int32_t cap, void *out, void *workspace,
+                               size_t workspace_bytes, void *stream) {
+    if (n_backlog < 1 || n_backlog > kMaxPrefillTokens + 1)
+        return WF_ERR_INVALID_ARG;
+    const wf_status_t st = check_drafter(dt, layer, pos, pos + n_backlog - 1, cap);
+    if (st != WF_OK)
+        return st;
+    if (!r || !k_cache || !v_cache || !out || !aligned16(r) || !aligned16(k_cache) ||
+        !aligned16(v_cache) || !aligned16(out))
+        return WF_ERR_INVALID_ARG;
+    if (n_backlog > 1 &&
+        !wf::prefill_fits(n_backlog - 1, layer->hidden, layer->n_kv_heads, layer->head_dim))
+        return WF_ERR_UNSUPPORTED;
+    const size_t need = wf::drafter_catchup_workspace_bytes(*layer, n_backlog, pos);
+    if (!workspace || workspace_bytes < need || !aligned16(workspace))
+        return WF_ERR_WORKSPACE;
+    return wf::launch_drafter_catchup(*layer, r, n_backlog, pos, k_cache, v_cache, cap, out,
+                                      workspace, static_cast<hipStream_t>(stream));
+}
+
 wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
                                const int32_t *accept, const int32_t *path,
                                int32_t gamma, int32_t ctx_len, int32_t cap,

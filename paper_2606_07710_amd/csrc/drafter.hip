@@ -1,0 +1,256 @@
+// drafter.hip -- the drafter side of a switch (Sec. 3.4 of the WhiFlash
+// paper).  Lazy catch-up brings the incoming drafter's KV cache up to date
+// over the backlog in one batch: KV-only prefill for every backlog token but
+// the last, which runs the drafter's full layer -- attention and a SwiGLU
+// MLP -- because the next draft starts from its hidden state.  The full
+// layer for M tokens at positions pos .. pos+M-1:
+//
+//   xn  = RMSNorm(r) * g1                     rmsnorm_bf16
+//   K/V = RoPE(Wk xn), Wv xn  -> cache rows    the KV-only prefill kernel
+//   q   = RoPE(Wq xn)                          skinny linear + reduce_rope_bf16
+//   a   = causal GQA attention over the cache  the verify-attention kernels
+//   h1  = r + Wo a                             skinny linear + reduce_store_bf16
+//   xn2 = RMSNorm(h1) * g2                     rmsnorm_bf16
+//   act = SiLU(Wg xn2) * (Wu xn2)              one skinny linear over [Wg; Wu]
+//                                              + reduce_swiglu_bf16
+//   out = h1 + Wd act                          skinny linear + reduce_store_bf16
+//
+// Activations are rounded to bf16 between the steps, as a bf16 model stores
+// them; every sum runs in fp32 in a fixed order.
+#include <cmath>
+
+#include "wf_api_internal.h"
+#include "wf_device.h"
+
+namespace wf {
+
+namespace {
+
+constexpr int kNormThreads = 256;
+constexpr int kMaxHalfDim = 64;
+
+struct RopeParams {
+    double theta[kMaxHalfDim];   // base^(-2i/D), i < D/2, formed on the host in fp64
+};
+
+// One workgroup per row: the sum of squares in a fixed order (thread
+// strides, then the wave butterfly, then the waves in order).
+__global__ __launch_bounds__(kNormThreads) void rmsnorm_bf16(const uint16_t *__restrict__ x,
+                                                             const uint16_t *__restrict__ g,
+                                                             float eps, uint16_t *__restrict__ y,
+                                                             int d) {
+    __shared__ float part[kNormThreads / kWave];
+    const uint16_t *xr = x + (size_t)blockIdx.x * d;
+    float ss = 0.f;
+    for (int c = threadIdx.x; c < d; c += kNormThreads) {
+        const float v = bf16_to_f32(xr[c]);
+        ss = fmaf(v, v, ss);
+    }
+    ss = wave_sum(ss);
+    if (threadIdx.x % kWave == 0)
+        part[threadIdx.x / kWave] = ss;
+    __syncthreads();
+    float tot = part[0];
+#pragma unroll
+    for (int w = 1; w < kNormThreads / kWave; ++w)
+        tot += part[w];
+    const float inv = 1.f / sqrtf(tot / (float)d + eps);
+    uint16_t *yr = y + (size_t)blockIdx.x * d;
+    for (int c = threadIdx.x; c < d; c += kNormThreads)
+        yr[c] = f32_to_bf16(bf16_to_f32(xr[c]) * inv * bf16_to_f32(g[c]));
+}
+
+__device__ __forceinline__ float sum_slices(const float *zpart, int ks, int n_out, int rows,
+                                            int f, int r) {
+    float s = 0.f;
+    for (int k = 0; k < ks; ++k)
+        s += zpart[((size_t)k * n_out + f) * rows + r];
+    return s;
+}
+
+// y[r][f] = bf16(sum of slices (+ res[r][f]))
+__global__ __launch_bounds__(256) void reduce_store_bf16(const float *__restrict__ zpart, int ks,
+                                                         int n_out, int rows,
+                                                         const uint16_t *__restrict__ res,
+                                                         uint16_t *__restrict__ y) {
+    const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (long long)rows * n_out)
+        return;
+    const int r = (int)(idx / n_out), f = (int)(idx % n_out);
+    float s = sum_slices(zpart, ks, n_out, rows, f, r);
+    if (res)
+        s += bf16_to_f32(res[idx]);
+    y[idx] = f32_to_bf16(s);
+}
+
+// q[r][h][i], q[r][h][i + D/2] = RoPE at position pos + r of the pair's sums
+// (angle formed and reduced modulo 2*pi in fp64, sine and cosine in fp32)
+__global__ __launch_bounds__(256) void reduce_rope_bf16(const float *__restrict__ zpart, int ks,
+                                                        int n_heads, int head_dim, int rows,
+                                                        int pos, RopeParams rp,
+                                                        uint16_t *__restrict__ q) {
+    const int half = head_dim / 2;
+    const int n_out = n_heads * head_dim;
+    const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (long long)rows * n_heads * half)
+        return;
+    const int i = (int)(idx % half);
+    const int h = (int)((idx / half) % n_heads);
+    const int r = (int)(idx / ((long long)half * n_heads));
+    float lo = sum_slices(zpart, ks, n_out, rows, h * head_dim + i, r);
+    float hi = sum_slices(zpart, ks, n_out, rows, h * head_dim + i + half, r);
+    constexpr double kTwoPi = 6.283185307179586;
+    constexpr double kInvTwoPi = 0.15915494309189535;
+    const double phi = (double)(pos + r) * rp.theta[i];
+    const double red = fma(-rint(phi * kInvTwoPi), kTwoPi, phi);
+    float sf, cf;
+    sincosf((float)red, &sf, &cf);
+    const float a = lo, b = hi;
+    lo = a * cf - b * sf;
+    hi = b * cf + a * sf;
+    uint16_t *qr = q + ((size_t)r * n_heads + h) * head_dim;
+    qr[i] = f32_to_bf16(lo);
+    qr[i + half] = f32_to_bf16(hi);
+}
+
+// act[r][i] = bf16(SiLU(gate) * up); features [0, inter) are the gate
+// projection, [inter, 2 inter) the up projection
+__global__ __launch_bounds__(256) void reduce_swiglu_bf16(const float *__restrict__ zpart, int ks,
+                                                          int inter, int rows,
+                                                          uint16_t *__restrict__ act) {
+    const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (long long)rows * inter)
+        return;
+    const int r = (int)(idx / inter), i = (int)(idx % inter);
+    const float gt = sum_slices(zpart, ks, 2 * inter, rows, i, r);
+    const float up = sum_slices(zpart, ks, 2 * inter, rows, inter + i, r);
+    act[idx] = f32_to_bf16(gt / (1.f + expf(-gt)) * up);
+}
+
+inline unsigned blocks_for(long long n) { return (unsigned)((n + 255) / 256); }
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace of the full layer: the attention call's (its zero block first,
+// which the prefill call shares), then the bf16 activations and the fp32
+// linear slices.
+struct DrafterLayout {
+    size_t attn, xn, q, a, h1, xn2, act, zpart, total;
+    AttnPlan plan;
+};
+
+DrafterLayout drafter_layout(const wf_decoder_layer_t &L, int M, int pos) {
+    DrafterLayout o{};
+    const int qd = L.n_q_heads * L.head_dim;
+    o.plan = plan_attn(WF_BF16, M, pos, L.n_q_heads, L.n_kv_heads, L.head_dim, 0);
+    size_t at = align256(attn_workspace_bytes(o.plan, M, L.n_q_heads, L.head_dim));
+    o.attn = 0;
+    o.xn = at;
+    at = align256(at + (size_t)M * L.hidden * 2);
+    o.q = at;
+    at = align256(at + (size_t)M * qd * 2);
+    o.a = at;
+    at = align256(at + (size_t)M * qd * 2);
+    o.h1 = at;
+    at = align256(at + (size_t)M * L.hidden * 2);
+    o.xn2 = at;
+    at = align256(at + (size_t)M * L.hidden * 2);
+    o.act = at;
+    at = align256(at + (size_t)M * L.inter * 2);
+    o.zpart = at;
+    const size_t zq = (size_t)linear_slices(L.hidden, qd) * qd;
+    const size_t zo = (size_t)linear_slices(qd, L.hidden) * L.hidden;
+    const size_t zgu = (size_t)linear_slices(L.hidden, 2 * L.inter) * 2 * L.inter;
+    const size_t zd = (size_t)linear_slices(L.inter, L.hidden) * L.hidden;
+    const size_t zmax = std::max(std::max(zq, zo), std::max(zgu, zd));
+    o.total = align256(at + zmax * M * sizeof(float));
+    return o;
+}
+
+}  // namespace
+
+size_t drafter_forward_workspace_bytes(const wf_decoder_layer_t &L, int M, int pos) {
+    return drafter_layout(L, M, pos).total;
+}
+
+size_t drafter_catchup_workspace_bytes(const wf_decoder_layer_t &L, int n, int pos) {
+    return align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)) +
+           (size_t)(n - 1) * L.hidden * 2;
+}
+
+wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, int M, int pos,
+                                   void *k_cache, void *v_cache, int cap, void *out,
+                                   void *workspace, hipStream_t stream) {
+    const DrafterLayout o = drafter_layout(L, M, pos);
+    char *ws = static_cast<char *>(workspace);
+    const auto *rb = static_cast<const uint16_t *>(r);
+    auto *xn = reinterpret_cast<uint16_t *>(ws + o.xn);
+    auto *q = reinterpret_cast<uint16_t *>(ws + o.q);
+    auto *a = reinterpret_cast<uint16_t *>(ws + o.a);
+    auto *h1 = reinterpret_cast<uint16_t *>(ws + o.h1);
+    auto *xn2 = reinterpret_cast<uint16_t *>(ws + o.xn2);
+    auto *act = reinterpret_cast<uint16_t *>(ws + o.act);
+    auto *zp = reinterpret_cast<float *>(ws + o.zpart);
+    const int d = L.hidden, qd = L.n_q_heads * L.head_dim, I = L.inter;
+    auto W = [](const void *p) { return static_cast<const uint16_t *>(p); };
+    wf_status_t st;
+
+    rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(rb, W(L.attn_norm), L.rms_eps, xn, d);
+    st = launch_prefill(WF_BF16, xn, L.w_k, L.w_v, k_cache, v_cache, M, pos, cap, d,
+                        L.n_kv_heads, L.head_dim, L.rope_base, workspace, stream);
+    if (st != WF_OK)
+        return st;
+    // q = RoPE(Wq xn)
+    if ((st = launch_linear_partial(xn, W(L.w_q), nullptr, qd, 0, M, d, zp, stream)) != WF_OK)
+        return st;
+    RopeParams rp{};
+    for (int i = 0; i < L.head_dim / 2; ++i)
+        rp.theta[i] = std::pow(L.rope_base, -2.0 * (double)i / (double)L.head_dim);
+    reduce_rope_bf16<<<blocks_for((long long)M * qd / 2), 256, 0, stream>>>(
+        zp, linear_slices(d, qd), L.n_q_heads, L.head_dim, M, pos, rp, q);
+    // a = attention over the cache, causal among the M tokens
+    st = launch_attn(WF_BF16, q, k_cache, v_cache, a, M, pos, cap, L.n_q_heads, L.n_kv_heads,
+                     L.head_dim, (float)(1.0 / std::sqrt((double)L.head_dim)), nullptr, o.plan,
+                     workspace, stream);
+    if (st != WF_OK)
+        return st;
+    // h1 = r + Wo a
+    if ((st = launch_linear_partial(a, W(L.w_o), nullptr, d, 0, M, qd, zp, stream)) != WF_OK)
+        return st;
+    reduce_store_bf16<<<blocks_for((long long)M * d), 256, 0, stream>>>(
+        zp, linear_slices(qd, d), d, M, rb, h1);
+    // act = SiLU(Wg xn2) * (Wu xn2)
+    rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(h1, W(L.mlp_norm), L.rms_eps, xn2, d);
+    if ((st = launch_linear_partial(xn2, W(L.w_gate), W(L.w_up), I, I, M, d, zp, stream)) != WF_OK)
+        return st;
+    reduce_swiglu_bf16<<<blocks_for((long long)M * I), 256, 0, stream>>>(
+        zp, linear_slices(d, 2 * I), I, M, act);
+    // out = h1 + Wd act
+    if ((st = launch_linear_partial(act, W(L.w_down), nullptr, d, 0, M, I, zp, stream)) != WF_OK)
+        return st;
+    reduce_store_bf16<<<blocks_for((long long)M * d), 256, 0, stream>>>(
+        zp, linear_slices(I, d), d, M, h1, static_cast<uint16_t *>(out));
+    return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
+}
+
+wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, int n, int pos,
+                                   void *k_cache, void *v_cache, int cap, void *out,
+                                   void *workspace, hipStream_t stream) {
+    const int d = L.hidden;
+    const auto *rb = static_cast<const uint16_t *>(r);
+    if (n > 1) {
+        auto *xnb = reinterpret_cast<uint16_t *>(
+            static_cast<char *>(workspace) + align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)));
+        rmsnorm_bf16<<<n - 1, kNormThreads, 0, stream>>>(rb, static_cast<const uint16_t *>(L.attn_norm),
+                                                         L.rms_eps, xnb, d);
+        const wf_status_t st = launch_prefill(WF_BF16, xnb, L.w_k, L.w_v, k_cache, v_cache, n - 1,
+                                              pos, cap, d, L.n_kv_heads, L.head_dim, L.rope_base,
+                                              workspace, stream);
+        if (st != WF_OK)
+            return st;
+    }
+    return launch_drafter_forward(L, rb + (size_t)(n - 1) * d, 1, pos + n - 1, k_cache, v_cache,
+                                  cap, out, workspace, stream);
+}
+
+}  // namespace wf

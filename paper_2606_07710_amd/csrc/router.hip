@@ -13,13 +13,10 @@
 // accepted position from the acceptance call), so no host round trip sits
 // between acceptance and routing.
 //
-// Kernel 1 forms z = W1 h without the bias, split over the input dimension
-// so the few hundred hidden units still spread over the chip: workgroup
-// (g, k) owns hidden units 16g .. 16g+15 and the k-th slice of d.  bf16: the
-// 8 waves take interleaved 32-wide chunks of the slice, z runs on 16x16x32
-// MFMA (A = 16 units x 32 dims, B = 32 dims x 16 rows) and the waves'
-// partial sums meet in LDS in wave order.  fp32: one thread per (unit, row),
-// a plain dot product over all of d (one slice).
+// Kernel 1 forms z = W1 h without the bias.  bf16: the skinny linear layer
+// of gemv.hip, split over the input dimension so the few hundred hidden
+// units still spread over the chip (one fp32 partial per slice).  fp32: one
+// thread per (unit, row), a plain dot product over all of d (one slice).
 // Kernel 2 (one workgroup per 16 hidden units): z = b1 + the slices in
 // order, GELU, times w2, and the 16 units of each row summed in unit order.
 // Kernel 3 (one workgroup): delta = b2 + the unit groups in order, then the
@@ -31,76 +28,10 @@ namespace wf {
 
 namespace {
 
-constexpr int kRouterWaves = 8;
-constexpr int kRouterBatch = 8;       // 32-wide chunks per wave per load batch
 constexpr int kRouterMaxGamma = 64;
 
 __device__ __forceinline__ float gelu_exact(float x) {
     return 0.5f * x * (1.f + erff(x * 0.70710678118654752f));
-}
-
-template <int NBL>
-__global__ __launch_bounds__(kRouterWaves * kWave) void router_hidden_bf16(
-    const uint16_t *__restrict__ h, const uint16_t *__restrict__ w1,
-    float *__restrict__ zpart, int gamma, int d, int m, int chunks_per_slice) {
-    __shared__ float zs[kRouterWaves][16][16 * NBL + 1];
-    const int u0 = 16 * blockIdx.x;
-    const int ks = blockIdx.y;
-    const int wave = wave_id();
-    const int lane = threadIdx.x % kWave;
-    const int m16 = lane & 15;
-    const int c4 = lane >> 4;
-    const int c_begin = ks * chunks_per_slice;
-    const int n_c = max(0, min(chunks_per_slice, d / 32 - c_begin));
-
-    const uint16_t *wp = w1 + (size_t)(u0 + m16) * d + (size_t)c_begin * 32 + c4 * 8;
-    // rows past gamma read row gamma-1: their columns are never used
-    const uint16_t *hp[NBL];
-#pragma unroll
-    for (int nb = 0; nb < NBL; ++nb)
-        hp[nb] = h + (size_t)min(16 * nb + m16, gamma - 1) * d + (size_t)c_begin * 32 + c4 * 8;
-
-    f32x4 acc[NBL];
-#pragma unroll
-    for (int nb = 0; nb < NBL; ++nb)
-        acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int cb = wave; cb < n_c; cb += kRouterWaves * kRouterBatch) {
-        bf16x8 wr[kRouterBatch], hr[kRouterBatch][NBL];
-#pragma unroll
-        for (int u = 0; u < kRouterBatch; ++u) {
-            const int c = cb + kRouterWaves * u;
-            if (c < n_c) {
-                wr[u] = load_bf16x8(wp + c * 32);
-#pragma unroll
-                for (int nb = 0; nb < NBL; ++nb)
-                    hr[u][nb] = load_bf16x8(hp[nb] + c * 32);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kRouterBatch; ++u) {
-            if (cb + kRouterWaves * u < n_c) {
-#pragma unroll
-                for (int nb = 0; nb < NBL; ++nb)
-                    acc[nb] = mfma16x16x32(wr[u], hr[u][nb], acc[nb]);
-            }
-        }
-    }
-    // lane (m16, c4) holds z of units 4*c4 + i for row 16*nb + m16
-#pragma unroll
-    for (int nb = 0; nb < NBL; ++nb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            zs[wave][4 * c4 + i][16 * nb + m16] = acc[nb][i];
-    __syncthreads();
-    // zpart [ks][m][gamma]
-    for (int idx = threadIdx.x; idx < 16 * gamma; idx += blockDim.x) {
-        const int u = idx / gamma, r = idx % gamma;
-        float z = zs[0][u][r];
-#pragma unroll
-        for (int ww = 1; ww < kRouterWaves; ++ww)
-            z += zs[ww][u][r];
-        zpart[((size_t)ks * m + u0 + u) * gamma + r] = z;
-    }
 }
 
 __global__ __launch_bounds__(256) void router_hidden_f32(
@@ -200,20 +131,8 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
-// Split of the input dimension for the bf16 hidden kernel: enough
-// workgroups to cover the chip, at least four 32-wide chunks per slice.
-static int router_slices(int d, int m) {
-    const int chunks = d / 32;
-    int ks = 1;
-    while ((m / 16) * ks * 2 <= 256 && chunks / (ks * 2) >= 4 && ks * 2 <= kMaxSlices)
-        ks *= 2;
-    return ks;
-}
-
-// Workspace after the zero block: z slices [ks][m][gamma], then the unit
-// group sums [cdiv(m, 16)][gamma].
 size_t router_workspace_bytes(wf_dtype_t dt, int gamma, int d, int m) {
-    const int ks = dt == WF_BF16 ? router_slices(d, m) : 1;
+    const int ks = dt == WF_BF16 ? linear_slices(d, m) : 1;
     return kCounterBytes + ((size_t)ks * m + (size_t)cdiv(m, 16)) * gamma * sizeof(float);
 }
 
@@ -226,17 +145,12 @@ wf_status_t launch_router(wf_dtype_t dt, const void *h, const void *w1,
     const int groups = cdiv(m, 16);
     int ks = 1;
     if (dt == WF_BF16) {
-        ks = router_slices(d, m);
-        const int cps = cdiv(d / 32, ks);
-        const dim3 grid(m / 16, ks);
-        const auto *hh = static_cast<const uint16_t *>(h);
-        const auto *ww1 = static_cast<const uint16_t *>(w1);
-        switch (cdiv(gamma, 16)) {
-        case 1: router_hidden_bf16<1><<<grid, kRouterWaves * kWave, 0, stream>>>(hh, ww1, zpart, gamma, d, m, cps); break;
-        case 2: router_hidden_bf16<2><<<grid, kRouterWaves * kWave, 0, stream>>>(hh, ww1, zpart, gamma, d, m, cps); break;
-        case 3: router_hidden_bf16<3><<<grid, kRouterWaves * kWave, 0, stream>>>(hh, ww1, zpart, gamma, d, m, cps); break;
-        default: router_hidden_bf16<4><<<grid, kRouterWaves * kWave, 0, stream>>>(hh, ww1, zpart, gamma, d, m, cps); break;
-        }
+        ks = linear_slices(d, m);
+        const wf_status_t st = launch_linear_partial(static_cast<const uint16_t *>(h),
+                                                     static_cast<const uint16_t *>(w1),
+                                                     nullptr, m, 0, gamma, d, zpart, stream);
+        if (st != WF_OK)
+            return st;
     } else {
         const long long threads = (long long)m * gamma;
         router_hidden_f32<<<(unsigned)((threads + 255) / 256), 256, 0, stream>>>(

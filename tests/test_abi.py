@@ -227,3 +227,45 @@ def test_router_workspace_query():
     assert need == COUNTER_BLOCK + (8 * 512 + 32) * 16 * 4
     assert wf.lib.wf_router_workspace_bytes(1, 16, 4096, 40) == 0
     assert wf.lib.wf_router_workspace_bytes(0, 3, 100, 40) == COUNTER_BLOCK + (40 + 3) * 3 * 4
+
+
+def _layer(**kw):
+    f = dict(hidden=4096, n_q_heads=32, n_kv_heads=8, head_dim=128, inter=12288,
+             rms_eps=1e-6, rope_base=1e6)
+    f.update(kw)
+    return wf.DecoderLayer(*[FAKE.value] * 9, f["hidden"], f["n_q_heads"],
+                           f["n_kv_heads"], f["head_dim"], f["inter"], f["rms_eps"],
+                           f["rope_base"])
+
+
+def _drafter(fn, layer=None, **kw):
+    a = dict(dt=1, r=FAKE, n=16, pos=4000, k=FAKE, v=FAKE, cap=4200, out=FAKE, ws=FAKE,
+             ws_bytes=1 << 34)
+    a.update(kw)
+    lay = _layer() if layer is None else layer
+    return getattr(wf.lib, fn)(a["dt"], ctypes.byref(lay), a["r"], a["n"], a["pos"],
+                               a["k"], a["v"], a["cap"], a["out"], a["ws"],
+                               a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("fn", ["wf_drafter_forward", "wf_drafter_catchup"])
+@pytest.mark.parametrize("kw,lay,status", [
+    (dict(dt=0), None, 2), (dict(n=0), None, 1), (dict(cap=4015), None, 1),
+    (dict(r=None), None, 1), (dict(out=ODD), None, 1), (dict(pos=-1), None, 1),
+    (dict(ws_bytes=100), None, 3), (dict(ws=None), None, 3),
+    ({}, dict(head_dim=96), 2), ({}, dict(hidden=4010), 2),
+    ({}, dict(n_kv_heads=5), 1), ({}, dict(rms_eps=0.0), 1),
+    ({}, dict(rope_base=-1.0), 1),
+])
+def test_drafter_rejects(fn, kw, lay, status):
+    layer = _layer(**lay) if lay else None
+    assert _drafter(fn, layer, **kw) == status
+
+
+def test_drafter_token_limits():
+    assert _drafter("wf_drafter_forward", n=65, cap=5000) == 1
+    assert _drafter("wf_drafter_catchup", n=4098, cap=9000) == 1
+    lay = _layer()
+    assert wf.lib.wf_drafter_forward_workspace_bytes(1, ctypes.byref(lay), 1, 4096) > COUNTER_BLOCK
+    assert wf.lib.wf_drafter_catchup_workspace_bytes(1, ctypes.byref(lay), 80, 4096) > COUNTER_BLOCK
+    assert wf.lib.wf_drafter_forward_workspace_bytes(0, ctypes.byref(lay), 1, 4096) == 0

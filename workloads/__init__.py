@@ -65,6 +65,9 @@ class Workload:
     # draft-tree verification: nodes per depth below the root (empty: the
     # block is a chain or a diffusion block, verified block-causally)
     tree_levels: tuple = ()
+    # drafter layer of the switch path: MLP width (0: none)
+    inter: int = 0
+    rms_eps: float = 1e-6
 
     @property
     def is_tree(self) -> bool:
@@ -159,6 +162,19 @@ CONFIGS = {
     5: _qwen_like(5, "32b-block16-ctx64k", 64, 5120, 64, 65536, 16, 32, 0.3,
                   "32B shapes, 64 layers, ctx 65536, gamma 16 block-causal, "
                   "32 catch-up tokens per layer, vocab 151936"),
+    7: Workload(cfg=7, name="8b-switch-catchup", dtype="bf16", n_layers=1,
+                hidden=4096, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                ctx_len=4096, gamma=1, vocab=151936, rope_base=1e6,
+                n_prefill=80, prefill_start=4096, prefill_cap=4096 + 80,
+                separate_drafter_cache=True, act_std=1.0, w_std=0.02,
+                qkv_std=0.02 * math.sqrt(4096), accept_p=None,
+                fixed_prefix=0, router_logits=False,
+                description="switch to a one-layer drafter with the 8B "
+                            "attention shapes and a 12288-wide SwiGLU MLP: "
+                            "lazy catch-up of its cache (4096 rows) over a "
+                            "backlog of 80 tokens -- KV-only prefill of 79, "
+                            "the full layer for the last",
+                inter=12288),
     6: _qwen_like(6, "8b-tree61-ctx8k", 36, 4096, 32, 8192,
                   1 + sum(EAGLE_LEVELS), 0, 0.3,
                   "8B shapes, 36 layers, ctx 8192, EAGLE-3-shaped draft tree "
@@ -172,7 +188,7 @@ TENSOR_IDS = {"q": 1, "k_cache": 2, "v_cache": 3, "x": 4, "w_k": 5, "w_v": 6,
               "router_boost": 11, "drafts": 12, "prefix": 13,
               "drafter_k_cache": 14, "drafter_v_cache": 15, "tree": 16,
               "tree_tokens": 17, "router_w1": 18, "router_b1": 19,
-              "router_w2": 20, "router_b2": 21}
+              "router_w2": 20, "router_b2": 21, "drafter": 22, "backlog": 23}
 
 
 def stream_seed(master: int, tensor: str | int, layer: int = 0) -> int:
@@ -406,6 +422,42 @@ def generate_router(w: Workload, device="cpu", seed=None):
         "w2": normal((m,), 0.05, stream_seed(m_seed, "router_w2"), dt, device),
         "b2": normal((1,), 0.05, stream_seed(m_seed, "router_b2"), dt, device),
     }
+
+
+DECODER_WEIGHTS = ("attn_norm", "w_q", "w_k", "w_v", "w_o", "mlp_norm",
+                   "w_gate", "w_up", "w_down")
+
+
+def generate_drafter(w: Workload, device="cpu", seed=None, cache_rows=None):
+    """One drafter layer with random weights (the trained drafters are not
+    available): projections N(0, w_std), RMSNorm gains 1 + N(0, 0.1); its KV
+    cache [Hkv][cap][D] with the first `cache_rows` rows (default ctx_len)
+    N(0, qkv_std) and the rest zero; the backlog's layer inputs r
+    [n_prefill][hidden] N(0, act_std)."""
+    m = master_seed(w.cfg) if seed is None else seed
+    dt = w.torch_dtype
+    d, qd, kd = w.hidden, w.n_q_heads * w.head_dim, w.n_kv_heads * w.head_dim
+    shapes = {"attn_norm": (d,), "w_q": (qd, d), "w_k": (kd, d), "w_v": (kd, d),
+              "w_o": (d, qd), "mlp_norm": (d,), "w_gate": (w.inter, d),
+              "w_up": (w.inter, d), "w_down": (d, w.inter)}
+    out = {}
+    for i, name in enumerate(DECODER_WEIGHTS):
+        s = stream_seed(m, "drafter", i)
+        if name.endswith("norm"):
+            t = normal(shapes[name], 0.1, s, torch.float32, device) + 1.0
+            out[name] = t.to(dt)
+        else:
+            out[name] = normal(shapes[name], w.w_std, s, dt, device)
+    rows = w.ctx_len if cache_rows is None else cache_rows
+    cap = rows + w.n_prefill
+    for name, tid in (("k_cache", 100), ("v_cache", 101)):
+        c = torch.zeros((w.n_kv_heads, cap, w.head_dim), dtype=dt, device=device)
+        if rows:
+            c[:, :rows] = normal((w.n_kv_heads, rows, w.head_dim), w.qkv_std,
+                                 stream_seed(m, "drafter", tid), dt, device)
+        out[name] = c
+    out["r"] = normal((w.n_prefill, d), w.act_std, stream_seed(m, "backlog"), dt, device)
+    return out
 
 
 def generate_head(w: Workload, device="cpu", seed=None):
