@@ -36,8 +36,13 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=3,
-                    help="workload 1..5 (default 3: 8B shapes, ctx 32K, "
-                         "gamma 16, 16 catch-up tokens)")
+                    help="workload 1..7 (default 3: 8B shapes, ctx 32K, "
+                         "gamma 16, 16 catch-up tokens; 6: draft-tree "
+                         "verification; 7: drafter switch catch-up)")
+    ap.add_argument("--switch-table", action="store_true",
+                    help="with --config 7: also sweep base KV length x "
+                         "backlog, compare KV-only catch-up with the full "
+                         "layer over the backlog and with per-round updates")
     ap.add_argument("--graph", action="store_true",
                     help="replay the step as one captured HIP graph")
     ap.add_argument("--overlap", action="store_true",
@@ -284,6 +289,171 @@ def cpu_baseline(w, layers, head, budget_s, max_layers=None, tree_mask=None):
     }
 
 
+def _time_calls(torch, fn, steps, warmup):
+    """Average ms of fn() over `steps` back-to-back calls on the current
+    stream, after `warmup` untimed ones."""
+    for _ in range(warmup):
+        fn()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def bench_switch(args, w):
+    """The drafter side of a switch: lazy catch-up of a one-layer drafter's
+    cache over the backlog (KV-only prefill of all backlog tokens but the
+    last, the full layer for the last).  One step = one catch-up."""
+    import dataclasses
+
+    import numpy as np
+    import torch
+
+    import paper_2606_07710_amd as wf
+    import workloads as W
+
+    dev = "cuda:0"
+    bases = (512, 1024, 2048, 4096, 8192, 16384) if args.switch_table else ()
+    backlogs = (1, 64, 128, 512, 1024) if args.switch_table else ()
+    max_rows = max((w.ctx_len,) + bases) + max((w.n_prefill,) + backlogs)
+    t0 = time.perf_counter()
+    big = dataclasses.replace(w, n_prefill=max(w.n_prefill, *backlogs) if backlogs
+                              else w.n_prefill)
+    t = W.generate_drafter(big, device=dev, cache_rows=max_rows - big.n_prefill)
+    layer = wf.decoder_layer({n: t[n] for n in W.DECODER_WEIGHTS}, w.n_q_heads,
+                             w.n_kv_heads, w.rms_eps, w.rope_base)
+    kc, vc, r_all = t["k_cache"], t["v_cache"], t["r"]
+    torch.cuda.synchronize()
+    log(f"inputs generated in {time.perf_counter() - t0:.1f}s "
+        f"(drafter weights {w.drafter_weight_bytes() / 2**20:.0f} MiB)")
+    ws = wf.alloc_workspace(max(
+        wf.wf_drafter_catchup_workspace_bytes(layer, n, b)
+        for n in (w.n_prefill,) + backlogs for b in (w.ctx_len,) + bases), dev)
+    fws = wf.alloc_workspace(max(
+        [wf.wf_drafter_forward_workspace_bytes(layer, n, b)
+         for n in (1, 64) for b in (w.ctx_len,) + bases]), dev)
+    pws = wf.alloc_workspace(wf.wf_kv_only_prefill_workspace_bytes(
+        1, 64, w.hidden, w.n_kv_heads, w.head_dim), dev)
+    out = torch.empty(w.hidden, dtype=torch.bfloat16, device=dev)
+    fout = torch.empty((64, w.hidden), dtype=torch.bfloat16, device=dev)
+
+    def catchup(n, pos):
+        return lambda: wf.wf_drafter_catchup(layer, r_all[:n], pos, kc, vc, out,
+                                             workspace=ws)
+
+    n, pos = w.n_prefill, w.ctx_len
+    catchup(n, pos)()
+    torch.cuda.synchronize()
+    ms = _time_calls(torch, catchup(n, pos), args.steps, args.warmup)
+    by = w.catchup_bytes(n, pos)
+    gbps = by / (ms * 1e-3) / 1e9
+    log(f"catch-up of {n} tokens at base KV {pos}: {ms * 1e3:.1f} us "
+        f"({gbps:.0f} GB/s of algorithmic bytes)")
+
+    table = None
+    if args.switch_table:
+        table = {"base_kv": list(bases), "backlog": list(backlogs),
+                 "lazy_catchup_us": [], "kv_only_vs_full_layer": [],
+                 "lazy_vs_per_round": []}
+        for b in bases:
+            row = []
+            for nb in backlogs:
+                row.append(round(_time_calls(torch, catchup(nb, b), args.steps,
+                                             args.warmup) * 1e3, 1))
+            table["lazy_catchup_us"].append(row)
+            log(f"base KV {b}: " + ", ".join(f"{nb}: {u} us" for nb, u in
+                                             zip(backlogs, row)))
+        # KV-only catch-up vs the full layer on every backlog token (one
+        # forward call; the forward takes at most 64 tokens)
+        for nb in (1, 16, 32, 64):
+            lazy = _time_calls(torch, catchup(nb, pos), args.steps, args.warmup)
+            full = _time_calls(torch, lambda: wf.wf_drafter_forward(
+                layer, r_all[:nb], pos, kc, vc, fout[:nb], workspace=fws),
+                args.steps, args.warmup)
+            table["kv_only_vs_full_layer"].append(
+                {"backlog": nb, "base_kv": pos, "kv_only_us": round(lazy * 1e3, 1),
+                 "full_layer_us": round(full * 1e3, 1),
+                 "saving": round(1.0 - lazy / full, 3)})
+            log(f"backlog {nb}: KV-only {lazy * 1e3:.1f} us, full layer "
+                f"{full * 1e3:.1f} us")
+        # one batched catch-up vs keeping the cache current every round
+        # (KV-only prefill of each round's tokens, the last token in full at
+        # the switch), same tokens
+        for per_round, rounds in ((4, 20), (8, 10), (2, 40)):
+            nb = per_round * rounds
+
+            def naive(per_round=per_round, rounds=rounds, nb=nb):
+                for k in range(rounds - 1):
+                    wf.wf_kv_only_prefill(r_all[k * per_round:(k + 1) * per_round],
+                                          t["w_k"], t["w_v"], kc, vc,
+                                          pos + k * per_round, w.rope_base,
+                                          workspace=pws)
+                wf.wf_drafter_catchup(layer, r_all[nb - per_round:nb],
+                                      pos + nb - per_round, kc, vc, out, workspace=ws)
+            lazy = _time_calls(torch, catchup(nb, pos), args.steps, args.warmup)
+            per = _time_calls(torch, naive, args.steps, args.warmup)
+            table["lazy_vs_per_round"].append(
+                {"tokens": nb, "rounds": rounds, "lazy_us": round(lazy * 1e3, 1),
+                 "per_round_us": round(per * 1e3, 1)})
+            log(f"{nb} tokens: lazy {lazy * 1e3:.1f} us, per round over {rounds} "
+                f"rounds {per * 1e3:.1f} us")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        host = {k: W.to_oracle(t[k]) for k in W.DECODER_WEIGHTS}
+        rh = W.to_oracle(r_all[:n])
+        kh = W.to_oracle(kc[:, :pos + n].contiguous())
+        vh = W.to_oracle(vc[:, :pos + n].contiguous())
+        t0 = time.perf_counter()
+        oracle.catchup(rh, pos, host, kh, vh, w.n_q_heads, w.n_kv_heads,
+                       w.rms_eps, w.rope_base)
+        cs = time.perf_counter() - t0
+        cpu = {"value": round(cs * 1e6, 1), "unit": "us",
+               "cores": oracle.num_threads(), "kind": "oracle",
+               "sample": f"one whole catch-up ({n} backlog tokens, base KV {pos})",
+               "measured_s": round(cs, 2)}
+
+    line = {
+        "metric": f"drafter switch catch-up us (8B-shape drafter layer, base KV "
+                  f"{pos}, backlog {n}, 1 GPU)",
+        "value": round(ms * 1e3, 2),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded; one drafter layer with the 8B attention "
+                "shapes and a 12288-wide SwiGLU MLP, random weights)",
+        "config": {"workload": w.name, "hidden": w.hidden, "q_heads": w.n_q_heads,
+                   "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "inter": w.inter, "base_kv": pos, "backlog": n},
+        "roofline": {
+            "kernel": "wf_drafter_catchup, whole call (rmsnorm, KV-only "
+                      "prefill, then the full layer for the last token)",
+            "bound": "hbm",
+            "achieved": round(gbps, 1),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(gbps / PEAK_HBM_GBPS, 4),
+            "traffic": None,
+            "bytes_per_launch": by,
+            "avg_launch_us": round(ms * 1e3, 2),
+        },
+        "cpu_baseline": cpu,
+    } | ({"switch_table": table} if table else {})
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -306,6 +476,8 @@ def main():
     torch.cuda.set_device(0)
     w = W.CONFIGS[args.config]
     log(f"workload {w.name}: {w.description}")
+    if w.inter:
+        return bench_switch(args, w)
 
     t0 = time.perf_counter()
     layers = [W.generate_layer(w, l, device=dev) for l in range(w.n_layers)]

@@ -39,6 +39,8 @@
  *                             for the last backlog token
  *   wf_drafter_forward        the drafter's full layer (attention + SwiGLU
  *                             MLP) for a few tokens
+ *   wf_switch_init/commit     host-side lazy catch-up bookkeeping: which
+ *                             backlog is due after each round
  *
  * Conventions shared by every call
  *   - Every tensor pointer is DEVICE memory owned by the caller, 16-byte
@@ -402,6 +404,51 @@ wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer,
 size_t wf_drafter_catchup_workspace_bytes(wf_dtype_t dt,
                                           const wf_decoder_layer_t *layer,
                                           int32_t n_backlog, int32_t pos);
+
+/* ------------------------------------------------------------------------
+ * Lazy catch-up bookkeeping (Sec. 3.4 and its lazy catch-up study in
+ * Sec. 4): a host-side record of how far the autoregressive drafter's KV
+ * cache lags the committed sequence.  Only that drafter's cache can fall
+ * behind: it is the one whose per-token K/V the next draft attends over.
+ * Host memory only; no GPU work.  Under lazy catch-up nothing is due while
+ * the diffusion drafter is active, and the whole backlog is due in one batch
+ * when the router switches back; the naive scheme it is compared with keeps
+ * the cache current every round.  The caller runs each due backlog through
+ * wf_drafter_catchup (r = the backlog tokens' layer inputs, pos = start).
+ * ---------------------------------------------------------------------- */
+#define WF_DRAFTER_AR 0          /* autoregressive drafter (its cache lags)  */
+#define WF_DRAFTER_DIFFUSION 1   /* diffusion (parallel) drafter             */
+
+typedef struct wf_switch_state {
+    int32_t active;        /* drafter of the next round: WF_DRAFTER_*        */
+    int32_t lazy;          /* 1: lazy catch-up; 0: update every round        */
+    int32_t committed;     /* tokens in the sequence (prompt + accepted)     */
+    int32_t ar_cache_len;  /* rows in the AR drafter's KV cache              */
+    int32_t switches;      /* rounds that switched to the AR drafter         */
+    int32_t max_backlog;   /* largest backlog handed out so far              */
+    int64_t caught_up;     /* tokens handed out for catch-up so far          */
+    int64_t catchups;      /* backlogs handed out so far (catch-up calls)    */
+} wf_switch_state_t;
+
+/* Start of a sequence: both drafters have processed the prompt_len prompt
+ * tokens; `active` drafts the first round.  WF_ERR_INVALID_ARG on a null
+ * state, prompt_len < 0, active or lazy out of range. */
+wf_status_t wf_switch_init(wf_switch_state_t *s, int32_t active, int32_t lazy,
+                           int32_t prompt_len);
+
+/* After a verify round: n_new >= 1 tokens joined the sequence (the accepted
+ * drafts plus the bonus token, i.e. accept_out[0] + 1) and the router chose
+ * next_drafter for the next round.  *start and *count receive the backlog
+ * now due -- cache rows and positions start .. start+count-1 -- with
+ * count = 0 when none is.  Lazy: due iff next_drafter is WF_DRAFTER_AR, and
+ * then it is every token since the cache last caught up; naive: the round's
+ * n_new tokens are due every round.  The state records the backlog as
+ * handed out (the caller must run it before the AR drafter drafts again).
+ * WF_ERR_INVALID_ARG (state unchanged) on null pointers, n_new < 1,
+ * next_drafter out of range, or a sequence length past INT32_MAX. */
+wf_status_t wf_switch_commit(wf_switch_state_t *s, int32_t n_new,
+                             int32_t next_drafter, int32_t *start,
+                             int32_t *count);
 
 #ifdef __cplusplus
 }

@@ -26,8 +26,9 @@ EXPORTED_SYMBOLS = (
     "wf_lmhead_accept_tree", "wf_kv_compact_path", "wf_router_neural",
     "wf_router_workspace_bytes", "wf_drafter_forward",
     "wf_drafter_forward_workspace_bytes", "wf_drafter_catchup",
-    "wf_drafter_catchup_workspace_bytes",
+    "wf_drafter_catchup_workspace_bytes", "wf_switch_init", "wf_switch_commit",
 )
+WF_DRAFTER_AR, WF_DRAFTER_DIFFUSION = 0, 1
 
 DECODER_WEIGHTS = ("attn_norm", "w_q", "w_k", "w_v", "w_o", "mlp_norm",
                    "w_gate", "w_up", "w_down")
@@ -41,6 +42,14 @@ class DecoderLayer(ctypes.Structure):
         ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
         ("inter", ctypes.c_int32), ("rms_eps", ctypes.c_float),
         ("rope_base", ctypes.c_double)]
+
+
+class SwitchState(ctypes.Structure):
+    """wf_switch_state_t: host-side lazy catch-up bookkeeping."""
+    _fields_ = [("active", ctypes.c_int32), ("lazy", ctypes.c_int32),
+                ("committed", ctypes.c_int32), ("ar_cache_len", ctypes.c_int32),
+                ("switches", ctypes.c_int32), ("max_backlog", ctypes.c_int32),
+                ("caught_up", ctypes.c_int64), ("catchups", ctypes.c_int64)]
 
 
 class WfError(RuntimeError):
@@ -97,6 +106,10 @@ def _load():
         q = getattr(lib, name + "_workspace_bytes")
         q.argtypes = [i32, p, i32, i32]
         q.restype = sz
+    lib.wf_switch_init.argtypes = [p, i32, i32, i32]
+    lib.wf_switch_init.restype = i32
+    lib.wf_switch_commit.argtypes = [p, i32, i32, p, p]
+    lib.wf_switch_commit.restype = i32
     return lib
 
 
@@ -393,3 +406,19 @@ def wf_drafter_catchup(layer, r, pos, k_cache, v_cache, out, workspace=None,
                                 _stream(stream))
     _check(st, "wf_drafter_catchup")
     return out
+
+
+def wf_switch_init(active, lazy, prompt_len) -> SwitchState:
+    s = SwitchState()
+    _check(lib.wf_switch_init(ctypes.byref(s), int(active), int(lazy), int(prompt_len)),
+           "wf_switch_init")
+    return s
+
+
+def wf_switch_commit(state, n_new, next_drafter):
+    """-> (start, count) of the backlog now due (count 0: none)."""
+    start, count = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib.wf_switch_commit(ctypes.byref(state), int(n_new), int(next_drafter),
+                                ctypes.byref(start), ctypes.byref(count)),
+           "wf_switch_commit")
+    return start.value, count.value

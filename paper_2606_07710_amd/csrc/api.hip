@@ -1,6 +1,8 @@
 // api.hip -- the extern "C" boundary of libwf: argument validation on the
 // host, workspace queries and dispatch to the kernel launchers.  Nothing is
 // enqueued unless every check passes.  The library holds no global state.
+#include <algorithm>
+#include <climits>
 #include <cmath>
 
 #include "wf_api_internal.h"
@@ -44,7 +46,7 @@ wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
 
 extern "C" {
 
-int32_t wf_abi_version(void) { return 4; }
+int32_t wf_abi_version(void) { return 5; }
 
 const char *wf_status_string(wf_status_t s) {
     switch (s) {
@@ -426,6 +428,46 @@ wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
                               ctx_len, cap, n_kv_heads, head_dim, n_layers,
                               n_layers > 1 ? layer_stride : 0,
                               static_cast<hipStream_t>(stream));
+}
+
+wf_status_t wf_switch_init(wf_switch_state_t *s, int32_t active, int32_t lazy,
+                           int32_t prompt_len) {
+    if (!s || prompt_len < 0 || (active != WF_DRAFTER_AR && active != WF_DRAFTER_DIFFUSION) ||
+        (lazy != 0 && lazy != 1))
+        return WF_ERR_INVALID_ARG;
+    *s = wf_switch_state_t{};
+    s->active = active;
+    s->lazy = lazy;
+    s->committed = prompt_len;
+    s->ar_cache_len = prompt_len;
+    return WF_OK;
+}
+
+wf_status_t wf_switch_commit(wf_switch_state_t *s, int32_t n_new, int32_t next_drafter,
+                             int32_t *start, int32_t *count) {
+    if (!s || !start || !count || n_new < 1 ||
+        (next_drafter != WF_DRAFTER_AR && next_drafter != WF_DRAFTER_DIFFUSION))
+        return WF_ERR_INVALID_ARG;
+    if (s->committed < 0 || s->ar_cache_len < 0 || s->ar_cache_len > s->committed ||
+        (long long)s->committed + n_new > INT32_MAX)
+        return WF_ERR_INVALID_ARG;
+    const int32_t committed = s->committed + n_new;
+    const bool due = !s->lazy || next_drafter == WF_DRAFTER_AR;
+    const int32_t from = s->ar_cache_len;
+    const int32_t n = due ? committed - from : 0;
+    if (next_drafter == WF_DRAFTER_AR && s->active != WF_DRAFTER_AR)
+        ++s->switches;
+    s->committed = committed;
+    s->active = next_drafter;
+    if (n > 0) {
+        s->ar_cache_len = committed;
+        s->caught_up += n;
+        ++s->catchups;
+        s->max_backlog = std::max(s->max_backlog, n);
+    }
+    *start = from;
+    *count = n;
+    return WF_OK;
 }
 
 }  // extern "C"

@@ -33,18 +33,44 @@ struct RopeParams {
     double theta[kMaxHalfDim];   // base^(-2i/D), i < D/2, formed on the host in fp64
 };
 
-// One workgroup per row: the sum of squares in a fixed order (thread
-// strides, then the wave butterfly, then the waves in order).
+// One workgroup per row.  Each thread takes 8-element chunks c, c + 256,
+// ... of the row with 16-byte loads, kRowBatch of them issued before any is
+// used; the sum of squares runs in a fixed order (chunk order within a
+// thread, then the wave butterfly, then the waves in order).  The scaling
+// pass reads the row again (a cache hit) with the gains.
+constexpr int kRowBatch = 4;
+
+__device__ __forceinline__ u32x4 load_u32x4(const uint16_t *p) {
+    return *reinterpret_cast<const u32x4 *>(p);
+}
+
+__device__ __forceinline__ float lo_f32(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_f32(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_bf16(const uint16_t *__restrict__ x,
                                                              const uint16_t *__restrict__ g,
                                                              float eps, uint16_t *__restrict__ y,
                                                              int d) {
     __shared__ float part[kNormThreads / kWave];
     const uint16_t *xr = x + (size_t)blockIdx.x * d;
+    const int n_chunks = d / 8;
     float ss = 0.f;
-    for (int c = threadIdx.x; c < d; c += kNormThreads) {
-        const float v = bf16_to_f32(xr[c]);
-        ss = fmaf(v, v, ss);
+    for (int c0 = threadIdx.x; c0 < n_chunks; c0 += kNormThreads * kRowBatch) {
+        u32x4 v[kRowBatch];
+#pragma unroll
+        for (int u = 0; u < kRowBatch; ++u)
+            if (c0 + u * kNormThreads < n_chunks)
+                v[u] = load_u32x4(xr + 8 * (c0 + u * kNormThreads));
+#pragma unroll
+        for (int u = 0; u < kRowBatch; ++u)
+            if (c0 + u * kNormThreads < n_chunks) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float a = lo_f32(v[u][e]), b = hi_f32(v[u][e]);
+                    ss = fmaf(a, a, ss);
+                    ss = fmaf(b, b, ss);
+                }
+            }
     }
     ss = wave_sum(ss);
     if (threadIdx.x % kWave == 0)
@@ -56,8 +82,25 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_bf16(const uint16_t *__r
         tot += part[w];
     const float inv = 1.f / sqrtf(tot / (float)d + eps);
     uint16_t *yr = y + (size_t)blockIdx.x * d;
-    for (int c = threadIdx.x; c < d; c += kNormThreads)
-        yr[c] = f32_to_bf16(bf16_to_f32(xr[c]) * inv * bf16_to_f32(g[c]));
+    for (int c0 = threadIdx.x; c0 < n_chunks; c0 += kNormThreads * kRowBatch) {
+        u32x4 v[kRowBatch], gv[kRowBatch];
+#pragma unroll
+        for (int u = 0; u < kRowBatch; ++u)
+            if (c0 + u * kNormThreads < n_chunks) {
+                v[u] = load_u32x4(xr + 8 * (c0 + u * kNormThreads));
+                gv[u] = load_u32x4(g + 8 * (c0 + u * kNormThreads));
+            }
+#pragma unroll
+        for (int u = 0; u < kRowBatch; ++u)
+            if (c0 + u * kNormThreads < n_chunks) {
+                u32x4 o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    o[e] = pack_bf16x2(lo_f32(v[u][e]) * inv * lo_f32(gv[u][e]),
+                                       hi_f32(v[u][e]) * inv * hi_f32(gv[u][e]));
+                *reinterpret_cast<u32x4 *>(yr + 8 * (c0 + u * kNormThreads)) = o;
+            }
+    }
 }
 
 __device__ __forceinline__ float sum_slices(const float *zpart, int ks, int n_out, int rows,

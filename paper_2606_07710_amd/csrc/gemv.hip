@@ -20,6 +20,7 @@ namespace {
 constexpr int kGemvWaves = 8;
 constexpr int kGemvBatch = 8;          // 32-wide chunks per wave per load batch
 constexpr int kGemvMaxSlices = 16;
+constexpr int kGemvTargetWorkgroups = 1024;
 
 template <int NBL>
 __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
@@ -94,8 +95,10 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 int linear_slices(int k_in, int n_out) {
     const int chunks = k_in / 32;
     const int tiles = n_out / 16;
+    // up to four workgroups per compute unit, at least 4 chunks per slice
     int ks = 1;
-    while (tiles * ks * 2 <= 256 && chunks / (ks * 2) >= 4 && ks * 2 <= kGemvMaxSlices)
+    while (tiles * ks * 2 <= kGemvTargetWorkgroups && chunks / (ks * 2) >= 4 &&
+           ks * 2 <= kGemvMaxSlices)
         ks *= 2;
     return ks;
 }

@@ -112,6 +112,21 @@ class Workload:
                 "lmhead": lm, "router_logits": logits,
                 "total": self.n_layers * (attn + pre) + lm + logits}
 
+    def drafter_weight_bytes(self) -> int:
+        """Bytes of one drafter layer's weights (projections and norms)."""
+        d, qd, kd, i = (self.hidden, self.n_q_heads * self.head_dim,
+                        self.n_kv_heads * self.head_dim, self.inter)
+        return (2 * qd * d + 2 * kd * d + 3 * i * d + 2 * d) * self.elem_bytes
+
+    def catchup_bytes(self, n: int, pos: int) -> int:
+        """Bytes a lazy catch-up over n backlog tokens from cache row pos must
+        move at least once: the layer's weights, the backlog inputs, the K/V
+        rows written, the cache rows the last token attends over, its
+        output."""
+        b, d, kd = self.elem_bytes, self.hidden, self.n_kv_heads * self.head_dim
+        return (self.drafter_weight_bytes() + n * d * b + 2 * n * kd * b
+                + 2 * (pos + n) * kd * b + d * b)
+
     def flops(self) -> dict:
         hq, dh, g, L = self.n_q_heads, self.head_dim, self.gamma, self.ctx_len
         attn = 4 * hq * dh * (g * L + g * (g + 1) // 2)
