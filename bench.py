@@ -4,7 +4,9 @@
 One step = the whole hot path over one synthetic batch, issued on one
 stream in model order:
   n_layers x wf_verify_attn      (block-causal GQA attention vs the cache)
-  n_layers x wf_kv_only_prefill  (catch-up K/V projection + RoPE + append)
+  1 x wf_kv_only_prefill_layers  (catch-up K/V projection + RoPE + append,
+                                  all layers' caches in one launch;
+                                  --prefill-per-layer: one call per layer)
   1 x wf_lmhead_accept_entropy   (LM head -> argmax, entropy, accept, route)
 (the router-heavy workload adds the logits-only LM-head call).  Inputs are
 seeded synthetic tensors already resident in HBM.  The default workload is
@@ -51,6 +53,12 @@ def parse():
                          "default: in a round the catch-up follows the route "
                          "decision and reads the target's features of the "
                          "accepted tokens, so it depends on the verification")
+    ap.add_argument("--prefill-per-layer", action="store_true",
+                    help="one wf_kv_only_prefill call per layer instead of one "
+                         "wf_kv_only_prefill_layers call for all layers")
+    ap.add_argument("--row-major-weights", action="store_true",
+                    help="stream W_k, W_v and W_lm in their row-major layout "
+                         "instead of the tiled copies made once at setup")
     ap.add_argument("--router", choices=("entropy", "neural"), default="entropy",
                     help="routing policy: the entropy rule evaluated with the "
                          "LM head (default), or the neural policy (a two-layer "
@@ -75,7 +83,8 @@ class Step:
     """Pre-marshalled C-ABI calls of one verification step."""
 
     def __init__(self, w, layers, head, outs, lmouts, draft, tau, ws_attn,
-                 ws_pre, ws_lm, wf, tree=None, router=None):
+                 ws_pre, ws_lm, wf, tree=None, router=None, pre_stack=None,
+                 w_lm_tiled=None):
         self.w, self.layers, self.head = w, layers, head
         self.outs, self.lmouts, self.draft, self.tau = outs, lmouts, draft, tau
         self.ws_attn, self.ws_pre, self.ws_lm, self.wf = ws_attn, ws_pre, ws_lm, wf
@@ -84,6 +93,11 @@ class Step:
         self.tree = tree
         # neural routing policy: {"w1", "b1", "w2", "b2", "delta", "route", "ws"}
         self.router = router
+        # all layers' catch-up inputs and caches as [L][...] stacks: one
+        # multi-layer prefill call ({"x", "w_k", "w_v", "k", "v"})
+        self.pre_stack = pre_stack
+        # the LM head's weight in the tiled layout (None: row-major)
+        self.w_lm_tiled = w_lm_tiled
 
     def build(self, stream, catchup=None):
         """Marshal every call for `stream`; with `catchup` (a second stream),
@@ -112,7 +126,7 @@ class Step:
                               w.n_q_heads, w.n_kv_heads, w.head_dim,
                               w.softmax_scale, 0, P(self.ws_attn),
                               self.ws_attn.numel(), s))
-            if w.n_prefill:
+            if w.n_prefill and self.pre_stack is None:
                 kc = t["drafter_k_cache"] if w.separate_drafter_cache else t["k_cache"]
                 vc = t["drafter_v_cache"] if w.separate_drafter_cache else t["v_cache"]
                 self.pre.append((code, P(t["x"]), P(t["w_k"]), P(t["w_v"]), P(kc),
@@ -120,7 +134,19 @@ class Step:
                                  kc.shape[1], w.hidden, w.n_kv_heads,
                                  w.head_dim, w.rope_base, P(self.ws_pre),
                                  self.ws_pre.numel(), s2))
+        self.pre_fn = wf.lib.wf_kv_only_prefill
+        ps = self.pre_stack
+        if ps is not None:
+            self.pre_fn = wf.lib.wf_kv_only_prefill_layers
+            pcode = wf.WF_BF16_TILED if isinstance(ps["w_k"], wf.TiledWeight) else code
+            self.pre = [(pcode, P(ps["x"]), P(ps["w_k"]), P(ps["w_v"]), P(ps["k"]),
+                         P(ps["v"]), w.n_prefill, w.prefill_start, ps["k"].shape[2],
+                         w.hidden, w.n_kv_heads, w.head_dim, w.rope_base,
+                         ps["x"].shape[0], ps["x"].stride(0), ps["w_k"].stride(0),
+                         ps["k"].stride(0), P(self.ws_pre), self.ws_pre.numel(), s2)]
         am, ent, acc = self.lmouts[0]
+        w_lm = self.head["w_lm"] if self.w_lm_tiled is None else self.w_lm_tiled
+        lcode = code if self.w_lm_tiled is None else wf.WF_BF16_TILED
         self.route = []
         rt = self.router
         if rt:
@@ -132,7 +158,7 @@ class Step:
                            rt["ws"].numel(), s)]
         if tr:
             self.lm_fn = wf.lib.wf_lmhead_accept_tree
-            self.lm = [(code, P(self.head["h"]), P(self.head["w_lm"]), None,
+            self.lm = [(lcode, P(self.head["h"]), P(w_lm), None,
                         P(self.draft), P(tr["parents"]), w.gamma, w.hidden,
                         w.vocab, self.tau, P(am), P(ent), P(acc), P(tr["path"]),
                         P(self.ws_lm), self.ws_lm.numel(), s)]
@@ -142,7 +168,7 @@ class Step:
                              ka.shape[0], ka[0].numel(), s)]
             return
         self.lm_fn = wf.lib.wf_lmhead_accept_entropy
-        self.lm = [(code, P(self.head["h"]), P(self.head["w_lm"]), None,
+        self.lm = [(lcode, P(self.head["h"]), P(w_lm), None,
                     P(self.draft), w.gamma, w.hidden, w.vocab, self.tau, P(am),
                     P(ent), P(acc), P(self.ws_lm), self.ws_lm.numel(), s)]
         if w.router_logits:
@@ -154,22 +180,22 @@ class Step:
 
     def run(self, check=False):
         lib = self.wf.lib
+
+        def prefill():
+            for a in self.pre:
+                rc = self.pre_fn(*a)
+                if check and rc:
+                    raise RuntimeError(f"KV-only prefill: {self.wf.status_string(rc)}")
         if self.catchup is not None:
             self.fork.record(self.stream)
             self.catchup.wait_event(self.fork)
-        for l, a in enumerate(self.attn):
+            prefill()                       # marshalled for the catch-up stream
+        for a in self.attn:
             rc = self.attn_fn(*a)
             if check and rc:
                 raise RuntimeError(f"verify attention: {self.wf.status_string(rc)}")
-            if self.catchup is not None and l < len(self.pre):
-                rc = lib.wf_kv_only_prefill(*self.pre[l])
-                if check and rc:
-                    raise RuntimeError(f"wf_kv_only_prefill: {self.wf.status_string(rc)}")
         if self.catchup is None:
-            for a in self.pre:
-                rc = lib.wf_kv_only_prefill(*a)
-                if check and rc:
-                    raise RuntimeError(f"wf_kv_only_prefill: {self.wf.status_string(rc)}")
+            prefill()
         else:
             self.join.record(self.catchup)
             self.stream.wait_event(self.join)
@@ -191,7 +217,7 @@ class Step:
         phases."""
         lib = self.wf.lib
         ph = [("attention", self.attn_fn, self.attn, self.stream),
-              ("prefill", lib.wf_kv_only_prefill, self.pre,
+              ("prefill", self.pre_fn, self.pre,
                self.catchup or self.stream),
               ("lmhead", self.lm_fn, self.lm, self.stream)]
         if self.compact:
@@ -496,6 +522,25 @@ def main():
         tree["mask"] = torch.from_numpy(
             W.ancestor_masks(par).view(np.int64).copy()).to(dev)
         tree["path"] = torch.empty(w.gamma, dtype=torch.int32, device=dev)
+    pre_stack = None
+    if w.n_prefill and w.n_layers > 1 and not args.prefill_per_layer:
+        # the layers' catch-up inputs, weights and caches as dense [L][...]
+        # stacks (per-layer views into them), so one call covers all layers
+        ck, cv = (("drafter_k_cache", "drafter_v_cache") if w.separate_drafter_cache
+                  else ("k_cache", "v_cache"))
+        pre_stack = {}
+        for key, name in (("x", "x"), ("w_k", "w_k"), ("w_v", "w_v"), ("k", ck), ("v", cv)):
+            st = torch.stack([t.pop(name) for t in layers])
+            for l, t in enumerate(layers):
+                t[name] = st[l]
+            pre_stack[key] = st
+            torch.cuda.empty_cache()
+    tiled = w.dtype == "bf16" and not args.row_major_weights
+    if pre_stack is not None and tiled:
+        # static weights: tiled once at setup, as at model load
+        pre_stack["w_k"] = wf.tile_weights(pre_stack["w_k"])
+        pre_stack["w_v"] = wf.tile_weights(pre_stack["w_v"])
+    w_lm_tiled = wf.tile_weights(head["w_lm"]) if tiled else None
     torch.cuda.synchronize()
     log(f"inputs generated in {time.perf_counter() - t0:.1f}s")
 
@@ -505,9 +550,9 @@ def main():
                                           w.gamma, w.ctx_len, w.n_q_heads,
                                           w.n_kv_heads, w.head_dim), dev)
     ws_pre = wf.alloc_workspace(
-        wf.wf_kv_only_prefill_workspace_bytes(1 if w.dtype == "bf16" else 0,
-                                              w.n_prefill, w.hidden,
-                                              w.n_kv_heads, w.head_dim), dev)
+        wf.wf_kv_only_prefill_layers_workspace_bytes(
+            1 if w.dtype == "bf16" else 0, w.n_prefill, w.hidden, w.n_kv_heads,
+            w.head_dim, w.n_layers if pre_stack else 1), dev)
     ws_lm = wf.alloc_workspace(wf.wf_lmhead_workspace_bytes(w.gamma, w.vocab), dev)
     lmouts = [(torch.empty(w.gamma, dtype=torch.int32, device=dev),
                torch.empty(w.gamma, dtype=torch.float32, device=dev),
@@ -541,7 +586,7 @@ def main():
         router["ws"] = wf.alloc_workspace(int(wf.lib.wf_router_workspace_bytes(
             1 if w.dtype == "bf16" else 0, w.gamma, w.hidden, m)), dev)
     step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_pre,
-                ws_lm, wf, tree, router)
+                ws_lm, wf, tree, router, pre_stack, w_lm_tiled)
     stream = torch.cuda.current_stream()
     catchup = torch.cuda.Stream() if args.overlap else None
     step.build(stream, catchup)
@@ -665,7 +710,11 @@ def main():
                    "catch_up_tokens": w.n_prefill, "vocab": w.vocab,
                    "graph": bool(graph is not None),
                    "schedule": "one stream, model order" if catchup is None else
-                               "catch-up prefill on a second stream"}
+                               "catch-up prefill on a second stream",
+                   "prefill": "one call for all layers" if step.pre_stack is not None
+                              else "one call per layer",
+                   "weights": "tiled (16x32 tiles, made once at setup)"
+                              if w_lm_tiled is not None else "row-major"}
                   | {"router": args.router}
                   | ({"draft_tree": {"nodes": w.gamma - 1,
                                      "depth": len(w.tree_levels),

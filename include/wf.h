@@ -15,6 +15,8 @@
  *                             gamma verify rows against the KV cache
  *   wf_kv_only_prefill        K/V projection + RoPE + cache append for
  *                             catch-up tokens
+ *   wf_kv_only_prefill_layers the same for several layers' caches in one
+ *                             launch
  *   wf_lmhead_accept_entropy  LM head reduced to argmax and entropy per row,
  *                             then greedy acceptance and the entropy route
  *
@@ -39,6 +41,8 @@
  *                             for the last backlog token
  *   wf_drafter_forward        the drafter's full layer (attention + SwiGLU
  *                             MLP) for a few tokens
+ *   wf_tile_weights           one-time copy of a weight into the tiled
+ *                             layout the WF_BF16_TILED calls stream
  *   wf_switch_init/commit     host-side lazy catch-up bookkeeping: which
  *                             backlog is due after each round
  *
@@ -82,7 +86,17 @@ typedef enum {
 
 typedef enum {
     WF_F32 = 0,               /* IEEE fp32 storage and arithmetic             */
-    WF_BF16 = 1               /* bf16 storage, fp32 accumulation              */
+    WF_BF16 = 1,              /* bf16 storage, fp32 accumulation              */
+    WF_BF16_TILED = 2         /* as WF_BF16, with the WEIGHT matrices (W_k,
+                                 W_v, W_lm) in the tiled layout that
+                                 wf_tile_weights writes; activations, caches
+                                 and outputs stay row-major.  Accepted by the
+                                 KV-only prefill calls and the LM-head calls
+                                 (where their bf16 kernels for gamma <= 16 and
+                                 d in {4096, 5120}, or d % 512 == 0, apply;
+                                 else WF_ERR_UNSUPPORTED) and nowhere else
+                                 (WF_ERR_INVALID_ARG).  Results are bit-for-bit
+                                 those of WF_BF16 on the untiled weights.     */
 } wf_dtype_t;
 
 /* Version of this ABI (bumped on any signature or semantic change). */
@@ -205,6 +219,38 @@ wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
 size_t wf_kv_only_prefill_workspace_bytes(wf_dtype_t dt, int32_t n_tok,
                                           int32_t d_in, int32_t n_kv_heads,
                                           int32_t head_dim);
+
+/* The same catch-up for n_layers caches in one launch (Sec. 3.4: the
+ * backlog is processed in one batch; the layers' K/V projections are
+ * independent of each other once their inputs are known).  Layer l reads
+ * x + l*x_layer_stride, w_k/w_v + l*w_layer_stride and writes
+ * k_cache/v_cache + l*cache_layer_stride (strides in ELEMENTS; all other
+ * arguments and the per-layer result exactly as wf_kv_only_prefill's).
+ * Limits as wf_kv_only_prefill's, and 1 <= n_layers <= 1024; with
+ * n_layers > 1 the strides must be at least one layer's x [n_tok][d_in],
+ * W [n_kv_heads*head_dim][d_in] and cache [n_kv_heads][cap][head_dim] (no
+ * two layers overlap) and keep every layer 16-byte aligned, else
+ * WF_ERR_INVALID_ARG.  With many layers the launch has enough workgroups
+ * without splitting the input dimension, so the bf16 sums may be formed in
+ * a different (still fixed) order than a single-layer call's.
+ * workspace >= wf_kv_only_prefill_layers_workspace_bytes(...) bytes. */
+wf_status_t wf_kv_only_prefill_layers(wf_dtype_t dt, const void *x,
+                                      const void *w_k, const void *w_v,
+                                      void *k_cache, void *v_cache,
+                                      int32_t n_tok, int32_t start_pos,
+                                      int32_t cap, int32_t d_in,
+                                      int32_t n_kv_heads, int32_t head_dim,
+                                      double rope_base, int32_t n_layers,
+                                      size_t x_layer_stride,
+                                      size_t w_layer_stride,
+                                      size_t cache_layer_stride,
+                                      void *workspace, size_t workspace_bytes,
+                                      void *stream);
+size_t wf_kv_only_prefill_layers_workspace_bytes(wf_dtype_t dt, int32_t n_tok,
+                                                 int32_t d_in,
+                                                 int32_t n_kv_heads,
+                                                 int32_t head_dim,
+                                                 int32_t n_layers);
 
 /* ------------------------------------------------------------------------
  * wf_lmhead_accept_entropy -- LM head, greedy acceptance and entropy route.
@@ -404,6 +450,31 @@ wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer,
 size_t wf_drafter_catchup_workspace_bytes(wf_dtype_t dt,
                                           const wf_decoder_layer_t *layer,
                                           int32_t n_backlog, int32_t pos);
+
+/* ------------------------------------------------------------------------
+ * Tiled weight layout (WF_BF16_TILED).  A bf16 weight W [rows][cols]
+ * (nn.Linear layout, cols % 32 == 0) is stored as 1 KB tiles of 16 rows x
+ * 32 columns: tile (rb, c), rb < ceil(rows/16), c < cols/32, starts at
+ * element (rb * cols/32 + c) * 512, and inside it element
+ * (16*q + r) * 8 + e holds W[16*rb + r][32*c + 8*q + e] (r < 16, q < 4,
+ * e < 8); rows past `rows` are zero.  Each tile is exactly one MFMA operand
+ * load of a wave (lane 16*q + r takes 16 contiguous bytes), so the kernels
+ * stream a weight in contiguous 1 KB pieces instead of 64-byte pieces of 16
+ * rows.  A one-time transform of static weights (at model load), like any
+ * inference engine's weight preprocessing.
+ * ---------------------------------------------------------------------- */
+/* Bytes of the tiled copy of a bf16 [rows][cols] weight (0 if rows < 1,
+ * cols < 32 or cols % 32 != 0). */
+size_t wf_tiled_weight_bytes(int32_t rows, int32_t cols);
+
+/* Writes the tiled copy of the bf16 weight w [rows][cols] into `tiled`
+ * (device, tiled_bytes >= wf_tiled_weight_bytes(rows, cols), 16-byte
+ * aligned, must not overlap w).  Layer stacks: tile each layer's matrix into
+ * its own slot (the tiled size equals the untiled one when rows % 16 == 0).
+ * WF_ERR_INVALID_ARG on null/misaligned pointers or bad sizes,
+ * WF_ERR_WORKSPACE if tiled_bytes is too small. */
+wf_status_t wf_tile_weights(const void *w, int32_t rows, int32_t cols,
+                            void *tiled, size_t tiled_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * Lazy catch-up bookkeeping (Sec. 3.4 and its lazy catch-up study in

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libwf.so")
 
 WF_OK, WF_ERR_INVALID_ARG, WF_ERR_UNSUPPORTED, WF_ERR_WORKSPACE, WF_ERR_HIP = range(5)
-WF_F32, WF_BF16 = 0, 1
+WF_F32, WF_BF16, WF_BF16_TILED = 0, 1, 2
 
 EXPORTED_SYMBOLS = (
     "wf_abi_version", "wf_status_string", "wf_verify_attn",
@@ -27,6 +27,8 @@ EXPORTED_SYMBOLS = (
     "wf_router_workspace_bytes", "wf_drafter_forward",
     "wf_drafter_forward_workspace_bytes", "wf_drafter_catchup",
     "wf_drafter_catchup_workspace_bytes", "wf_switch_init", "wf_switch_commit",
+    "wf_kv_only_prefill_layers", "wf_kv_only_prefill_layers_workspace_bytes",
+    "wf_tiled_weight_bytes", "wf_tile_weights",
 )
 WF_DRAFTER_AR, WF_DRAFTER_DIFFUSION = 0, 1
 
@@ -106,6 +108,15 @@ def _load():
         q = getattr(lib, name + "_workspace_bytes")
         q.argtypes = [i32, p, i32, i32]
         q.restype = sz
+    lib.wf_kv_only_prefill_layers.argtypes = [i32, p, p, p, p, p, i32, i32, i32, i32,
+                                              i32, i32, f64, i32, sz, sz, sz, p, sz, p]
+    lib.wf_kv_only_prefill_layers.restype = i32
+    lib.wf_kv_only_prefill_layers_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
+    lib.wf_kv_only_prefill_layers_workspace_bytes.restype = sz
+    lib.wf_tiled_weight_bytes.argtypes = [i32, i32]
+    lib.wf_tiled_weight_bytes.restype = sz
+    lib.wf_tile_weights.argtypes = [p, i32, i32, p, sz, p]
+    lib.wf_tile_weights.restype = i32
     lib.wf_switch_init.argtypes = [p, i32, i32, i32]
     lib.wf_switch_init.restype = i32
     lib.wf_switch_commit.argtypes = [p, i32, i32, p, p]
@@ -122,6 +133,59 @@ def status_string(status: int) -> str:
 
 def abi_version() -> int:
     return int(lib.wf_abi_version())
+
+
+class TiledWeight:
+    """A bf16 weight (or a [L] stack of them) in the tiled layout that
+    wf_tile_weights writes: `data` [L?][n] holds the tiles, `shape` is the
+    logical [L?][rows][cols].  Passed wherever a weight is, it selects
+    WF_BF16_TILED."""
+
+    def __init__(self, data, shape):
+        self.data, self.shape = data, tuple(shape)
+        self.dtype, self.device, self.is_cuda = data.dtype, data.device, data.is_cuda
+
+    def data_ptr(self):
+        return self.data.data_ptr()
+
+    def is_contiguous(self):
+        return self.data.is_contiguous()
+
+    def stride(self, dim):
+        if dim != 0 or len(self.shape) != 3:
+            raise ValueError("layer stride of a tiled stack only")
+        return self.data.stride(0)
+
+
+def wf_tiled_weight_bytes(rows, cols) -> int:
+    return int(lib.wf_tiled_weight_bytes(int(rows), int(cols)))
+
+
+def tile_weights(w, stream=None) -> TiledWeight:
+    """Tiled copy of a bf16 weight [rows][cols] or stack [L][rows][cols]."""
+    if w.dtype != torch.bfloat16:
+        raise TypeError("tiled weights are bf16")
+    rows, cols = w.shape[-2:]
+    n = wf_tiled_weight_bytes(rows, cols) // 2
+    if n == 0:
+        raise ValueError(f"cannot tile a [{rows}][{cols}] weight (cols % 32 != 0)")
+    layers = w.shape[0] if w.dim() == 3 else None
+    out = torch.empty((layers, n) if layers else (n,), dtype=torch.bfloat16, device=w.device)
+    for l in range(layers or 1):
+        src, dst = (w[l], out[l]) if layers else (w, out)
+        _check(lib.wf_tile_weights(_dev(src, "w"), rows, cols, _dev(dst, "tiled"), 2 * n,
+                                   _stream(stream)), "wf_tile_weights")
+    return TiledWeight(out, w.shape)
+
+
+def _weight_code(x, *ws) -> int:
+    """dtype code of a call whose activations are x and weights ws."""
+    tiled = [isinstance(w, TiledWeight) for w in ws if w is not None]
+    if any(tiled):
+        if not all(tiled) or x.dtype != torch.bfloat16:
+            raise TypeError("tiled weights: all weights tiled, bf16 activations")
+        return WF_BF16_TILED
+    return _dtype_code(x)
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -212,7 +276,7 @@ def wf_kv_only_prefill(x, w_k, w_v, k_cache, v_cache, start_pos, rope_base,
     """x [n][d_in]; w_k, w_v [Hkv*D][d_in]; caches [Hkv][cap][D]."""
     n_tok, d_in = x.shape
     hkv, cap, dh = k_cache.shape
-    code = _dtype_code(x)
+    code = _weight_code(x, w_k, w_v)
     need = wf_kv_only_prefill_workspace_bytes(code, n_tok, d_in, hkv, dh)
     if workspace is None and need:
         workspace = alloc_workspace(need, x.device)
@@ -224,6 +288,36 @@ def wf_kv_only_prefill(x, w_k, w_v, k_cache, v_cache, start_pos, rope_base,
                                 workspace.numel() if workspace is not None else 0,
                                 _stream(stream))
     _check(st, "wf_kv_only_prefill")
+
+
+def wf_kv_only_prefill_layers_workspace_bytes(dtype, n_tok, d_in, n_kv_heads, head_dim,
+                                              n_layers) -> int:
+    code = dtype if isinstance(dtype, int) else (
+        WF_F32 if dtype == torch.float32 else WF_BF16)
+    return int(lib.wf_kv_only_prefill_layers_workspace_bytes(code, n_tok, d_in, n_kv_heads,
+                                                             head_dim, n_layers))
+
+
+def wf_kv_only_prefill_layers(x, w_k, w_v, k_cache, v_cache, start_pos, rope_base,
+                              workspace=None, stream=None):
+    """x [L][n][d_in]; w_k, w_v [L][Hkv*D][d_in]; caches [L][Hkv][cap][D]
+    (each a dense stack, so the layer strides are those of dim 0)."""
+    n_layers, n_tok, d_in = x.shape
+    _, hkv, cap, dh = k_cache.shape
+    if w_k.shape[0] != n_layers or v_cache.stride(0) != k_cache.stride(0) or \
+            w_v.stride(0) != w_k.stride(0) or k_cache.shape[0] != n_layers:
+        raise ValueError("layer stacks must match")
+    code = _weight_code(x, w_k, w_v)
+    need = wf_kv_only_prefill_layers_workspace_bytes(code, n_tok, d_in, hkv, dh, n_layers)
+    if workspace is None and need:
+        workspace = alloc_workspace(need, x.device)
+    st = lib.wf_kv_only_prefill_layers(
+        code, _dev(x, "x"), _dev(w_k, "w_k"), _dev(w_v, "w_v"), _dev(k_cache, "k_cache"),
+        _dev(v_cache, "v_cache"), n_tok, int(start_pos), cap, d_in, hkv, dh,
+        float(rope_base), n_layers, x.stride(0), w_k.stride(0), k_cache.stride(0),
+        _dev(workspace, "workspace"), workspace.numel() if workspace is not None else 0,
+        _stream(stream))
+    _check(st, "wf_kv_only_prefill_layers")
 
 
 def wf_lmhead_accept_entropy(h, w_lm, logits, draft, tau, argmax_out,
@@ -238,7 +332,7 @@ def wf_lmhead_accept_entropy(h, w_lm, logits, draft, tau, argmax_out,
     else:
         gamma, d = h.shape
         vocab = w_lm.shape[0]
-        code = _dtype_code(h)
+        code = _weight_code(h, w_lm)
     need = wf_lmhead_workspace_bytes(gamma, vocab)
     dev = (logits if logits is not None else h).device
     if workspace is None:
@@ -295,7 +389,7 @@ def wf_lmhead_accept_tree(h, w_lm, logits, tokens, parents, tau, argmax_out,
     else:
         gamma, d = h.shape
         vocab = w_lm.shape[0]
-        code = _dtype_code(h)
+        code = _weight_code(h, w_lm)
     need = wf_lmhead_workspace_bytes(gamma, vocab)
     dev = (logits if logits is not None else h).device
     if workspace is None:

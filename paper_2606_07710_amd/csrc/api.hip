@@ -22,6 +22,11 @@ inline bool aligned16(const void *p) {
 
 inline bool dtype_ok(wf_dtype_t dt) { return dt == WF_F32 || dt == WF_BF16; }
 
+// bf16 storage, weights row-major or tiled (the calls that take weights)
+inline bool is_bf16(wf_dtype_t dt) { return dt == WF_BF16 || dt == WF_BF16_TILED; }
+inline bool weight_dtype_ok(wf_dtype_t dt) { return dtype_ok(dt) || dt == WF_BF16_TILED; }
+inline wf_dtype_t storage(wf_dtype_t dt) { return is_bf16(dt) ? WF_BF16 : dt; }
+
 inline bool head_dim_ok(int dh) { return dh == 64 || dh == 128; }
 
 wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
@@ -138,7 +143,7 @@ namespace {
 wf_status_t check_prefill(wf_dtype_t dt, int n_tok, int start_pos, int cap,
                           int d_in, int n_kv_heads, int head_dim,
                           double rope_base) {
-    if (!dtype_ok(dt))
+    if (!weight_dtype_ok(dt))
         return WF_ERR_INVALID_ARG;
     if (n_tok < 0 || n_tok > kMaxPrefillTokens || start_pos < 0 ||
         (long long)start_pos + n_tok > cap || d_in < 1 || n_kv_heads < 1 ||
@@ -148,9 +153,9 @@ wf_status_t check_prefill(wf_dtype_t dt, int n_tok, int start_pos, int cap,
         return WF_ERR_INVALID_ARG;
     if (!head_dim_ok(head_dim))
         return WF_ERR_UNSUPPORTED;
-    if (dt == WF_BF16 && d_in % 32 != 0)
+    if (is_bf16(dt) && d_in % 32 != 0)
         return WF_ERR_UNSUPPORTED;
-    if (dt == WF_BF16 && n_tok > 0 && !wf::prefill_fits(n_tok, d_in, n_kv_heads, head_dim))
+    if (is_bf16(dt) && n_tok > 0 && !wf::prefill_fits(n_tok, d_in, n_kv_heads, head_dim))
         return WF_ERR_UNSUPPORTED;
     return WF_OK;
 }
@@ -161,7 +166,7 @@ size_t wf_kv_only_prefill_workspace_bytes(wf_dtype_t dt, int32_t n_tok,
                                           int32_t head_dim) {
     if (check_prefill(dt, n_tok, 0, n_tok, d_in, n_kv_heads, head_dim, 1.0) != WF_OK)
         return 0;
-    return wf::prefill_workspace_bytes(dt, n_tok, d_in, n_kv_heads, head_dim);
+    return wf::prefill_workspace_bytes(storage(dt), n_tok, d_in, n_kv_heads, head_dim);
 }
 
 wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
@@ -182,12 +187,81 @@ wf_status_t wf_kv_only_prefill(wf_dtype_t dt, const void *x, const void *w_k,
     if (!aligned16(x) || !aligned16(w_k) || !aligned16(w_v) ||
         !aligned16(k_cache) || !aligned16(v_cache))
         return WF_ERR_INVALID_ARG;
-    const size_t need = wf::prefill_workspace_bytes(dt, n_tok, d_in, n_kv_heads, head_dim);
+    const size_t need = wf::prefill_workspace_bytes(storage(dt), n_tok, d_in, n_kv_heads,
+                                                    head_dim);
     if (need && (!workspace || workspace_bytes < need || !aligned16(workspace)))
         return WF_ERR_WORKSPACE;
     return wf::launch_prefill(dt, x, w_k, w_v, k_cache, v_cache, n_tok,
                               start_pos, cap, d_in, n_kv_heads, head_dim,
                               rope_base, workspace, static_cast<hipStream_t>(stream));
+}
+
+namespace {
+wf_status_t check_prefill_layers(wf_dtype_t dt, int n_tok, int cap, int d_in, int n_kv_heads,
+                                 int head_dim, int n_layers, size_t x_ls, size_t w_ls,
+                                 size_t c_ls) {
+    if (n_layers < 1 || n_layers > kMaxLayers)
+        return WF_ERR_INVALID_ARG;
+    if (n_layers == 1)
+        return WF_OK;
+    const size_t eb = is_bf16(dt) ? 2 : 4;
+    if (x_ls < (size_t)n_tok * d_in || w_ls < (size_t)n_kv_heads * head_dim * d_in ||
+        c_ls < (size_t)n_kv_heads * cap * head_dim)
+        return WF_ERR_INVALID_ARG;
+    if ((x_ls * eb) % 16 || (w_ls * eb) % 16 || (c_ls * eb) % 16)
+        return WF_ERR_INVALID_ARG;
+    if (is_bf16(dt) && n_tok > 0 &&
+        !wf::prefill_fits(n_tok, d_in, n_kv_heads, head_dim, n_layers))
+        return WF_ERR_UNSUPPORTED;
+    return WF_OK;
+}
+}  // namespace
+
+size_t wf_kv_only_prefill_layers_workspace_bytes(wf_dtype_t dt, int32_t n_tok, int32_t d_in,
+                                                 int32_t n_kv_heads, int32_t head_dim,
+                                                 int32_t n_layers) {
+    if (check_prefill(dt, n_tok, 0, n_tok, d_in, n_kv_heads, head_dim, 1.0) != WF_OK ||
+        n_layers < 1 || n_layers > kMaxLayers ||
+        (is_bf16(dt) && n_tok > 0 &&
+         !wf::prefill_fits(n_tok, d_in, n_kv_heads, head_dim, n_layers)))
+        return 0;
+    return wf::prefill_workspace_bytes(storage(dt), n_tok, d_in, n_kv_heads, head_dim);
+}
+
+wf_status_t wf_kv_only_prefill_layers(wf_dtype_t dt, const void *x, const void *w_k,
+                                      const void *w_v, void *k_cache, void *v_cache,
+                                      int32_t n_tok, int32_t start_pos, int32_t cap,
+                                      int32_t d_in, int32_t n_kv_heads, int32_t head_dim,
+                                      double rope_base, int32_t n_layers,
+                                      size_t x_layer_stride, size_t w_layer_stride,
+                                      size_t cache_layer_stride, void *workspace,
+                                      size_t workspace_bytes, void *stream) {
+    wf_status_t st = check_prefill(dt, n_tok, start_pos, cap, d_in, n_kv_heads, head_dim,
+                                   rope_base);
+    if (st != WF_OK)
+        return st;
+    st = check_prefill_layers(dt, n_tok, cap, d_in, n_kv_heads, head_dim, n_layers,
+                              x_layer_stride, w_layer_stride, cache_layer_stride);
+    if (st != WF_OK)
+        return st;
+    if (n_tok == 0)
+        return WF_OK;
+    if (!x || !w_k || !w_v || !k_cache || !v_cache)
+        return WF_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(w_k) || !aligned16(w_v) ||
+        !aligned16(k_cache) || !aligned16(v_cache))
+        return WF_ERR_INVALID_ARG;
+    const size_t need = wf::prefill_workspace_bytes(storage(dt), n_tok, d_in, n_kv_heads,
+                                                    head_dim);
+    if (need && (!workspace || workspace_bytes < need || !aligned16(workspace)))
+        return WF_ERR_WORKSPACE;
+    const bool one = n_layers == 1;
+    return wf::launch_prefill(dt, x, w_k, w_v, k_cache, v_cache, n_tok, start_pos, cap, d_in,
+                              n_kv_heads, head_dim, rope_base, workspace,
+                              static_cast<hipStream_t>(stream), n_layers,
+                              one ? 0 : (long long)x_layer_stride,
+                              one ? 0 : (long long)w_layer_stride,
+                              one ? 0 : (long long)cache_layer_stride);
 }
 
 size_t wf_lmhead_workspace_bytes(int32_t gamma, int32_t vocab) {
@@ -213,11 +287,15 @@ wf_status_t check_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
         if (h || w_lm || !aligned16(logits))
             return WF_ERR_INVALID_ARG;
     } else {
-        if (!dtype_ok(dt) || !h || !w_lm || d < 1)
+        if (!weight_dtype_ok(dt) || !h || !w_lm || d < 1)
             return WF_ERR_INVALID_ARG;
         if (!aligned16(h) || !aligned16(w_lm))
             return WF_ERR_INVALID_ARG;
-        if (dt == WF_BF16 && d % 32 != 0)
+        if (is_bf16(dt) && d % 32 != 0)
+            return WF_ERR_UNSUPPORTED;
+        // tiled weights: only the persistent kernels read them
+        if (dt == WF_BF16_TILED &&
+            !((gamma <= 16 && (d == 4096 || d == 5120)) || d % 512 == 0))
             return WF_ERR_UNSUPPORTED;
     }
     if (!argmax_out || !entropy_out || !accept_out)
@@ -428,6 +506,27 @@ wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,
                               ctx_len, cap, n_kv_heads, head_dim, n_layers,
                               n_layers > 1 ? layer_stride : 0,
                               static_cast<hipStream_t>(stream));
+}
+
+size_t wf_tiled_weight_bytes(int32_t rows, int32_t cols) {
+    if (rows < 1 || cols < 32 || cols % 32 != 0)
+        return 0;
+    return wf::tiled_weight_bytes(rows, cols);
+}
+
+wf_status_t wf_tile_weights(const void *w, int32_t rows, int32_t cols, void *tiled,
+                            size_t tiled_bytes, void *stream) {
+    if (!w || !tiled || !aligned16(w) || !aligned16(tiled) || rows < 1 || cols < 32 ||
+        cols % 32 != 0)
+        return WF_ERR_INVALID_ARG;
+    const size_t need = wf::tiled_weight_bytes(rows, cols);
+    if (tiled_bytes < need)
+        return WF_ERR_WORKSPACE;
+    const auto a = reinterpret_cast<uintptr_t>(w), b = reinterpret_cast<uintptr_t>(tiled);
+    const size_t in_bytes = (size_t)rows * cols * 2;
+    if (a < b + need && b < a + in_bytes)
+        return WF_ERR_INVALID_ARG;                  // overlapping copies
+    return wf::launch_tile_weights(w, rows, cols, tiled, static_cast<hipStream_t>(stream));
 }
 
 wf_status_t wf_switch_init(wf_switch_state_t *s, int32_t active, int32_t lazy,

@@ -286,7 +286,7 @@ __global__ __launch_bounds__(512) void lm_tiles_bf16(const uint16_t *__restrict_
 template <int CPW>
 __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict__ h,
                                                       const uint16_t *__restrict__ w,
-                                                      LmFinish f, int vocab) {
+                                                      LmFinish f, int vocab, int tiled) {
     constexpr int D = CPW * 32 * kLmWaves;
     constexpr int P = kLmStreamPrefetch;
     static_assert(CPW % P == 0 && CPW >= P, "chunks per wave");
@@ -313,8 +313,15 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
     // W rows of tile t, block mb.  Rows past the workgroup's run (a ragged
     // last tile) re-read its last row, which is in L2, and are masked out of
     // the states.
+    // (tiled W: the block's 1 KB tiles of this wave's slice, one per chunk,
+    // read contiguously; blocks past the run re-read its last block)
     const int row_end = min(b1 * 16, vocab) - 1;
+    const int cs = tiled ? 512 : 32;               // elements between chunks
     auto wrow = [&](int t, int mb) {
+        if (tiled) {
+            const int blk = min(b0 + kLmMB * t + mb, b1 - 1);
+            return w + ((size_t)blk * (D / 32) + wave * CPW) * 512 + lane * 8;
+        }
         const int row = min((b0 + kLmMB * t + mb) * 16 + m16, row_end);
         return w + (size_t)row * D + wave * CPW * 32 + c4 * 8;
     };
@@ -326,7 +333,7 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
         for (int p = 0; p < P; ++p)
 #pragma unroll
             for (int mb = 0; mb < kLmMB; ++mb)
-                wb[p][mb] = load_bf16x8(wrow(t0, mb) + p * 32);
+                wb[p][mb] = load_bf16x8(wrow(t0, mb) + p * cs);
     }
     RowState run[2] = {state_empty(), state_empty()};
 
@@ -355,11 +362,11 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
             if (u + P < CPW) {
 #pragma unroll
                 for (int mb = 0; mb < kLmMB; ++mb)
-                    wb[p][mb] = load_bf16x8(cur[mb] + (u + P) * 32);
+                    wb[p][mb] = load_bf16x8(cur[mb] + (u + P) * cs);
             } else if (!LAST) {
 #pragma unroll
                 for (int mb = 0; mb < kLmMB; ++mb)
-                    wb[p][mb] = load_bf16x8(nxt[mb] + (u + P - CPW) * 32);
+                    wb[p][mb] = load_bf16x8(nxt[mb] + (u + P - CPW) * cs);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -421,7 +428,7 @@ constexpr int kWideMaxBlocksPerWave = 5;
 template <int NBL, int MBW, int P>
 __global__ __launch_bounds__(512) void lm_wide_bf16(const uint16_t *__restrict__ h,
                                                     const uint16_t *__restrict__ w,
-                                                    LmFinish f, int d, int vocab) {
+                                                    LmFinish f, int d, int vocab, int tiled) {
     constexpr int ROWS = 16 * NBL;
     constexpr int CPB = kWideK / 32;                   // chunks per K-block
     constexpr int HLOADS = ROWS * kWideGran / 512;     // h granules per thread per K-block
@@ -439,11 +446,15 @@ __global__ __launch_bounds__(512) void lm_wide_bf16(const uint16_t *__restrict__
     const int b1 = (int)((long long)(blockIdx.x + 1) * nblk / gridDim.x);
     const int nkb = d / kWideK;
 
+    // chunk 0 of each of this wave's blocks (tiled W: the block's first
+    // 1 KB tile; chunks follow 512 elements apart instead of 32)
+    const int cs = tiled ? 512 : 32;
     const uint16_t *wrow[MBW];
 #pragma unroll
     for (int j = 0; j < MBW; ++j) {
         const int blk = max(min(b0 + wave + 8 * j, b1 - 1), 0);
-        wrow[j] = w + (size_t)min(blk * 16 + m16, vocab - 1) * d + c4 * 8;
+        wrow[j] = tiled ? w + (size_t)blk * (d / 32) * 512 + lane * 8
+                        : w + (size_t)min(blk * 16 + m16, vocab - 1) * d + c4 * 8;
     }
     // h staging: granule idx = threadIdx.x + 512 q of the K-block is row
     // idx / kWideGran, granule idx % kWideGran (rows past gamma repeat the
@@ -488,7 +499,7 @@ __global__ __launch_bounds__(512) void lm_wide_bf16(const uint16_t *__restrict__
         for (int p = 0; p < P; ++p)
 #pragma unroll
             for (int j = 0; j < MBW; ++j)
-                wb[p][j] = load_bf16x8(wrow[j] + p * 32);
+                wb[p][j] = load_bf16x8(wrow[j] + p * cs);
         __syncthreads();
     }
 
@@ -520,7 +531,7 @@ __global__ __launch_bounds__(512) void lm_wide_bf16(const uint16_t *__restrict__
             if (!LAST || u + P < CPB) {
 #pragma unroll
                 for (int j = 0; j < MBW; ++j)
-                    wb[p][j] = load_bf16x8(wrow[j] + (cbase + u + P) * 32);
+                    wb[p][j] = load_bf16x8(wrow[j] + (size_t)(cbase + u + P) * cs);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -638,6 +649,9 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
                           float tau, int32_t *argmax_out, float *entropy_out,
                           int32_t *accept_out, int32_t *path_out,
                           void *workspace, hipStream_t stream) {
+    const int tiled = dt == WF_BF16_TILED ? 1 : 0;
+    if (tiled)
+        dt = WF_BF16;
     char *ws = static_cast<char *>(workspace);
     LmFinish f;
     f.states = reinterpret_cast<RowState *>(ws + kCounterBytes);
@@ -659,9 +673,9 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
         const uint16_t *hb = static_cast<const uint16_t *>(h);
         const uint16_t *wb = static_cast<const uint16_t *>(w_lm);
         if (d == 4096)
-            lm_stream_bf16<16><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, vocab);
+            lm_stream_bf16<16><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, vocab, tiled);
         else
-            lm_stream_bf16<20><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, vocab);
+            lm_stream_bf16<20><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, vocab, tiled);
     } else if (dt == WF_BF16 && d % kWideK == 0) {
         // persistent: about one workgroup per CU, each wave at most
         // kWideMaxBlocksPerWave 16-row vocabulary blocks
@@ -674,12 +688,15 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
         const int nbl = cdiv(gamma, 16);
 #define WF_WIDE(NBLV, MBWV, PV)                                                              \
     if (nbl == NBLV && mbw <= MBWV) {                                                      \
-        lm_wide_bf16<NBLV, MBWV, PV><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, d, vocab);  \
+        lm_wide_bf16<NBLV, MBWV, PV><<<f.n_tiles, 512, 0, stream>>>(hb, wb, f, d, vocab,   \
+                                                                    tiled);                \
     } else
         WF_WIDE(1, 2, 4) WF_WIDE(1, 5, 4) WF_WIDE(2, 2, 4) WF_WIDE(2, 5, 4)
         WF_WIDE(3, 2, 4) WF_WIDE(3, 5, 2) WF_WIDE(4, 2, 4) WF_WIDE(4, 5, 2)
         { return WF_ERR_UNSUPPORTED; }
 #undef WF_WIDE
+    } else if (tiled) {
+        return WF_ERR_UNSUPPORTED;              // no tiled form of the tile kernel
     } else if (dt == WF_BF16) {
         f.n_tiles = cdiv(vocab, kLmTile);
         const uint16_t *hb = static_cast<const uint16_t *>(h);

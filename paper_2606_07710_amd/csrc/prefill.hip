@@ -39,6 +39,9 @@ struct PrefillParams {
     double theta[kMaxHalfDim];  // RoPE frequencies base^(-2i/D), i < D/2
     unsigned long long *slots; // bf16 path: k-slice exchange slots, zero between calls
     int chunks_per_split;      // 32-wide chunks of d_in per k-slice
+    int token_blocks;          // blockIdx.z = layer * token_blocks + token block
+    long long x_ls, w_ls, c_ls; // element strides between layers (x, W_k|W_v, caches)
+    int w_tiled;               // W_k, W_v in 16x32 tiles of 1 KB (bf16 path)
 };
 
 // Rotation of the pair (lo, hi) = (k_i, k_{i+D/2}) by pos * theta_i, with
@@ -71,7 +74,8 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
 
     const int unit = blockIdx.x;         // (g, kind, pair)
     const int ks = blockIdx.y;
-    const int tb = blockIdx.z;
+    const int tb = blockIdx.z % a.token_blocks;
+    const int layer = blockIdx.z / a.token_blocks;
     const int pair = unit % PAIRS;
     const int kind = (unit / PAIRS) % 2; // 0 = K, 1 = V
     const int g = unit / (2 * PAIRS);
@@ -82,15 +86,28 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
     const int m16 = lane & 15;
     const int c4 = lane >> 4;
 
-    const uint16_t *w = static_cast<const uint16_t *>(kind ? a.w_v : a.w_k);
-    const uint16_t *x = static_cast<const uint16_t *>(a.x);
+    const uint16_t *w = static_cast<const uint16_t *>(kind ? a.w_v : a.w_k) + layer * a.w_ls;
+    const uint16_t *x = static_cast<const uint16_t *>(a.x) + layer * a.x_ls;
     const int f_lo = g * DH + 16 * pair;           // first feature, low half
     const int c_begin = ks * a.chunks_per_split;   // 32-wide chunks of d_in
     // chunks of this slice (the last slices of a power-of-two split may be
     // short or empty)
     const int n_c = max(0, min(a.chunks_per_split, a.d_in / 32 - c_begin));
-    const uint16_t *wp0 = w + (size_t)(f_lo + m16) * a.d_in + c4 * 8;
-    const uint16_t *wp1 = w + (size_t)(f_lo + DH / 2 + m16) * a.d_in + c4 * 8;
+    // W operand of chunk c: row-major, lane (m16, c4) reads 16 bytes of row
+    // m16 (64 contiguous bytes per row and load); tiled, the wave reads the
+    // chunk's 1 KB tile contiguously
+    const uint16_t *wp0, *wp1;
+    int wstep;
+    if (a.w_tiled) {
+        const size_t kch = (size_t)(a.d_in / 32);
+        wp0 = w + (size_t)(f_lo / 16) * kch * 512 + lane * 8;
+        wp1 = w + (size_t)((f_lo + DH / 2) / 16) * kch * 512 + lane * 8;
+        wstep = 512;
+    } else {
+        wp0 = w + (size_t)(f_lo + m16) * a.d_in + c4 * 8;
+        wp1 = w + (size_t)(f_lo + DH / 2 + m16) * a.d_in + c4 * 8;
+        wstep = 32;
+    }
     // Tokens past n_tok read the last token instead: they only feed MFMA
     // output columns that are never stored.
     const uint16_t *xp[NBT];
@@ -113,8 +130,9 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
             const int c = cb + WAVES * u;
             if (c < n_c) {
                 const int off = (c_begin + c) * 32;
-                wr[u][0] = load_bf16x8(wp0 + off);
-                wr[u][1] = load_bf16x8(wp1 + off);
+                const size_t woff = (size_t)(c_begin + c) * wstep;
+                wr[u][0] = load_bf16x8(wp0 + woff);
+                wr[u][1] = load_bf16x8(wp1 + woff);
 #pragma unroll
                 for (int nb = 0; nb < NBT; ++nb)
                     xr[u][nb] = load_bf16x8(xp[nb] + off);
@@ -151,9 +169,10 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
     // bf16 cache write.  Slot 0 means empty; a parked pair is stored as
     // (bits(hi) << 32) | (bits(lo) + 1), never 0 for arithmetic results.
     const int ksplit = gridDim.y;
-    const size_t ub = (size_t)unit * gridDim.z + tb;           // (unit, token block)
+    const size_t ub =                                          // (layer, unit, token block)
+        ((size_t)layer * gridDim.x + unit) * a.token_blocks + tb;
     unsigned long long *slots = a.slots + ub * (size_t)(ksplit - 1) * (16 * TOK);
-    uint16_t *cache = static_cast<uint16_t *>(kind ? a.v_cache : a.k_cache);
+    uint16_t *cache = static_cast<uint16_t *>(kind ? a.v_cache : a.k_cache) + layer * a.c_ls;
     for (int idx = threadIdx.x; idx < 16 * TOK; idx += blockDim.x) {
         const int e = idx / TOK;
         const int tl = idx % TOK;
@@ -225,17 +244,20 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
-PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim) {
+PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers) {
     PrefillPlan p{};
     p.nbt = std::min(4, std::max(1, cdiv(n_tok, 16)));
     p.token_blocks = std::max(1, cdiv(n_tok, 16 * p.nbt));
     p.units = n_kv_heads * 2 * (head_dim / 32);
     const int chunks = d_in / 32;
     // a power-of-two number of k-slices: enough to cover the chip, at least
-    // 4 chunks per slice.  units * token_blocks * (ksplit - 1) < 512, so the
-    // exchange slots stay under 512 * 1024 pairs = the 4 MiB zero block.
+    // 4 chunks per slice.  layers * units * token_blocks * (ksplit - 1) <
+    // 512, so the exchange slots stay under 512 * 1024 pairs = the 4 MiB
+    // zero block.  Several layers in one launch need fewer slices (none from
+    // 256 (layer, unit, token block) triples up).
+    const long long base = (long long)p.units * p.token_blocks * n_layers;
     int ks = 1;
-    while (ks * 2 * p.units * p.token_blocks <= kPfTargetWorkgroups && chunks / (ks * 2) >= 4)
+    while (ks * 2 * base <= kPfTargetWorkgroups && chunks / (ks * 2) >= 4)
         ks *= 2;
     p.chunks_per_split = cdiv(chunks, ks);
     p.ksplit = ks;
@@ -244,13 +266,15 @@ PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim) {
 
 // Exchange slots: (ksplit - 1) internal tree nodes x 16*16*nbt pairs per
 // (unit, token block), inside the workspace's zero block.
-static size_t prefill_slot_bytes(const PrefillPlan &p) {
-    return (size_t)p.units * p.token_blocks * (p.ksplit - 1) * (16 * 16 * p.nbt) *
+static size_t prefill_slot_bytes(const PrefillPlan &p, int n_layers) {
+    return (size_t)n_layers * p.units * p.token_blocks * (p.ksplit - 1) * (16 * 16 * p.nbt) *
            sizeof(unsigned long long);
 }
 
-bool prefill_fits(int n_tok, int d_in, int n_kv_heads, int head_dim) {
-    return prefill_slot_bytes(plan_prefill(n_tok, d_in, n_kv_heads, head_dim)) <= kCounterBytes;
+bool prefill_fits(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers) {
+    const PrefillPlan p = plan_prefill(n_tok, d_in, n_kv_heads, head_dim, n_layers);
+    return prefill_slot_bytes(p, n_layers) <= kCounterBytes &&
+           (long long)p.token_blocks * n_layers <= 65535;
 }
 
 size_t prefill_workspace_bytes(wf_dtype_t dt, int n_tok, int d_in, int n_kv_heads,
@@ -264,16 +288,21 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            const void *w_v, void *k_cache, void *v_cache,
                            int n_tok, int start_pos, int cap, int d_in,
                            int n_kv_heads, int head_dim, double rope_base,
-                           void *workspace, hipStream_t stream) {
+                           void *workspace, hipStream_t stream, int n_layers,
+                           long long x_ls, long long w_ls, long long c_ls) {
+    const bool tiled = dt == WF_BF16_TILED;
+    if (tiled)
+        dt = WF_BF16;
     PrefillParams a{x, w_k, w_v, k_cache, v_cache, n_tok, start_pos, cap, d_in,
-                    n_kv_heads, {}, nullptr, 0};
+                    n_kv_heads, {}, nullptr, 0, 1, x_ls, w_ls, c_ls, tiled ? 1 : 0};
     for (int i = 0; i < head_dim / 2; ++i)
         a.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
     if (dt == WF_BF16) {
-        const PrefillPlan p = plan_prefill(n_tok, d_in, n_kv_heads, head_dim);
+        const PrefillPlan p = plan_prefill(n_tok, d_in, n_kv_heads, head_dim, n_layers);
         a.chunks_per_split = p.chunks_per_split;
+        a.token_blocks = p.token_blocks;
         a.slots = static_cast<unsigned long long *>(workspace);
-        dim3 grid(p.units, p.ksplit, p.token_blocks), block(256);
+        dim3 grid(p.units, p.ksplit, p.token_blocks * n_layers), block(256);
 #define WF_PF_CASE(DHV, NBV)                                                        \
     if (head_dim == DHV && p.nbt == NBV) {                                          \
         prefill_bf16<DHV, NBV><<<grid, block, 0, stream>>>(a);                      \
@@ -285,7 +314,15 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
     } else {
         const long long total = (long long)n_tok * n_kv_heads * head_dim;
         const unsigned blocks = (unsigned)((total + 255) / 256);
-        prefill_f32<<<blocks, 256, 0, stream>>>(a, head_dim);
+        for (int l = 0; l < n_layers; ++l) {
+            PrefillParams al = a;
+            al.x = static_cast<const float *>(x) + l * x_ls;
+            al.w_k = static_cast<const float *>(w_k) + l * w_ls;
+            al.w_v = static_cast<const float *>(w_v) + l * w_ls;
+            al.k_cache = static_cast<float *>(k_cache) + l * c_ls;
+            al.v_cache = static_cast<float *>(v_cache) + l * c_ls;
+            prefill_f32<<<blocks, 256, 0, stream>>>(al, head_dim);
+        }
     }
     if (hipGetLastError() != hipSuccess)
         return WF_ERR_HIP;

@@ -96,15 +96,24 @@ struct PrefillPlan {
     int chunks_per_split;
 };
 
-PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim);
+PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers = 1);
 size_t prefill_workspace_bytes(wf_dtype_t dt, int n_tok, int d_in, int n_kv_heads,
                                int head_dim);
-// Whether the bf16 plan's exchange slots fit the workspace zero block.
-bool prefill_fits(int n_tok, int d_in, int n_kv_heads, int head_dim);
+// Whether the bf16 plan's exchange slots fit the workspace zero block (and
+// its grid the launch limits).
+bool prefill_fits(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers = 1);
+// n_layers independent prefills in one launch: layer l reads x + l*x_ls,
+// w_k/w_v + l*w_ls and writes the caches at + l*c_ls (element strides).
 wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            const void *w_v, void *k_cache, void *v_cache,
                            int n_tok, int start_pos, int cap, int d_in,
                            int n_kv_heads, int head_dim, double rope_base,
-                           void *workspace, hipStream_t stream);
+                           void *workspace, hipStream_t stream, int n_layers = 1,
+                           long long x_ls = 0, long long w_ls = 0, long long c_ls = 0);
+
+// Tiled bf16 weights (16x32 tiles of 1 KB, one wave operand load each).
+size_t tiled_weight_bytes(int rows, int cols);
+wf_status_t launch_tile_weights(const void *w, int rows, int cols, void *tiled,
+                                hipStream_t stream);
 
 }  // namespace wf

@@ -118,6 +118,37 @@ def test_prefill_zero_tokens_is_a_noop():
     assert _prefill(n=0) == 0
 
 
+def _prefill_layers(**kw):
+    a = dict(dt=1, x=FAKE, wk=FAKE, wv=FAKE, kc=FAKE, vc=FAKE, n=16, start=10,
+             cap=26, d_in=4096, hkv=8, dh=128, base=1e6, layers=36,
+             xs=16 * 4096, ws_=8 * 128 * 4096, cs=8 * 26 * 128, ws=FAKE,
+             ws_bytes=1 << 30)
+    a.update(kw)
+    return wf.lib.wf_kv_only_prefill_layers(
+        a["dt"], a["x"], a["wk"], a["wv"], a["kc"], a["vc"], a["n"], a["start"],
+        a["cap"], a["d_in"], a["hkv"], a["dh"], a["base"], a["layers"], a["xs"],
+        a["ws_"], a["cs"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(layers=0), 1), (dict(layers=1025), 1), (dict(xs=16 * 4096 - 8), 1),
+    (dict(ws_=8 * 128 * 4096 - 8), 1), (dict(cs=8 * 26 * 128 - 8), 1),
+    (dict(xs=16 * 4096 + 4), 1), (dict(cs=8 * 26 * 128 + 1), 1),
+    (dict(x=None), 1), (dict(cap=25), 1), (dict(dh=80), 2), (dict(d_in=100), 2),
+    (dict(ws=None), 3), (dict(ws_bytes=64), 3), (dict(kc=ODD), 1),
+    (dict(dt=0, xs=16 * 4096 + 2), 1),
+])
+def test_prefill_layers_rejects(kw, status):
+    assert _prefill_layers(**kw) == status
+
+
+def test_prefill_layers_workspace_query_and_noop():
+    assert wf.wf_kv_only_prefill_layers_workspace_bytes(1, 16, 4096, 8, 128, 36) == COUNTER_BLOCK
+    assert wf.wf_kv_only_prefill_layers_workspace_bytes(1, 16, 4096, 8, 128, 0) == 0
+    assert wf.wf_kv_only_prefill_layers_workspace_bytes(0, 16, 4096, 8, 128, 36) == 0
+    assert _prefill_layers(n=0) == 0
+
+
 def _lm(**kw):
     a = dict(dt=1, h=FAKE, w=FAKE, logits=None, draft=FAKE, gamma=16,
              d=4096, vocab=151936, tau=1.0, am=FAKE, ent=FAKE, acc=FAKE,
@@ -222,9 +253,10 @@ def test_router_rejects(kw, status):
 
 
 def test_router_workspace_query():
-    # z in 8 slices of d, then 32 unit-group sums, per row
+    # z in 16 slices of d (32 unit tiles x 16 slices = 512 workgroups), then
+    # 32 unit-group sums, per row
     need = wf.lib.wf_router_workspace_bytes(1, 16, 4096, 512)
-    assert need == COUNTER_BLOCK + (8 * 512 + 32) * 16 * 4
+    assert need == COUNTER_BLOCK + (16 * 512 + 32) * 16 * 4
     assert wf.lib.wf_router_workspace_bytes(1, 16, 4096, 40) == 0
     assert wf.lib.wf_router_workspace_bytes(0, 3, 100, 40) == COUNTER_BLOCK + (40 + 3) * 3 * 4
 
@@ -269,3 +301,33 @@ def test_drafter_token_limits():
     assert wf.lib.wf_drafter_forward_workspace_bytes(1, ctypes.byref(lay), 1, 4096) > COUNTER_BLOCK
     assert wf.lib.wf_drafter_catchup_workspace_bytes(1, ctypes.byref(lay), 80, 4096) > COUNTER_BLOCK
     assert wf.lib.wf_drafter_forward_workspace_bytes(0, ctypes.byref(lay), 1, 4096) == 0
+
+
+def test_tiled_weight_bytes_and_rejects():
+    assert wf.wf_tiled_weight_bytes(16, 32) == 16 * 32 * 2
+    assert wf.wf_tiled_weight_bytes(37, 96) == 48 * 96 * 2          # rows padded to 16
+    assert wf.wf_tiled_weight_bytes(151936, 4096) == 151936 * 4096 * 2
+    for rows, cols in ((0, 32), (16, 16), (16, 100), (-1, 64)):
+        assert wf.wf_tiled_weight_bytes(rows, cols) == 0
+    t = wf.lib.wf_tile_weights
+    assert t(None, 16, 32, FAKE, 1 << 20, None) == 1
+    assert t(FAKE, 16, 32, None, 1 << 20, None) == 1
+    assert t(ODD, 16, 32, FAKE, 1 << 20, None) == 1
+    assert t(FAKE, 16, 100, 1 << 30, 1 << 20, None) == 1
+    assert t(FAKE, 16, 32, 1 << 30, 64, None) == 3               # too small
+    assert t(FAKE, 16, 32, (1 << 20) + 512, 1 << 20, None) == 1   # overlapping
+
+
+def test_tiled_dtype_only_where_weights_are_streamed():
+    # calls without weights reject it
+    assert _attn(dt=2) == 1
+    assert _compact(dt=2) == 1
+    # LM head: the persistent kernels only
+    assert _lm(dt=2, d=96, gamma=16) == 2
+    assert _lm(dt=2, d=1056, gamma=16) == 2
+    # prefill: accepted (validated like bf16), workspace as bf16
+    assert _prefill(dt=2, d_in=100) == 2
+    assert _prefill(dt=2, n=0) == 0
+    assert wf.wf_kv_only_prefill_workspace_bytes(2, 16, 4096, 8, 128) == COUNTER_BLOCK
+    assert wf.wf_kv_only_prefill_layers_workspace_bytes(2, 16, 4096, 8, 128, 36) == COUNTER_BLOCK
+    assert _prefill_layers(dt=2, xs=16 * 4096 + 4) == 1

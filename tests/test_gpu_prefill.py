@@ -82,3 +82,61 @@ def test_zero_tokens_is_a_noop():
     wf.wf_kv_only_prefill(x[:0], wk, wv, kc, vc, 10, 1e6)
     torch.cuda.synchronize()
     assert torch.equal(kc, k0)
+
+
+LAYER_CASES = [
+    # n_layers, n_tok, d_in, n_kv_heads, head_dim, start_pos, checked layers
+    (3, 16, 1024, 2, 128, 100, (0, 1, 2)),
+    (5, 70, 512, 2, 64, 7, (0, 4)),
+    (36, 16, 4096, 8, 128, 32784, (0, 17, 35)),
+]
+
+
+@pytest.mark.parametrize("L,n,d_in,hkv,dh,start,check", LAYER_CASES)
+def test_layers_match_oracle_and_single_layer_calls(L, n, d_in, hkv, dh, start, check):
+    """All layers' catch-up in one launch: each layer's rows within the bar
+    of the oracle (the layers listed) and of a single-layer call (all), the
+    other rows untouched."""
+    print(f"prefill layers L={L} n={n} d_in={d_in} hkv={hkv} dh={dh} start={start}",
+          flush=True)
+    cap = start + n + 2
+    bf = torch.bfloat16
+    x = W.normal((L, n, d_in), 1.0, W.stream_seed(L, "x"), bf, DEV)
+    wk = W.normal((L, hkv * dh, d_in), 0.02, W.stream_seed(L, "w_k"), bf, DEV)
+    wv = W.normal((L, hkv * dh, d_in), 0.02, W.stream_seed(L, "w_v"), bf, DEV)
+    kc = W.normal((L, hkv, cap, dh), 1.0, W.stream_seed(L, "k_cache"), bf, DEV)
+    vc = W.normal((L, hkv, cap, dh), 1.0, W.stream_seed(L, "v_cache"), bf, DEV)
+    k0, v0 = kc.clone(), vc.clone()
+    k1, v1 = kc.clone(), vc.clone()
+    wf.wf_kv_only_prefill_layers(x, wk, wv, kc, vc, start, 1e6)
+    for l in range(L):
+        wf.wf_kv_only_prefill(x[l], wk[l], wv[l], k1[l], v1[l], start, 1e6)
+    torch.cuda.synchronize()
+    rows = slice(start, start + n)
+    for l in range(L):
+        assert max_vec_rel_err(host64(kc[l][:, rows]), host64(k1[l][:, rows])) <= TOL["bf16"]
+        assert max_vec_rel_err(host64(vc[l][:, rows]), host64(v1[l][:, rows])) <= TOL["bf16"]
+    for l in check:
+        kr, vr = oracle.kv_only_prefill(W.to_oracle(x[l]), W.to_oracle(wk[l]),
+                                        W.to_oracle(wv[l]), start, hkv, dh, 1e6)
+        assert max_vec_rel_err(host64(kc[l][:, rows]), kr) <= TOL["bf16"]
+        assert max_vec_rel_err(host64(vc[l][:, rows]), vr) <= TOL["bf16"]
+    for a, b in ((kc, k0), (vc, v0)):
+        assert torch.equal(a[:, :, :start], b[:, :, :start])
+        assert torch.equal(a[:, :, start + n:], b[:, :, start + n:])
+
+
+def test_layers_f32_equals_single_layer_calls():
+    L, n, d_in, hkv, dh, start = 3, 5, 100, 3, 64, 20
+    f = torch.float32
+    x = W.normal((L, n, d_in), 0.02, 1, f, DEV)
+    wk = W.normal((L, hkv * dh, d_in), 0.02, 2, f, DEV)
+    wv = W.normal((L, hkv * dh, d_in), 0.02, 3, f, DEV)
+    kc = W.normal((L, hkv, start + n, dh), 1.0, 4, f, DEV)
+    vc = W.normal((L, hkv, start + n, dh), 1.0, 5, f, DEV)
+    k1, v1 = kc.clone(), vc.clone()
+    wf.wf_kv_only_prefill_layers(x, wk, wv, kc, vc, start, 1e4)
+    for l in range(L):
+        wf.wf_kv_only_prefill(x[l], wk[l], wv[l], k1[l], v1[l], start, 1e4)
+    torch.cuda.synchronize()
+    assert torch.equal(kc, k1) and torch.equal(vc, v1)
