@@ -351,8 +351,11 @@ def bench_switch(args, w):
     big = dataclasses.replace(w, n_prefill=max(w.n_prefill, *backlogs) if backlogs
                               else w.n_prefill)
     t = W.generate_drafter(big, device=dev, cache_rows=max_rows - big.n_prefill)
-    layer = wf.decoder_layer({n: t[n] for n in W.DECODER_WEIGHTS}, w.n_q_heads,
-                             w.n_kv_heads, w.rms_eps, w.rope_base)
+    tiled = not args.row_major_weights
+    # static weights: the projections tiled once at setup, as at model load
+    lw = {n: (t[n] if n.endswith("norm") or not tiled else wf.tile_weights(t[n]))
+          for n in W.DECODER_WEIGHTS}
+    layer = wf.decoder_layer(lw, w.n_q_heads, w.n_kv_heads, w.rms_eps, w.rope_base)
     kc, vc, r_all = t["k_cache"], t["v_cache"], t["r"]
     torch.cuda.synchronize()
     log(f"inputs generated in {time.perf_counter() - t0:.1f}s "
@@ -416,7 +419,7 @@ def bench_switch(args, w):
             def naive(per_round=per_round, rounds=rounds, nb=nb):
                 for k in range(rounds - 1):
                     wf.wf_kv_only_prefill(r_all[k * per_round:(k + 1) * per_round],
-                                          t["w_k"], t["w_v"], kc, vc,
+                                          lw["w_k"], lw["w_v"], kc, vc,
                                           pos + k * per_round, w.rope_base,
                                           workspace=pws)
                 wf.wf_drafter_catchup(layer, r_all[nb - per_round:nb],
@@ -462,7 +465,9 @@ def bench_switch(args, w):
                 "shapes and a 12288-wide SwiGLU MLP, random weights)",
         "config": {"workload": w.name, "hidden": w.hidden, "q_heads": w.n_q_heads,
                    "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
-                   "inter": w.inter, "base_kv": pos, "backlog": n},
+                   "inter": w.inter, "base_kv": pos, "backlog": n,
+                   "weights": "tiled (16x32 tiles, made once at setup)" if tiled
+                              else "row-major"},
         "roofline": {
             "kernel": "wf_drafter_catchup, whole call (rmsnorm, KV-only "
                       "prefill, then the full layer for the last token)",

@@ -88,13 +88,15 @@ typedef enum {
     WF_F32 = 0,               /* IEEE fp32 storage and arithmetic             */
     WF_BF16 = 1,              /* bf16 storage, fp32 accumulation              */
     WF_BF16_TILED = 2         /* as WF_BF16, with the WEIGHT matrices (W_k,
-                                 W_v, W_lm) in the tiled layout that
-                                 wf_tile_weights writes; activations, caches
-                                 and outputs stay row-major.  Accepted by the
-                                 KV-only prefill calls and the LM-head calls
-                                 (where their bf16 kernels for gamma <= 16 and
-                                 d in {4096, 5120}, or d % 512 == 0, apply;
-                                 else WF_ERR_UNSUPPORTED) and nowhere else
+                                 W_v, W_lm, the drafter layer's projections)
+                                 in the tiled layout that wf_tile_weights
+                                 writes; activations, norm gains, caches and
+                                 outputs stay row-major.  Accepted by the
+                                 KV-only prefill, drafter and LM-head calls
+                                 (the LM head where its bf16 kernels for
+                                 gamma <= 16 and d in {4096, 5120}, or
+                                 d % 512 == 0, apply; else
+                                 WF_ERR_UNSUPPORTED) and nowhere else
                                  (WF_ERR_INVALID_ARG).  Results are bit-for-bit
                                  those of WF_BF16 on the untiled weights.     */
 } wf_dtype_t;
@@ -417,7 +419,8 @@ typedef struct wf_decoder_layer {
  * among them).  r [n_tok][hidden] is the layer input (pre-norm residual
  * stream); the tokens' K/V are written to cache rows pos .. pos+n_tok-1 and
  * attention reads rows [0, pos + t]; out [n_tok][hidden].
- * Limits: dt == WF_BF16 (else WF_ERR_UNSUPPORTED); 1 <= n_tok <= 64;
+ * Limits: dt == WF_BF16 or WF_BF16_TILED (the seven projections tiled;
+ *         else WF_ERR_UNSUPPORTED); 1 <= n_tok <= 64;
  *         pos >= 0; pos + n_tok <= cap; head_dim in {64, 128};
  *         n_q_heads % n_kv_heads == 0; hidden, inter and
  *         n_q_heads*head_dim multiples of 32; weights, r, out and the

@@ -449,9 +449,17 @@ def decoder_layer(weights, n_q_heads, n_kv_heads, rms_eps, rope_base):
     head_dim = w_q.shape[0] // n_q_heads
     if w_k.shape[0] != n_kv_heads * head_dim:
         raise ValueError("w_k rows must be n_kv_heads * head_dim")
-    return DecoderLayer(*[_dev(weights[n], n).value for n in DECODER_WEIGHTS],
-                        w_q.shape[1], n_q_heads, n_kv_heads, head_dim,
-                        w_gate.shape[0], float(rms_eps), float(rope_base))
+    layer = DecoderLayer(*[_dev(weights[n], n).value for n in DECODER_WEIGHTS],
+                         w_q.shape[1], n_q_heads, n_kv_heads, head_dim,
+                         w_gate.shape[0], float(rms_eps), float(rope_base))
+    # the struct holds raw device pointers: keep the tensors alive with it
+    layer.keepalive = dict(weights)
+    # projections tiled (wf_tile_weights) -> the calls pass WF_BF16_TILED
+    mats = [weights[n] for n in DECODER_WEIGHTS if not n.endswith("norm")]
+    layer.tiled = all(isinstance(m, TiledWeight) for m in mats)
+    if not layer.tiled and any(isinstance(m, TiledWeight) for m in mats):
+        raise TypeError("tile all seven projections or none")
+    return layer
 
 
 def wf_drafter_forward_workspace_bytes(layer, n_tok, pos) -> int:
@@ -470,7 +478,7 @@ def wf_drafter_forward(layer, r, pos, k_cache, v_cache, out, workspace=None,
                        stream=None):
     """layer: DecoderLayer; r, out [n_tok][hidden]; caches [Hkv][cap][D]."""
     n_tok = r.shape[0]
-    code = _dtype_code(r)
+    code = WF_BF16_TILED if getattr(layer, "tiled", False) else _dtype_code(r)
     need = int(lib.wf_drafter_forward_workspace_bytes(code, ctypes.byref(layer), n_tok,
                                                       int(pos)))
     if workspace is None:
@@ -488,7 +496,7 @@ def wf_drafter_catchup(layer, r, pos, k_cache, v_cache, out, workspace=None,
                        stream=None):
     """layer: DecoderLayer; r [n_backlog][hidden]; out [hidden]."""
     n = r.shape[0]
-    code = _dtype_code(r)
+    code = WF_BF16_TILED if getattr(layer, "tiled", False) else _dtype_code(r)
     need = int(lib.wf_drafter_catchup_workspace_bytes(code, ctypes.byref(layer), n,
                                                       int(pos)))
     if workspace is None:

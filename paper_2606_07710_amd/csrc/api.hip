@@ -395,7 +395,7 @@ namespace {
 // is checked by the caller).
 wf_status_t check_drafter(wf_dtype_t dt, const wf_decoder_layer_t *L, int pos, int last_row,
                           int cap) {
-    if (!dtype_ok(dt) || !L)
+    if (!weight_dtype_ok(dt) || !L)
         return WF_ERR_INVALID_ARG;
     if (L->hidden < 1 || L->inter < 1 || L->n_kv_heads < 1 || L->n_q_heads < 1 ||
         L->n_q_heads > kMaxQHeads || L->n_q_heads % L->n_kv_heads != 0)
@@ -410,7 +410,7 @@ wf_status_t check_drafter(wf_dtype_t dt, const wf_decoder_layer_t *L, int pos, i
     for (const void *p : ws)
         if (!p || !aligned16(p))
             return WF_ERR_INVALID_ARG;
-    if (dt != WF_BF16 || !head_dim_ok(L->head_dim))
+    if (!is_bf16(dt) || !head_dim_ok(L->head_dim))
         return WF_ERR_UNSUPPORTED;
     if (L->hidden % 32 != 0 || L->inter % 32 != 0 || (L->n_q_heads * L->head_dim) % 32 != 0)
         return WF_ERR_UNSUPPORTED;
@@ -445,7 +445,8 @@ wf_status_t wf_drafter_forward(wf_dtype_t dt, const wf_decoder_layer_t *layer, c
     if (!workspace || workspace_bytes < need || !aligned16(workspace))
         return WF_ERR_WORKSPACE;
     return wf::launch_drafter_forward(*layer, r, n_tok, pos, k_cache, v_cache, cap, out,
-                                      workspace, static_cast<hipStream_t>(stream));
+                                      workspace, static_cast<hipStream_t>(stream),
+                                      dt == WF_BF16_TILED);
 }
 
 size_t wf_drafter_catchup_workspace_bytes(wf_dtype_t dt, const wf_decoder_layer_t *layer,
@@ -478,7 +479,8 @@ wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer, c
     if (!workspace || workspace_bytes < need || !aligned16(workspace))
         return WF_ERR_WORKSPACE;
     return wf::launch_drafter_catchup(*layer, r, n_backlog, pos, k_cache, v_cache, cap, out,
-                                      workspace, static_cast<hipStream_t>(stream));
+                                      workspace, static_cast<hipStream_t>(stream),
+                                      dt == WF_BF16_TILED);
 }
 
 wf_status_t wf_kv_compact_path(wf_dtype_t dt, void *k_cache, void *v_cache,

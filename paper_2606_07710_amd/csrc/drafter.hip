@@ -223,7 +223,8 @@ size_t drafter_catchup_workspace_bytes(const wf_decoder_layer_t &L, int n, int p
 
 wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, int M, int pos,
                                    void *k_cache, void *v_cache, int cap, void *out,
-                                   void *workspace, hipStream_t stream) {
+                                   void *workspace, hipStream_t stream, bool tiled) {
+    const wf_dtype_t wdt = tiled ? WF_BF16_TILED : WF_BF16;
     const DrafterLayout o = drafter_layout(L, M, pos);
     char *ws = static_cast<char *>(workspace);
     const auto *rb = static_cast<const uint16_t *>(r);
@@ -239,12 +240,12 @@ wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, i
     wf_status_t st;
 
     rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(rb, W(L.attn_norm), L.rms_eps, xn, d);
-    st = launch_prefill(WF_BF16, xn, L.w_k, L.w_v, k_cache, v_cache, M, pos, cap, d,
+    st = launch_prefill(wdt, xn, L.w_k, L.w_v, k_cache, v_cache, M, pos, cap, d,
                         L.n_kv_heads, L.head_dim, L.rope_base, workspace, stream);
     if (st != WF_OK)
         return st;
     // q = RoPE(Wq xn)
-    if ((st = launch_linear_partial(xn, W(L.w_q), nullptr, qd, 0, M, d, zp, stream)) != WF_OK)
+    if ((st = launch_linear_partial(xn, W(L.w_q), nullptr, qd, 0, M, d, zp, stream, tiled)) != WF_OK)
         return st;
     RopeParams rp{};
     for (int i = 0; i < L.head_dim / 2; ++i)
@@ -258,18 +259,19 @@ wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, i
     if (st != WF_OK)
         return st;
     // h1 = r + Wo a
-    if ((st = launch_linear_partial(a, W(L.w_o), nullptr, d, 0, M, qd, zp, stream)) != WF_OK)
+    if ((st = launch_linear_partial(a, W(L.w_o), nullptr, d, 0, M, qd, zp, stream, tiled)) != WF_OK)
         return st;
     reduce_store_bf16<<<blocks_for((long long)M * d), 256, 0, stream>>>(
         zp, linear_slices(qd, d), d, M, rb, h1);
     // act = SiLU(Wg xn2) * (Wu xn2)
     rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(h1, W(L.mlp_norm), L.rms_eps, xn2, d);
-    if ((st = launch_linear_partial(xn2, W(L.w_gate), W(L.w_up), I, I, M, d, zp, stream)) != WF_OK)
+    if ((st = launch_linear_partial(xn2, W(L.w_gate), W(L.w_up), I, I, M, d, zp, stream,
+                                    tiled)) != WF_OK)
         return st;
     reduce_swiglu_bf16<<<blocks_for((long long)M * I), 256, 0, stream>>>(
         zp, linear_slices(d, 2 * I), I, M, act);
     // out = h1 + Wd act
-    if ((st = launch_linear_partial(act, W(L.w_down), nullptr, d, 0, M, I, zp, stream)) != WF_OK)
+    if ((st = launch_linear_partial(act, W(L.w_down), nullptr, d, 0, M, I, zp, stream, tiled)) != WF_OK)
         return st;
     reduce_store_bf16<<<blocks_for((long long)M * d), 256, 0, stream>>>(
         zp, linear_slices(I, d), d, M, h1, static_cast<uint16_t *>(out));
@@ -278,7 +280,7 @@ wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, i
 
 wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, int n, int pos,
                                    void *k_cache, void *v_cache, int cap, void *out,
-                                   void *workspace, hipStream_t stream) {
+                                   void *workspace, hipStream_t stream, bool tiled) {
     const int d = L.hidden;
     const auto *rb = static_cast<const uint16_t *>(r);
     if (n > 1) {
@@ -286,14 +288,15 @@ wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, i
             static_cast<char *>(workspace) + align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)));
         rmsnorm_bf16<<<n - 1, kNormThreads, 0, stream>>>(rb, static_cast<const uint16_t *>(L.attn_norm),
                                                          L.rms_eps, xnb, d);
-        const wf_status_t st = launch_prefill(WF_BF16, xnb, L.w_k, L.w_v, k_cache, v_cache, n - 1,
+        const wf_status_t st = launch_prefill(tiled ? WF_BF16_TILED : WF_BF16, xnb, L.w_k, L.w_v,
+                                              k_cache, v_cache, n - 1,
                                               pos, cap, d, L.n_kv_heads, L.head_dim, L.rope_base,
                                               workspace, stream);
         if (st != WF_OK)
             return st;
     }
     return launch_drafter_forward(L, rb + (size_t)(n - 1) * d, 1, pos + n - 1, k_cache, v_cache,
-                                  cap, out, workspace, stream);
+                                  cap, out, workspace, stream, tiled);
 }
 
 }  // namespace wf

@@ -9,7 +9,8 @@
 // one fp32 partial per slice, zpart[k][feature][row]; the caller's epilogue
 // kernel adds the slices in order.  Two weight matrices may share a launch
 // (features [0, n_a) from w_a, [n_a, n_a + n_b) from w_b), as the gate and
-// up projections of a SwiGLU MLP do.
+// up projections of a SwiGLU MLP do.  Weights row-major or in 16x32 tiles
+// of 1 KB (one contiguous wave load per chunk).
 #include "wf_api_internal.h"
 #include "wf_device.h"
 
@@ -26,7 +27,7 @@ template <int NBL>
 __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     const uint16_t *__restrict__ x, const uint16_t *__restrict__ w_a,
     const uint16_t *__restrict__ w_b, int n_a, float *__restrict__ zpart, int rows,
-    int k_in, int n_out, int chunks_per_slice) {
+    int k_in, int n_out, int chunks_per_slice, int tiled) {
     __shared__ float zs[kGemvWaves][16][16 * NBL + 1];
     const int f0 = 16 * blockIdx.x;
     const int ks = blockIdx.y;
@@ -37,9 +38,21 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     const int c_begin = ks * chunks_per_slice;
     const int n_c = max(0, min(chunks_per_slice, k_in / 32 - c_begin));
 
-    const int f = f0 + m16;
-    const uint16_t *wrow = f < n_a ? w_a + (size_t)f * k_in : w_b + (size_t)(f - n_a) * k_in;
-    const uint16_t *wp = wrow + (size_t)c_begin * 32 + c4 * 8;
+    // W operand of chunk c: row-major, 16 bytes of row f0 + m16 per lane;
+    // tiled, the 1 KB tile of the 16-feature block (n_a % 16 == 0, so a
+    // block never straddles the two matrices)
+    const uint16_t *wp;
+    int wstep;
+    if (tiled) {
+        const int blk = f0 < n_a ? f0 / 16 : (f0 - n_a) / 16;
+        wp = (f0 < n_a ? w_a : w_b) + ((size_t)blk * (k_in / 32) + c_begin) * 512 + lane * 8;
+        wstep = 512;
+    } else {
+        const int f = f0 + m16;
+        const uint16_t *wrow = f < n_a ? w_a + (size_t)f * k_in : w_b + (size_t)(f - n_a) * k_in;
+        wp = wrow + (size_t)c_begin * 32 + c4 * 8;
+        wstep = 32;
+    }
     // rows past `rows` read the last row: their columns are never used
     const uint16_t *xp[NBL];
 #pragma unroll
@@ -56,7 +69,7 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
         for (int u = 0; u < kGemvBatch; ++u) {
             const int c = cb + kGemvWaves * u;
             if (c < n_c) {
-                wr[u] = load_bf16x8(wp + c * 32);
+                wr[u] = load_bf16x8(wp + (size_t)c * wstep);
 #pragma unroll
                 for (int nb = 0; nb < NBL; ++nb)
                     xr[u][nb] = load_bf16x8(xp[nb] + c * 32);
@@ -105,17 +118,18 @@ int linear_slices(int k_in, int n_out) {
 
 wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
                                   const uint16_t *w_b, int n_a, int n_b, int rows,
-                                  int k_in, float *zpart, hipStream_t stream) {
+                                  int k_in, float *zpart, hipStream_t stream, bool tiled) {
+    const int t = tiled ? 1 : 0;
     const int n_out = n_a + n_b;
     const int ks = linear_slices(k_in, n_out);
     const int cps = cdiv(k_in / 32, ks);
     const dim3 grid(n_out / 16, ks);
     const dim3 block(kGemvWaves * kWave);
     switch (cdiv(rows, 16)) {
-    case 1: linear_partial_bf16<1><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps); break;
-    case 2: linear_partial_bf16<2><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps); break;
-    case 3: linear_partial_bf16<3><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps); break;
-    default: linear_partial_bf16<4><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps); break;
+    case 1: linear_partial_bf16<1><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t); break;
+    case 2: linear_partial_bf16<2><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t); break;
+    case 3: linear_partial_bf16<3><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t); break;
+    default: linear_partial_bf16<4><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t); break;
     }
     return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
 }

@@ -59,7 +59,8 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
 int linear_slices(int k_in, int n_out);
 wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
                                   const uint16_t *w_b, int n_a, int n_b, int rows,
-                                  int k_in, float *zpart, hipStream_t stream);
+                                  int k_in, float *zpart, hipStream_t stream,
+                                  bool tiled = false);
 
 // Neural routing policy: delta = w2 . GELU(W1 h + b1) + b2 for every row,
 // route at the row *row names.
@@ -70,15 +71,16 @@ wf_status_t launch_router(wf_dtype_t dt, const void *h, const void *w1,
                           float *delta_out, int32_t *route_out, void *workspace,
                           hipStream_t stream);
 
-// Drafter layer and lazy catch-up (drafter.hip); bf16 only.
+// Drafter layer and lazy catch-up (drafter.hip); bf16 only, the weight
+// matrices row-major or (tiled) in 16x32 tiles.
 size_t drafter_forward_workspace_bytes(const wf_decoder_layer_t &L, int M, int pos);
 size_t drafter_catchup_workspace_bytes(const wf_decoder_layer_t &L, int n, int pos);
 wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, int M, int pos,
                                    void *k_cache, void *v_cache, int cap, void *out,
-                                   void *workspace, hipStream_t stream);
+                                   void *workspace, hipStream_t stream, bool tiled);
 wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, int n, int pos,
                                    void *k_cache, void *v_cache, int cap, void *out,
-                                   void *workspace, hipStream_t stream);
+                                   void *workspace, hipStream_t stream, bool tiled);
 
 // Path compaction after tree acceptance: block rows path[t] -> t, t <= n,
 // in n_layers caches layer_stride elements apart.

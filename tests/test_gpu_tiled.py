@@ -89,3 +89,35 @@ def test_lmhead_tiled_is_bit_exact(gamma, d, vocab):
     torch.cuda.synchronize()
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("M,backlog", [(16, 0), (1, 0), (0, 80)])
+def test_drafter_tiled_is_bit_exact(M, backlog):
+    """The drafter layer (forward of M tokens, or catch-up over a backlog)
+    with its seven projections tiled gives the row-major call's bits."""
+    import dataclasses
+    print(f"drafter tiled M={M} backlog={backlog}", flush=True)
+    n = M or backlog
+    w = dataclasses.replace(W.CONFIGS[7], cfg=77, ctx_len=1000, n_prefill=n,
+                            prefill_start=1000, prefill_cap=1000 + n)
+    t = W.generate_drafter(w, device=DEV)
+    names = W.DECODER_WEIGHTS
+    row = wf.decoder_layer({k: t[k] for k in names}, w.n_q_heads, w.n_kv_heads,
+                           w.rms_eps, w.rope_base)
+    tiled = wf.decoder_layer({k: (t[k] if k.endswith("norm") else wf.tile_weights(t[k]))
+                              for k in names}, w.n_q_heads, w.n_kv_heads, w.rms_eps,
+                             w.rope_base)
+    assert tiled.tiled and not row.tiled
+    res = []
+    for layer in (row, tiled):
+        kc, vc = t["k_cache"].clone(), t["v_cache"].clone()
+        if M:
+            out = torch.empty((M, w.hidden), dtype=BF, device=DEV)
+            wf.wf_drafter_forward(layer, t["r"], 1000, kc, vc, out)
+        else:
+            out = torch.empty(w.hidden, dtype=BF, device=DEV)
+            wf.wf_drafter_catchup(layer, t["r"], 1000, kc, vc, out)
+        res.append((out, kc, vc))
+    torch.cuda.synchronize()
+    for a, b in zip(*res):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
