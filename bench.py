@@ -4,10 +4,14 @@
 One step = the whole hot path over one synthetic batch, issued on one
 stream in model order:
   n_layers x wf_verify_attn      (block-causal GQA attention vs the cache)
-  1 x wf_kv_only_prefill_layers  (catch-up K/V projection + RoPE + append,
-                                  all layers' caches in one launch;
-                                  --prefill-per-layer: one call per layer)
+  n_layers x wf_kv_only_prefill  (catch-up K/V projection + RoPE + append;
+                                  --batch-prefill-layers: one
+                                  wf_kv_only_prefill_layers call for all
+                                  layers, reported as an upper bound only)
   1 x wf_lmhead_accept_entropy   (LM head -> argmax, entropy, accept, route)
+W_k, W_v and W_lm are streamed in the tiled layout (wf_tile_weights, done
+once at setup like weight preprocessing at model load;
+--row-major-weights: the untiled tensors).
 (the router-heavy workload adds the logits-only LM-head call).  Inputs are
 seeded synthetic tensors already resident in HBM.  The default workload is
 8B shapes at 32K context with a 16-token block (36 layers).
@@ -53,9 +57,10 @@ def parse():
                          "default: in a round the catch-up follows the route "
                          "decision and reads the target's features of the "
                          "accepted tokens, so it depends on the verification")
-    ap.add_argument("--prefill-per-layer", action="store_true",
-                    help="one wf_kv_only_prefill call per layer instead of one "
-                         "wf_kv_only_prefill_layers call for all layers")
+    ap.add_argument("--batch-prefill-layers", action="store_true",
+                    help="one wf_kv_only_prefill_layers call for all layers "
+                         "instead of one call per layer (an upper bound: a "
+                         "real forward has a layer-to-layer dependency)")
     ap.add_argument("--row-major-weights", action="store_true",
                     help="stream W_k, W_v and W_lm in their row-major layout "
                          "instead of the tiled copies made once at setup")
@@ -129,7 +134,9 @@ class Step:
             if w.n_prefill and self.pre_stack is None:
                 kc = t["drafter_k_cache"] if w.separate_drafter_cache else t["k_cache"]
                 vc = t["drafter_v_cache"] if w.separate_drafter_cache else t["v_cache"]
-                self.pre.append((code, P(t["x"]), P(t["w_k"]), P(t["w_v"]), P(kc),
+                wk, wv = t.get("w_k_tiled", t["w_k"]), t.get("w_v_tiled", t["w_v"])
+                pc = wf.WF_BF16_TILED if isinstance(wk, wf.TiledWeight) else code
+                self.pre.append((pc, P(t["x"]), P(wk), P(wv), P(kc),
                                  P(vc), w.n_prefill, w.prefill_start,
                                  kc.shape[1], w.hidden, w.n_kv_heads,
                                  w.head_dim, w.rope_base, P(self.ws_pre),
@@ -528,7 +535,7 @@ def main():
             W.ancestor_masks(par).view(np.int64).copy()).to(dev)
         tree["path"] = torch.empty(w.gamma, dtype=torch.int32, device=dev)
     pre_stack = None
-    if w.n_prefill and w.n_layers > 1 and not args.prefill_per_layer:
+    if w.n_prefill and w.n_layers > 1 and args.batch_prefill_layers:
         # the layers' catch-up inputs, weights and caches as dense [L][...]
         # stacks (per-layer views into them), so one call covers all layers
         ck, cv = (("drafter_k_cache", "drafter_v_cache") if w.separate_drafter_cache
@@ -545,6 +552,10 @@ def main():
         # static weights: tiled once at setup, as at model load
         pre_stack["w_k"] = wf.tile_weights(pre_stack["w_k"])
         pre_stack["w_v"] = wf.tile_weights(pre_stack["w_v"])
+    elif w.n_prefill and tiled:
+        for t in layers:
+            t["w_k_tiled"] = wf.tile_weights(t["w_k"])
+            t["w_v_tiled"] = wf.tile_weights(t["w_v"])
     w_lm_tiled = wf.tile_weights(head["w_lm"]) if tiled else None
     torch.cuda.synchronize()
     log(f"inputs generated in {time.perf_counter() - t0:.1f}s")
@@ -639,6 +650,20 @@ def main():
     log(f"timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step "
         f"(host wall {wall / args.steps * 1e6:.1f} us/step)")
 
+    # the spread of single steps (a second run of K steps, an event between
+    # consecutive steps; not part of `value`)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record()
+    for i in range(args.steps):
+        one_step()
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    spread = {q: round(float(np.percentile(per_step, p)) * 1e3, 1)
+              for q, p in (("p10", 10), ("median", 50), ("p90", 90))}
+    log(f"single steps (us): {spread}")
+
     # ---- timed region 2: each phase alone, calls back to back --------------
     # Events bracket only whole runs of one kind of call, so a per-call
     # average includes no event overhead and matches what a kernel trace
@@ -716,8 +741,8 @@ def main():
                    "graph": bool(graph is not None),
                    "schedule": "one stream, model order" if catchup is None else
                                "catch-up prefill on a second stream",
-                   "prefill": "one call for all layers" if step.pre_stack is not None
-                              else "one call per layer",
+                   "prefill": "one call for all layers (upper bound)"
+                              if step.pre_stack is not None else "one call per layer",
                    "weights": "tiled (16x32 tiles, made once at setup)"
                               if w_lm_tiled is not None else "row-major"}
                   | {"router": args.router}
@@ -726,6 +751,9 @@ def main():
                                      "nodes_per_depth": list(w.tree_levels)}}
                      if tree else {}),
         "step_hbm_gbps": round(step_gbps, 1),
+        "step_us_spread": spread,
+        # catch-up prefill / step: the analog of the paper's switching cost
+        "prefill_share": round(breakdown.get("prefill", 0.0) / (ms_per_step * 1e3), 4),
         "step_algorithmic_bytes": by["total"],
         "breakdown_us": breakdown,   # each phase run alone, back to back
         "roofline": {
