@@ -438,12 +438,13 @@ size_t wf_drafter_forward_workspace_bytes(wf_dtype_t dt,
                                           int32_t n_tok, int32_t pos);
 
 /* Lazy catch-up over a backlog of n_backlog tokens whose layer inputs are
- * r [n_backlog][hidden], starting at cache row pos: KV-only prefill of
- * RMSNorm(r[t]) * attn_norm for t < n_backlog - 1 (cache rows pos ..), then
- * the full layer for the last token; out [hidden] is its output.  The cache
- * rows and out equal those of wf_drafter_forward over the whole backlog
- * (to rounding).  Limits as for wf_drafter_forward, with
- * 1 <= n_backlog <= 4097 and pos + n_backlog <= cap.
+ * r [n_backlog][hidden], starting at cache row pos: RMSNorm(r[t]) *
+ * attn_norm and KV-only prefill for the whole backlog in one batch each
+ * (cache rows pos .. pos+n_backlog-1), then the rest of the layer --
+ * attention, W_o, the MLP -- for the last token only; out [hidden] is its
+ * output.  The cache rows and out equal those of wf_drafter_forward over
+ * the whole backlog (to rounding).  Limits as for wf_drafter_forward, with
+ * 1 <= n_backlog <= 4096 and pos + n_backlog <= cap.
  * workspace >= wf_drafter_catchup_workspace_bytes(...) bytes. */
 wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer,
                                const void *r, int32_t n_backlog, int32_t pos,

@@ -451,11 +451,10 @@ wf_status_t wf_drafter_forward(wf_dtype_t dt, const wf_decoder_layer_t *layer, c
 
 size_t wf_drafter_catchup_workspace_bytes(wf_dtype_t dt, const wf_decoder_layer_t *layer,
                                           int32_t n_backlog, int32_t pos) {
-    if (n_backlog < 1 || n_backlog > kMaxPrefillTokens + 1 ||
+    if (n_backlog < 1 || n_backlog > kMaxPrefillTokens ||
         check_drafter(dt, layer, pos, pos + n_backlog - 1, pos + n_backlog) != WF_OK)
         return 0;
-    if (n_backlog > 1 &&
-        !wf::prefill_fits(n_backlog - 1, layer->hidden, layer->n_kv_heads, layer->head_dim))
+    if (!wf::prefill_fits(n_backlog, layer->hidden, layer->n_kv_heads, layer->head_dim))
         return 0;
     return wf::drafter_catchup_workspace_bytes(*layer, n_backlog, pos);
 }
@@ -464,7 +463,7 @@ wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer, c
                                int32_t n_backlog, int32_t pos, void *k_cache, void *v_cache,
                                int32_t cap, void *out, void *workspace,
                                size_t workspace_bytes, void *stream) {
-    if (n_backlog < 1 || n_backlog > kMaxPrefillTokens + 1)
+    if (n_backlog < 1 || n_backlog > kMaxPrefillTokens)
         return WF_ERR_INVALID_ARG;
     const wf_status_t st = check_drafter(dt, layer, pos, pos + n_backlog - 1, cap);
     if (st != WF_OK)
@@ -472,8 +471,7 @@ wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer, c
     if (!r || !k_cache || !v_cache || !out || !aligned16(r) || !aligned16(k_cache) ||
         !aligned16(v_cache) || !aligned16(out))
         return WF_ERR_INVALID_ARG;
-    if (n_backlog > 1 &&
-        !wf::prefill_fits(n_backlog - 1, layer->hidden, layer->n_kv_heads, layer->head_dim))
+    if (!wf::prefill_fits(n_backlog, layer->hidden, layer->n_kv_heads, layer->head_dim))
         return WF_ERR_UNSUPPORTED;
     const size_t need = wf::drafter_catchup_workspace_bytes(*layer, n_backlog, pos);
     if (!workspace || workspace_bytes < need || !aligned16(workspace))

@@ -126,6 +126,58 @@ __global__ __launch_bounds__(256) void reduce_store_bf16(const float *__restrict
     y[idx] = f32_to_bf16(s);
 }
 
+// h1 = bf16(sum of slices + res) and xn2 = bf16(RMSNorm(h1) * g), one
+// workgroup per row: each thread forms h1 for the 8-feature chunks c, c +
+// 256, ... that rmsnorm_bf16 gives it, so the sum of squares (of the stored
+// bf16 h1) runs in the same order and xn2 has the bits of the two-kernel
+// form.  Requires n_out % 8 == 0.
+__global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_bf16(
+    const float *__restrict__ zpart, int ks, int n_out, int rows,
+    const uint16_t *__restrict__ res, const uint16_t *__restrict__ g, float eps,
+    uint16_t *__restrict__ h1, uint16_t *__restrict__ xn) {
+    __shared__ float part[kNormThreads / kWave];
+    const int r = blockIdx.x;
+    const int n_chunks = n_out / 8;
+    float ss = 0.f;
+    for (int c = threadIdx.x; c < n_chunks; c += kNormThreads) {
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float v[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int f = 8 * c + 2 * e + h;
+                v[h] = sum_slices(zpart, ks, n_out, rows, f, r) +
+                       bf16_to_f32(res[(size_t)r * n_out + f]);
+            }
+            o[e] = pack_bf16x2(v[0], v[1]);
+            const float a = lo_f32(o[e]), b = hi_f32(o[e]);
+            ss = fmaf(a, a, ss);
+            ss = fmaf(b, b, ss);
+        }
+        *reinterpret_cast<u32x4 *>(h1 + (size_t)r * n_out + 8 * c) = o;
+    }
+    ss = wave_sum(ss);
+    if (threadIdx.x % kWave == 0)
+        part[threadIdx.x / kWave] = ss;
+    __syncthreads();
+    float tot = part[0];
+#pragma unroll
+    for (int w = 1; w < kNormThreads / kWave; ++w)
+        tot += part[w];
+    const float inv = 1.f / sqrtf(tot / (float)n_out + eps);
+    for (int c = threadIdx.x; c < n_chunks; c += kNormThreads) {
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(h1 + (size_t)r * n_out + 8 * c);
+        const u32x4 gv = *reinterpret_cast<const u32x4 *>(g + 8 * c);
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            o[e] = pack_bf16x2(lo_f32(v[e]) * inv * lo_f32(gv[e]),
+                               hi_f32(v[e]) * inv * hi_f32(gv[e]));
+        *reinterpret_cast<u32x4 *>(xn + (size_t)r * n_out + 8 * c) = o;
+    }
+}
+
 // q[r][h][i], q[r][h][i + D/2] = RoPE at position pos + r of the pair's sums
 // (angle formed and reduced modulo 2*pi in fp64, sine and cosine in fp32)
 __global__ __launch_bounds__(256) void reduce_rope_bf16(const float *__restrict__ zpart, int ks,
@@ -218,16 +270,21 @@ size_t drafter_forward_workspace_bytes(const wf_decoder_layer_t &L, int M, int p
 
 size_t drafter_catchup_workspace_bytes(const wf_decoder_layer_t &L, int n, int pos) {
     return align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)) +
-           (size_t)(n - 1) * L.hidden * 2;
+           (size_t)n * L.hidden * 2;
 }
 
-wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, int M, int pos,
-                                   void *k_cache, void *v_cache, int cap, void *out,
-                                   void *workspace, hipStream_t stream, bool tiled) {
+namespace {
+
+// The full layer for M tokens.  xn_given: the tokens' RMSNorm(r) * g1 with
+// their K/V already in the cache (the catch-up normalises and prefills the
+// whole backlog in one batch), else both are formed here.
+wf_status_t drafter_forward(const wf_decoder_layer_t &L, const uint16_t *rb, int M, int pos,
+                            void *k_cache, void *v_cache, int cap, void *out,
+                            void *workspace, hipStream_t stream, bool tiled,
+                            const uint16_t *xn_given) {
     const wf_dtype_t wdt = tiled ? WF_BF16_TILED : WF_BF16;
     const DrafterLayout o = drafter_layout(L, M, pos);
     char *ws = static_cast<char *>(workspace);
-    const auto *rb = static_cast<const uint16_t *>(r);
     auto *xn = reinterpret_cast<uint16_t *>(ws + o.xn);
     auto *q = reinterpret_cast<uint16_t *>(ws + o.q);
     auto *a = reinterpret_cast<uint16_t *>(ws + o.a);
@@ -239,11 +296,15 @@ wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, i
     auto W = [](const void *p) { return static_cast<const uint16_t *>(p); };
     wf_status_t st;
 
-    rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(rb, W(L.attn_norm), L.rms_eps, xn, d);
-    st = launch_prefill(wdt, xn, L.w_k, L.w_v, k_cache, v_cache, M, pos, cap, d,
-                        L.n_kv_heads, L.head_dim, L.rope_base, workspace, stream);
-    if (st != WF_OK)
-        return st;
+    if (xn_given) {
+        xn = const_cast<uint16_t *>(xn_given);
+    } else {
+        rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(rb, W(L.attn_norm), L.rms_eps, xn, d);
+        st = launch_prefill(wdt, xn, L.w_k, L.w_v, k_cache, v_cache, M, pos, cap, d,
+                            L.n_kv_heads, L.head_dim, L.rope_base, workspace, stream);
+        if (st != WF_OK)
+            return st;
+    }
     // q = RoPE(Wq xn)
     if ((st = launch_linear_partial(xn, W(L.w_q), nullptr, qd, 0, M, d, zp, stream, tiled)) != WF_OK)
         return st;
@@ -258,13 +319,12 @@ wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, i
                      workspace, stream);
     if (st != WF_OK)
         return st;
-    // h1 = r + Wo a
+    // h1 = r + Wo a and xn2 = RMSNorm(h1) * g2 in one pass per row
     if ((st = launch_linear_partial(a, W(L.w_o), nullptr, d, 0, M, qd, zp, stream, tiled)) != WF_OK)
         return st;
-    reduce_store_bf16<<<blocks_for((long long)M * d), 256, 0, stream>>>(
-        zp, linear_slices(qd, d), d, M, rb, h1);
+    residual_rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(
+        zp, linear_slices(qd, d), d, M, rb, W(L.mlp_norm), L.rms_eps, h1, xn2);
     // act = SiLU(Wg xn2) * (Wu xn2)
-    rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(h1, W(L.mlp_norm), L.rms_eps, xn2, d);
     if ((st = launch_linear_partial(xn2, W(L.w_gate), W(L.w_up), I, I, M, d, zp, stream,
                                     tiled)) != WF_OK)
         return st;
@@ -278,25 +338,34 @@ wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, i
     return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
 }
 
+}  // namespace
+
+wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, int M, int pos,
+                                   void *k_cache, void *v_cache, int cap, void *out,
+                                   void *workspace, hipStream_t stream, bool tiled) {
+    return drafter_forward(L, static_cast<const uint16_t *>(r), M, pos, k_cache, v_cache, cap,
+                           out, workspace, stream, tiled, nullptr);
+}
+
+// Catch-up: RMSNorm and KV-only prefill of the whole backlog in one batch
+// each (the last token's K/V included), then the rest of the layer for the
+// last token from its normalised row.
 wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, int n, int pos,
                                    void *k_cache, void *v_cache, int cap, void *out,
                                    void *workspace, hipStream_t stream, bool tiled) {
     const int d = L.hidden;
     const auto *rb = static_cast<const uint16_t *>(r);
-    if (n > 1) {
-        auto *xnb = reinterpret_cast<uint16_t *>(
-            static_cast<char *>(workspace) + align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)));
-        rmsnorm_bf16<<<n - 1, kNormThreads, 0, stream>>>(rb, static_cast<const uint16_t *>(L.attn_norm),
-                                                         L.rms_eps, xnb, d);
-        const wf_status_t st = launch_prefill(tiled ? WF_BF16_TILED : WF_BF16, xnb, L.w_k, L.w_v,
-                                              k_cache, v_cache, n - 1,
-                                              pos, cap, d, L.n_kv_heads, L.head_dim, L.rope_base,
-                                              workspace, stream);
-        if (st != WF_OK)
-            return st;
-    }
-    return launch_drafter_forward(L, rb + (size_t)(n - 1) * d, 1, pos + n - 1, k_cache, v_cache,
-                                  cap, out, workspace, stream, tiled);
+    auto *xnb = reinterpret_cast<uint16_t *>(
+        static_cast<char *>(workspace) + align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)));
+    rmsnorm_bf16<<<n, kNormThreads, 0, stream>>>(rb, static_cast<const uint16_t *>(L.attn_norm),
+                                                 L.rms_eps, xnb, d);
+    const wf_status_t st = launch_prefill(tiled ? WF_BF16_TILED : WF_BF16, xnb, L.w_k, L.w_v,
+                                          k_cache, v_cache, n, pos, cap, d, L.n_kv_heads,
+                                          L.head_dim, L.rope_base, workspace, stream);
+    if (st != WF_OK)
+        return st;
+    return drafter_forward(L, rb + (size_t)(n - 1) * d, 1, pos + n - 1, k_cache, v_cache, cap,
+                           out, workspace, stream, tiled, xnb + (size_t)(n - 1) * d);
 }
 
 }  // namespace wf

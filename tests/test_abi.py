@@ -296,7 +296,7 @@ def test_drafter_rejects(fn, kw, lay, status):
 
 def test_drafter_token_limits():
     assert _drafter("wf_drafter_forward", n=65, cap=5000) == 1
-    assert _drafter("wf_drafter_catchup", n=4098, cap=9000) == 1
+    assert _drafter("wf_drafter_catchup", n=4097, cap=9000) == 1
     lay = _layer()
     assert wf.lib.wf_drafter_forward_workspace_bytes(1, ctypes.byref(lay), 1, 4096) > COUNTER_BLOCK
     assert wf.lib.wf_drafter_catchup_workspace_bytes(1, ctypes.byref(lay), 80, 4096) > COUNTER_BLOCK
