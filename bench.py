@@ -702,12 +702,23 @@ def main():
     step_gbps = by["total"] / (ms_per_step * 1e-3) / 1e9
 
     # ---- plain copy for the HBM traffic counters (not timed) ---------------
+    copy_gbps = None
     if args.copy_probe_mib:
         n = args.copy_probe_mib << 20
         src = torch.empty(n, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
+        # the same copy timed: a plain-streaming reference for the roofline
+        c0 = torch.cuda.Event(enable_timing=True)
+        c1 = torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for _ in range(4):
+            dst.copy_(src)
+        c1.record()
+        torch.cuda.synchronize()
+        copy_gbps = 4 * 2 * n / (c0.elapsed_time(c1) * 1e-3) / 1e9
+        log(f"device copy: {copy_gbps:.0f} GB/s (read + write)")
         del src, dst
 
     cpu = None
@@ -767,6 +778,10 @@ def main():
             "traffic": measured_traffic() if w.cfg == 3 else None,
             "bytes_per_launch": by["attn_per_layer"],
             "avg_launch_us": round(attn_avg_ms * 1e3, 2),
+            # a plain device copy in the same run (bytes read + written per
+            # second): what plain streaming reaches on this part
+            "copy_gbps": round(copy_gbps, 1) if copy_gbps else None,
+            "frac_of_copy": round(achieved / copy_gbps, 4) if copy_gbps else None,
         },
         "cpu_baseline": cpu,
     }

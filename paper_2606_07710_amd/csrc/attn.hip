@@ -789,14 +789,15 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
         // rows per wave 16*nb; rg row groups x ks key streams per workgroup
         // (at most 8 waves, so each wave may hold up to 256 registers)
         // and a ring of nbuf stages of ks tiles (LDS: nbuf*ks tiles)
+        // (more than 64 rows, e.g. a draft tree's 244: 64-row workgroups
+        // in several row groups; 128-row ones measured slower, 27.8 against
+        // 26.1 us at 244 rows and 8K keys, the key step costing more)
         if (rows <= 16) {
             p.nb = 1; p.rg = 1; p.ks = 4; p.nbuf = 2;
         } else if (rows <= 32) {
             p.nb = 1; p.rg = 2; p.ks = 4; p.nbuf = 2;
-        } else if (rows <= 64) {
-            p.nb = 1; p.rg = 4; p.ks = 2; p.nbuf = 3;
         } else {
-            p.nb = 2; p.rg = 4; p.ks = 2; p.nbuf = 3;
+            p.nb = 1; p.rg = 4; p.ks = 2; p.nbuf = 3;
         }
         p.n_row_groups = cdiv(rows, 16 * p.nb * p.rg);
     } else {
@@ -874,9 +875,9 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
         attn_partial_bf16<DHV, NBV, RGV, KSV, NBUFV><<<grid, block, 0, stream>>>(a);  \
     } else
         WF_ATTN_CASE(128, 1, 1, 4, 2) WF_ATTN_CASE(128, 1, 2, 4, 2)
-        WF_ATTN_CASE(128, 1, 4, 2, 3) WF_ATTN_CASE(128, 2, 4, 2, 3)
+        WF_ATTN_CASE(128, 1, 4, 2, 3)
         WF_ATTN_CASE(64, 1, 1, 4, 2) WF_ATTN_CASE(64, 1, 2, 4, 2)
-        WF_ATTN_CASE(64, 1, 4, 2, 3) WF_ATTN_CASE(64, 2, 4, 2, 3)
+        WF_ATTN_CASE(64, 1, 4, 2, 3)
         { return WF_ERR_UNSUPPORTED; }
 #undef WF_ATTN_CASE
     } else {
