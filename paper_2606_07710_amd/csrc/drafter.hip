@@ -103,11 +103,19 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_bf16(const uint16_t *__r
     }
 }
 
+// The slices of one output in order; all loads are issued before the first
+// add (one memory round trip, not ks).
 __device__ __forceinline__ float sum_slices(const float *zpart, int ks, int n_out, int rows,
                                             int f, int r) {
+    float v[kLinearMaxSlices];
+#pragma unroll
+    for (int k = 0; k < kLinearMaxSlices; ++k)
+        v[k] = k < ks ? zpart[((size_t)k * n_out + f) * rows + r] : 0.f;
     float s = 0.f;
-    for (int k = 0; k < ks; ++k)
-        s += zpart[((size_t)k * n_out + f) * rows + r];
+#pragma unroll
+    for (int k = 0; k < kLinearMaxSlices; ++k)
+        if (k < ks)
+            s += v[k];
     return s;
 }
 
@@ -124,58 +132,6 @@ __global__ __launch_bounds__(256) void reduce_store_bf16(const float *__restrict
     if (res)
         s += bf16_to_f32(res[idx]);
     y[idx] = f32_to_bf16(s);
-}
-
-// h1 = bf16(sum of slices + res) and xn2 = bf16(RMSNorm(h1) * g), one
-// workgroup per row: each thread forms h1 for the 8-feature chunks c, c +
-// 256, ... that rmsnorm_bf16 gives it, so the sum of squares (of the stored
-// bf16 h1) runs in the same order and xn2 has the bits of the two-kernel
-// form.  Requires n_out % 8 == 0.
-__global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_bf16(
-    const float *__restrict__ zpart, int ks, int n_out, int rows,
-    const uint16_t *__restrict__ res, const uint16_t *__restrict__ g, float eps,
-    uint16_t *__restrict__ h1, uint16_t *__restrict__ xn) {
-    __shared__ float part[kNormThreads / kWave];
-    const int r = blockIdx.x;
-    const int n_chunks = n_out / 8;
-    float ss = 0.f;
-    for (int c = threadIdx.x; c < n_chunks; c += kNormThreads) {
-        u32x4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            float v[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int f = 8 * c + 2 * e + h;
-                v[h] = sum_slices(zpart, ks, n_out, rows, f, r) +
-                       bf16_to_f32(res[(size_t)r * n_out + f]);
-            }
-            o[e] = pack_bf16x2(v[0], v[1]);
-            const float a = lo_f32(o[e]), b = hi_f32(o[e]);
-            ss = fmaf(a, a, ss);
-            ss = fmaf(b, b, ss);
-        }
-        *reinterpret_cast<u32x4 *>(h1 + (size_t)r * n_out + 8 * c) = o;
-    }
-    ss = wave_sum(ss);
-    if (threadIdx.x % kWave == 0)
-        part[threadIdx.x / kWave] = ss;
-    __syncthreads();
-    float tot = part[0];
-#pragma unroll
-    for (int w = 1; w < kNormThreads / kWave; ++w)
-        tot += part[w];
-    const float inv = 1.f / sqrtf(tot / (float)n_out + eps);
-    for (int c = threadIdx.x; c < n_chunks; c += kNormThreads) {
-        const u32x4 v = *reinterpret_cast<const u32x4 *>(h1 + (size_t)r * n_out + 8 * c);
-        const u32x4 gv = *reinterpret_cast<const u32x4 *>(g + 8 * c);
-        u32x4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            o[e] = pack_bf16x2(lo_f32(v[e]) * inv * lo_f32(gv[e]),
-                               hi_f32(v[e]) * inv * hi_f32(gv[e]));
-        *reinterpret_cast<u32x4 *>(xn + (size_t)r * n_out + 8 * c) = o;
-    }
 }
 
 // q[r][h][i], q[r][h][i + D/2] = RoPE at position pos + r of the pair's sums
@@ -319,11 +275,14 @@ wf_status_t drafter_forward(const wf_decoder_layer_t &L, const uint16_t *rb, int
                      workspace, stream);
     if (st != WF_OK)
         return st;
-    // h1 = r + Wo a and xn2 = RMSNorm(h1) * g2 in one pass per row
+    // h1 = r + Wo a (the slices summed over many workgroups), then
+    // xn2 = RMSNorm(h1) * g2.  (One workgroup per row doing both took
+    // 13 us: a single CU summing the slices of a whole row is latency-bound.)
     if ((st = launch_linear_partial(a, W(L.w_o), nullptr, d, 0, M, qd, zp, stream, tiled)) != WF_OK)
         return st;
-    residual_rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(
-        zp, linear_slices(qd, d), d, M, rb, W(L.mlp_norm), L.rms_eps, h1, xn2);
+    reduce_store_bf16<<<blocks_for((long long)M * d), 256, 0, stream>>>(
+        zp, linear_slices(qd, d), d, M, rb, h1);
+    rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(h1, W(L.mlp_norm), L.rms_eps, xn2, d);
     // act = SiLU(Wg xn2) * (Wu xn2)
     if ((st = launch_linear_partial(xn2, W(L.w_gate), W(L.w_up), I, I, M, d, zp, stream,
                                     tiled)) != WF_OK)

@@ -20,7 +20,6 @@ namespace {
 
 constexpr int kGemvWaves = 8;
 constexpr int kGemvBatch = 8;          // 32-wide chunks per wave per load batch
-constexpr int kGemvMaxSlices = 16;
 constexpr int kGemvTargetWorkgroups = 1024;
 
 template <int NBL>
@@ -111,7 +110,7 @@ int linear_slices(int k_in, int n_out) {
     // up to four workgroups per compute unit, at least 4 chunks per slice
     int ks = 1;
     while (tiles * ks * 2 <= kGemvTargetWorkgroups && chunks / (ks * 2) >= 4 &&
-           ks * 2 <= kGemvMaxSlices)
+           ks * 2 <= kLinearMaxSlices)
         ks *= 2;
     return ks;
 }

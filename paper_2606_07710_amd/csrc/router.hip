@@ -55,8 +55,6 @@ __device__ __forceinline__ float ld_param(const void *p, int i) {
                 : static_cast<const float *>(p)[i];
 }
 
-constexpr int kMaxSlices = 16;
-
 // part [cdiv(m,16)][gamma]: w2 . GELU(z) over the group's 16 units
 template <bool BF16>
 __global__ __launch_bounds__(256) void router_units(const float *__restrict__ zpart,
@@ -74,14 +72,14 @@ __global__ __launch_bounds__(256) void router_units(const float *__restrict__ zp
     for (int q = 0; q < kRouterMaxGamma / 16; ++q) {
         const int r = rr + 16 * q;
         if (r < gamma) {
-            float zs[kMaxSlices];
+            float zs[kLinearMaxSlices];
 #pragma unroll
-            for (int k = 0; k < kMaxSlices; ++k)
+            for (int k = 0; k < kLinearMaxSlices; ++k)
                 zs[k] = (unit_ok && k < n_slices)
                             ? zpart[((size_t)k * m + u0 + u) * gamma + r] : 0.f;
             float z = bias;
 #pragma unroll
-            for (int k = 0; k < kMaxSlices; ++k)
+            for (int k = 0; k < kLinearMaxSlices; ++k)
                 if (k < n_slices)
                     z += zs[k];
             cs[u][r] = unit_ok ? w2u * gelu_exact(z) : 0.f;

@@ -57,6 +57,7 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
 // slice of W[f] . x[r] for rows <= 64, features n_a + n_b (a multiple of
 // 16; [0, n_a) from w_a, the rest from w_b) and k_in a multiple of 32.
 int linear_slices(int k_in, int n_out);
+constexpr int kLinearMaxSlices = 16;     // linear_slices never exceeds this
 wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
                                   const uint16_t *w_b, int n_a, int n_b, int rows,
                                   int k_in, float *zpart, hipStream_t stream,
