@@ -644,6 +644,7 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
         if (vis) {
             const float *kr = kbase + (size_t)j * DH;
             float dot = 0.f;
+#pragma unroll 16
             for (int d = 0; d < DH; ++d)
                 dot = fmaf(qs[d], kr[d], dot);
             sc = dot;
@@ -655,11 +656,12 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
 #pragma unroll
         for (int e = 0; e < E; ++e)
             acc[e] *= alpha;
+        // every key up to cnt is a cache row in range; a masked key has
+        // p = 0 and adds nothing (no branch, so the loads can be batched)
         const int cnt = min(kWave, k_end - kb);
+#pragma unroll 16
         for (int tt = 0; tt < cnt; ++tt) {
             const float pt = __shfl(p, tt, kWave);
-            if (pt == 0.f)              // masked key (uniform: broadcast value)
-                continue;
             const float *vr = vbase + (size_t)(kb + tt) * DH;
 #pragma unroll
             for (int e = 0; e < E; ++e)
@@ -811,9 +813,12 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
     int splits = num_splits;
     if (splits <= 0) {
         // one workgroup per CU of the 256-CU chip, but give every key
-        // stream of a workgroup at least two tiles
+        // stream of a workgroup at least two tiles (fp32: one wave per
+        // split and pair, at least one 64-key block each)
         const int target = std::max(1, 256 / (n_kv_heads * p.n_row_groups));
-        const int max_by_work = std::max(1, n_tiles / (2 * std::max(p.ks, 4)));
+        const int max_by_work = dt == WF_BF16
+                                    ? std::max(1, n_tiles / (2 * std::max(p.ks, 4)))
+                                    : std::max(1, cdiv(n_keys, kWave));
         splits = std::max(1, std::min(target, max_by_work));
     }
     splits = std::min(splits, n_tiles);

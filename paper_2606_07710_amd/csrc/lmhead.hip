@@ -575,29 +575,61 @@ __global__ __launch_bounds__(512) void lm_wide_bf16(const uint16_t *__restrict__
     }
 }
 
+// NR = verify rows per thread (rows rq, rq + 4, ...: ceil(gamma / 4) rounded
+// up to a power of two), a template parameter so the inner loop carries no
+// per-row branches.
+template <int NR>
 __global__ __launch_bounds__(256) void lm_tiles_f32(const float *__restrict__ h,
                                                     const float *__restrict__ w,
                                                     LmFinish f, int d, int vocab) {
     RowState *states = f.states;
     const int gamma = f.gamma, n_tiles = f.n_tiles;
-    constexpr int kRowsPerThread = kMaxGamma / 4;
+    constexpr int kRowsPerThread = NR;
+    static_assert(kMaxGamma == kLmTile, "h and W tiles share the staging map");
     __shared__ __attribute__((aligned(16))) float zs[kMaxGamma][kLmTile + 4];
     const int tile = blockIdx.x;
     const int v0 = tile * kLmTile;
     const int vl = threadIdx.x % kLmTile;
     const int rq = threadIdx.x / kLmTile;
-    const float *wr = w + (size_t)min(v0 + vl, vocab - 1) * d;
+    // h and the tile's W rows are staged in LDS 128 dims at a time with
+    // coalesced loads; W rows are padded so the 64 threads of a wave (64
+    // vocabulary rows, one column) hit distinct banks, and a wave's threads
+    // share one verify-row group, so each h read is a broadcast.  Each
+    // thread's sum still runs over the dimensions in order.
+    // (every thread issues all of its staging loads before its first LDS
+    // store: one memory round trip per chunk)
+    constexpr int KC = 128;
+    constexpr int NL = kLmTile * KC / 256;          // staged floats per thread
+    __shared__ float hs[kMaxGamma][KC];
+    __shared__ float wt[kLmTile][KC + 1];
     float acc[kRowsPerThread];
 #pragma unroll
     for (int k = 0; k < kRowsPerThread; ++k)
         acc[k] = 0.f;
-    for (int c = 0; c < d; ++c) {
-        const float wv = wr[c];
+    for (int c0 = 0; c0 < d; c0 += KC) {
+        const int kc = min(KC, d - c0);
+        float hv[NL], wv_[NL];
 #pragma unroll
-        for (int k = 0; k < kRowsPerThread; ++k) {
-            const int r = rq + 4 * k;
-            if (r < gamma)
-                acc[k] = fmaf(h[(size_t)r * d + c], wv, acc[k]);
+        for (int u = 0; u < NL; ++u) {
+            const int idx = threadIdx.x + 256 * u;
+            const int r = idx / KC, c = idx % KC;     // kMaxGamma * KC == kLmTile * KC
+            hv[u] = (r < gamma && c < kc) ? h[(size_t)r * d + c0 + c] : 0.f;
+            wv_[u] = c < kc ? w[(size_t)min(v0 + r, vocab - 1) * d + c0 + c] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < NL; ++u) {
+            const int idx = threadIdx.x + 256 * u;
+            hs[idx / KC][idx % KC] = hv[u];
+            wt[idx / KC][idx % KC] = wv_[u];
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int c = 0; c < kc; ++c) {
+            const float wv = wt[vl][c];
+#pragma unroll
+            for (int k = 0; k < kRowsPerThread; ++k)      // rows past gamma: zeros
+                acc[k] = fmaf(hs[rq + 4 * k][c], wv, acc[k]);
         }
     }
 #pragma unroll
@@ -710,9 +742,17 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
         }
     } else {
         f.n_tiles = cdiv(vocab, kLmTile);
-        lm_tiles_f32<<<f.n_tiles, 256, 0, stream>>>(static_cast<const float *>(h),
-                                                   static_cast<const float *>(w_lm),
-                                                   f, d, vocab);
+        const float *hf = static_cast<const float *>(h);
+        const float *wf32 = static_cast<const float *>(w_lm);
+        const int nr = cdiv(gamma, 4);
+        if (nr <= 2)
+            lm_tiles_f32<2><<<f.n_tiles, 256, 0, stream>>>(hf, wf32, f, d, vocab);
+        else if (nr <= 4)
+            lm_tiles_f32<4><<<f.n_tiles, 256, 0, stream>>>(hf, wf32, f, d, vocab);
+        else if (nr <= 8)
+            lm_tiles_f32<8><<<f.n_tiles, 256, 0, stream>>>(hf, wf32, f, d, vocab);
+        else
+            lm_tiles_f32<16><<<f.n_tiles, 256, 0, stream>>>(hf, wf32, f, d, vocab);
     }
     lm_finish_rows<<<gamma, kFinishThreads, 0, stream>>>(f);
     if (hipGetLastError() != hipSuccess)

@@ -212,13 +212,17 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
     }
 }
 
-// fp32 path: one thread per (token, KV head, rotation pair, K or V).
+// fp32 path: one wave per (token, KV head, rotation pair, K or V).  Lane
+// l takes the input dims l, l + 64, ... (coalesced loads) in order; the two
+// dot products then meet in a fixed butterfly, and lane 0 rotates and
+// writes the pair.
 __global__ __launch_bounds__(256) void prefill_f32(PrefillParams a, int dh) {
     const int half = dh / 2;
     const long long total = (long long)a.n_tok * a.n_kv_heads * half * 2;
-    const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    const long long idx = ((long long)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+    const int lane = threadIdx.x % kWave;
     if (idx >= total)
-        return;
+        return;                          // whole waves: idx is wave-uniform
     const int i = (int)(idx % half);
     const int kind = (int)((idx / half) % 2);
     const int g = (int)((idx / (2 * half)) % a.n_kv_heads);
@@ -228,10 +232,16 @@ __global__ __launch_bounds__(256) void prefill_f32(PrefillParams a, int dh) {
     const float *w_lo = w + (size_t)(g * dh + i) * a.d_in;
     const float *w_hi = w + (size_t)(g * dh + i + half) * a.d_in;
     float lo = 0.f, hi = 0.f;
-    for (int c = 0; c < a.d_in; ++c) {
-        lo = fmaf(w_lo[c], x[c], lo);
-        hi = fmaf(w_hi[c], x[c], hi);
+#pragma unroll 4
+    for (int c = lane; c < a.d_in; c += kWave) {
+        const float xv = x[c];
+        lo = fmaf(w_lo[c], xv, lo);
+        hi = fmaf(w_hi[c], xv, hi);
     }
+    lo = wave_sum(lo);
+    hi = wave_sum(hi);
+    if (lane != 0)
+        return;
     const int pos = a.start_pos + t;
     if (kind == 0)
         rope_pair(lo, hi, a.theta[i], pos);
@@ -312,8 +322,8 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
         { return WF_ERR_UNSUPPORTED; }
 #undef WF_PF_CASE
     } else {
-        const long long total = (long long)n_tok * n_kv_heads * head_dim;
-        const unsigned blocks = (unsigned)((total + 255) / 256);
+        const long long total = (long long)n_tok * n_kv_heads * head_dim;   // waves
+        const unsigned blocks = (unsigned)((total * kWave + 255) / 256);
         for (int l = 0; l < n_layers; ++l) {
             PrefillParams al = a;
             al.x = static_cast<const float *>(x) + l * x_ls;
