@@ -33,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
+PEAK_BF16_FLOPS = 2.5e15       # dense bf16 MFMA
 
 
 def parse():
@@ -782,6 +783,9 @@ def main():
             # second): what plain streaming reaches on this part
             "copy_gbps": round(copy_gbps, 1) if copy_gbps else None,
             "frac_of_copy": round(achieved / copy_gbps, 4) if copy_gbps else None,
+            # secondary: the call's flops against the dense bf16 MFMA peak
+            "mfma_util": round(w.flops()["attn_per_layer"] / (attn_avg_ms * 1e-3)
+                               / PEAK_BF16_FLOPS, 4),
         },
         "cpu_baseline": cpu,
     }
