@@ -105,3 +105,32 @@ def test_tree_tokens_accept_exactly_k():
         for j in range(1, 61):
             depth[j] = depth[int(par[j])] + 1
         assert max(depth[j] for j in accepted) == min(k, 8)
+
+
+def test_switch_workload_and_drafter_generator():
+    """Workload 7: one drafter layer with the 8B attention shapes, a 4096-row
+    cache and an 80-token backlog; the generator gives every projection its
+    nn.Linear shape, gains near 1, a cache whose rows past the base are
+    zero, and the same bytes for the same seed."""
+    import dataclasses
+    w = W.CONFIGS[7]
+    assert (w.hidden, w.n_q_heads, w.n_kv_heads, w.head_dim, w.inter) == (4096, 32, 8, 128, 12288)
+    assert (w.ctx_len, w.n_prefill, w.n_layers) == (4096, 80, 1)
+    small = dataclasses.replace(w, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64,
+                                inter=512, ctx_len=10, n_prefill=3)
+    t = W.generate_drafter(small)
+    shapes = {"attn_norm": (256,), "w_q": (256, 256), "w_k": (128, 256), "w_v": (128, 256),
+              "w_o": (256, 256), "mlp_norm": (256,), "w_gate": (512, 256),
+              "w_up": (512, 256), "w_down": (256, 512)}
+    for name, shp in shapes.items():
+        assert tuple(t[name].shape) == shp, name
+    assert tuple(t["k_cache"].shape) == (2, 13, 64) and tuple(t["r"].shape) == (3, 256)
+    assert not t["k_cache"][:, 10:].any() and t["k_cache"][:, :10].abs().sum() > 0
+    g = t["attn_norm"].float()
+    assert (g - 1).abs().max() < 1.0 and (g - 1).abs().mean() > 0.01
+    t2 = W.generate_drafter(small)
+    for name in shapes:
+        assert torch.equal(t[name], t2[name])
+    assert w.drafter_weight_bytes() == (2 * 4096 * 4096 + 2 * 1024 * 4096
+                                        + 3 * 12288 * 4096 + 2 * 4096) * 2
+    assert w.catchup_bytes(80, 4096) == 403_988_480
