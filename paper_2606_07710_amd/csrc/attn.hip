@@ -791,15 +791,19 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
         // rows per wave 16*nb; rg row groups x ks key streams per workgroup
         // (at most 8 waves, so each wave may hold up to 256 registers)
         // and a ring of nbuf stages of ks tiles (LDS: nbuf*ks tiles)
-        // (more than 64 rows, e.g. a draft tree's 244: 64-row workgroups
-        // in several row groups; 128-row ones measured slower, 27.8 against
-        // 26.1 us at 244 rows and 8K keys, the key step costing more)
+        // (65-128 rows, e.g. 64 q heads over 8 KV heads with a 16-token
+        // block: one 128-row workgroup per (head, split), 60 against 72 us
+        // at 64K keys with two 64-row ones; more rows, e.g. a draft tree's
+        // 244: 64-row workgroups in several row groups, 26.1 against
+        // 27.8 us at 8K keys with 128-row ones)
         if (rows <= 16) {
             p.nb = 1; p.rg = 1; p.ks = 4; p.nbuf = 2;
         } else if (rows <= 32) {
             p.nb = 1; p.rg = 2; p.ks = 4; p.nbuf = 2;
-        } else {
+        } else if (rows <= 64 || rows > 128) {
             p.nb = 1; p.rg = 4; p.ks = 2; p.nbuf = 3;
+        } else {
+            p.nb = 2; p.rg = 4; p.ks = 2; p.nbuf = 3;
         }
         p.n_row_groups = cdiv(rows, 16 * p.nb * p.rg);
     } else {
@@ -880,9 +884,9 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
         attn_partial_bf16<DHV, NBV, RGV, KSV, NBUFV><<<grid, block, 0, stream>>>(a);  \
     } else
         WF_ATTN_CASE(128, 1, 1, 4, 2) WF_ATTN_CASE(128, 1, 2, 4, 2)
-        WF_ATTN_CASE(128, 1, 4, 2, 3)
+        WF_ATTN_CASE(128, 1, 4, 2, 3) WF_ATTN_CASE(128, 2, 4, 2, 3)
         WF_ATTN_CASE(64, 1, 1, 4, 2) WF_ATTN_CASE(64, 1, 2, 4, 2)
-        WF_ATTN_CASE(64, 1, 4, 2, 3)
+        WF_ATTN_CASE(64, 1, 4, 2, 3) WF_ATTN_CASE(64, 2, 4, 2, 3)
         { return WF_ERR_UNSUPPORTED; }
 #undef WF_ATTN_CASE
     } else {

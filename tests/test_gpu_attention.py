@@ -59,6 +59,8 @@ CASES = [
     ("bf16", 64, 300, 8, 8, 64),
     ("bf16", 16, 4000, 64, 8, 128),
     ("bf16", 3, 129, 12, 4, 64),
+    ("bf16", 12, 700, 32, 4, 64),        # 96 rows per KV head: 128-row groups
+    ("bf16", 30, 900, 16, 4, 128),       # 120 rows per KV head
     ("f32", 8, 256, 8, 2, 64),
     ("f32", 3, 1000, 4, 4, 128),
     ("f32", 1, 0, 2, 1, 64),
