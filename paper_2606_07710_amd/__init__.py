@@ -464,13 +464,15 @@ def decoder_layer(weights, n_q_heads, n_kv_heads, rms_eps, rope_base):
 
 def wf_drafter_forward_workspace_bytes(layer, n_tok, pos) -> int:
     """Workspace of a bf16 wf_drafter_forward call (0: shapes rejected)."""
-    return int(lib.wf_drafter_forward_workspace_bytes(WF_BF16, ctypes.byref(layer),
+    code = WF_BF16_TILED if getattr(layer, "tiled", False) else WF_BF16
+    return int(lib.wf_drafter_forward_workspace_bytes(code, ctypes.byref(layer),
                                                       int(n_tok), int(pos)))
 
 
 def wf_drafter_catchup_workspace_bytes(layer, n_backlog, pos) -> int:
     """Workspace of a bf16 wf_drafter_catchup call (0: shapes rejected)."""
-    return int(lib.wf_drafter_catchup_workspace_bytes(WF_BF16, ctypes.byref(layer),
+    code = WF_BF16_TILED if getattr(layer, "tiled", False) else WF_BF16
+    return int(lib.wf_drafter_catchup_workspace_bytes(code, ctypes.byref(layer),
                                                       int(n_backlog), int(pos)))
 
 
