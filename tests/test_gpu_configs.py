@@ -43,8 +43,11 @@ def test_layers(cfg):
         if w.n_prefill:
             kc = t["drafter_k_cache"] if w.separate_drafter_cache else t["k_cache"]
             vc = t["drafter_v_cache"] if w.separate_drafter_cache else t["v_cache"]
-            wf.wf_kv_only_prefill(t["x"], t["w_k"], t["w_v"], kc, vc,
-                                  w.prefill_start, w.rope_base)
+            # as the benchmark runs it: bf16 weights in the tiled layout
+            tiled = w.dtype == "bf16"
+            wk = wf.tile_weights(t["w_k"]) if tiled else t["w_k"]
+            wv = wf.tile_weights(t["w_v"]) if tiled else t["w_v"]
+            wf.wf_kv_only_prefill(t["x"], wk, wv, kc, vc, w.prefill_start, w.rope_base)
             torch.cuda.synchronize()
             kr, vr = oracle.kv_only_prefill(
                 W.to_oracle(t["x"]), W.to_oracle(t["w_k"]),
@@ -92,10 +95,12 @@ def test_lmhead(cfg):
     print(f"config {cfg}: LM head oracle done", flush=True)
     tau = float(np.median(ent_ref))
     bar = 1e-2 if w.dtype == "bf16" else 1e-6
+    # as the benchmark runs it: bf16 W_lm in the tiled layout
+    w_lm = wf.tile_weights(hd["w_lm"]) if w.dtype == "bf16" else hd["w_lm"]
     for ds in range(16):
         k = W.prefix_len(w, ds)
         draft = W.make_drafts(am_ref, k, w.vocab, 100 * cfg + ds)
-        am, ent, acc = _lm(hd["h"], hd["w_lm"], None, draft, tau, w.gamma)
+        am, ent, acc = _lm(hd["h"], w_lm, None, draft, tau, w.gamma)
         if ds == 0:
             check_argmax(am, am_ref, margin, z, w.dtype)
             assert entropy_rel_err(ent, ent_ref) <= TOL[w.dtype]
