@@ -51,7 +51,7 @@ wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
 
 extern "C" {
 
-int32_t wf_abi_version(void) { return 5; }
+int32_t wf_abi_version(void) { return 6; }
 
 const char *wf_status_string(wf_status_t s) {
     switch (s) {

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert wf.abi_version() == 5
+    assert wf.abi_version() == 6
     assert wf.status_string(wf.WF_OK) == "ok"
     assert "workspace" in wf.status_string(wf.WF_ERR_WORKSPACE)
     assert wf.status_string(99) == "unknown status"
