@@ -196,12 +196,14 @@ wf_status_t wf_verify_attn_tree(wf_dtype_t dt, const void *q,
  * (angles formed in fp64).
  *
  * x         [n_tok][d_in], the layer input after RMSNorm.
- * w_k, w_v  [n_kv_heads*head_dim][d_in] each (output feature major).
+ * w_k, w_v  [n_kv_heads*head_dim][d_in] each (output feature major);
+ *           with WF_BF16_TILED their tiled copies (wf_tile_weights).
  * k_cache, v_cache  [n_kv_heads][cap][head_dim]; only rows
- *           [start_pos, start_pos+n_tok) are written (dtype dt).
+ *           [start_pos, start_pos+n_tok) are written (bf16 for both bf16
+ *           dtypes, else fp32).
  * Limits:   0 <= n_tok <= 4096 (0 is a no-op); start_pos >= 0;
  *           start_pos + n_tok <= cap; head_dim in {64, 128};
- *           d_in >= 1, and d_in % 32 == 0 for WF_BF16.
+ *           d_in >= 1, and d_in % 32 == 0 for the bf16 dtypes.
  * workspace >= wf_kv_only_prefill_workspace_bytes(...) bytes (may be NULL
  *           when that is 0: fp32, or no tokens).  The bf16 path splits the
  *           input dimension across a power-of-two number of workgroups whose
@@ -277,8 +279,12 @@ size_t wf_kv_only_prefill_layers_workspace_bytes(wf_dtype_t dt, int32_t n_tok,
  * draft     [gamma-1] int32: draft[j] is the token at block row j+1, checked
  *           against the argmax of row j.  May be NULL only when gamma == 1.
  * argmax_out [gamma] int32, entropy_out [gamma] fp32, accept_out [3] int32.
+ * w_lm with WF_BF16_TILED: its tiled copy (wf_tile_weights; rows padded to
+ *           a multiple of 16, so the buffer holds ceil(vocab/16)*16 rows).
  * Limits:   1 <= gamma <= 64; 1 <= vocab <= 2^30; d >= 1, and
- *           d % 32 == 0 for WF_BF16.
+ *           d % 32 == 0 for the bf16 dtypes; WF_BF16_TILED needs
+ *           gamma <= 16 with d in {4096, 5120}, or d % 512 == 0
+ *           (else WF_ERR_UNSUPPORTED).
  * workspace >= wf_lmhead_workspace_bytes(gamma, vocab) bytes.
  * ---------------------------------------------------------------------- */
 wf_status_t wf_lmhead_accept_entropy(wf_dtype_t dt, const void *h,
