@@ -51,6 +51,8 @@ CASES = [
     ("bf16", 33, 1000, 32, 8, 128),
     ("bf16", 61, 2049, 32, 8, 128),
     ("bf16", 64, 300, 16, 2, 128),
+    ("bf16", 20, 517, 32, 8, 128),             # 80 rows per KV head: 128-row workgroups
+    ("bf16", 40, 700, 16, 4, 64),              # 160 rows, head_dim 64: three row groups
     ("f32", 9, 100, 8, 2, 64),
     ("f32", 61, 257, 8, 2, 64),
 ]
