@@ -1,0 +1,115 @@
+"""Seeded random-shape GPU parity sweep against the fp64 oracle: verify
+attention (block-causal and tree masks, Sec. 3.2), KV-only prefill (Sec.
+3.4) and the LM head with acceptance and entropy (Sec. 3.3.1), over shapes
+drawn from the ranges the C ABI accepts (tests/random_cases.py: gamma 1..64,
+ragged context and vocabulary, head_dim 64 and 128, fp32 and bf16,
+row-major and tiled weights).  Each test runs a bounded number of cases
+from a fixed seed, prints every case before it runs, and stops at the first
+mismatch.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import random_cases as R
+import workloads as W
+from parity import (TOL, accept_is_consistent, check_argmax, entropy_rel_err,
+                    host64, max_vec_rel_err)
+
+pytestmark = pytest.mark.gpu
+
+wf = pytest.importorskip("paper_2606_07710_amd")
+DEV = "cuda"
+DT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def test_attention_random_shapes():
+    for c in R.attn_cases():
+        print(f"random attn #{c['case']}: {c['dt']} gamma={c['gamma']} "
+              f"ctx={c['ctx']} hq={c['hq']} hkv={c['hkv']} dh={c['dh']} "
+              f"splits={c['splits']} tree={c['tree']} std={c['std']}", flush=True)
+        dt, gamma, ctx, seed = c["dt"], c["gamma"], c["ctx"], c["seed"]
+        hq, hkv, dh, cap, std = c["hq"], c["hkv"], c["dh"], c["cap"], c["std"]
+        q = W.normal((gamma, hq, dh), std, W.stream_seed(seed, "q"), DT[dt], DEV)
+        k = W.normal((hkv, cap, dh), std, W.stream_seed(seed, "k_cache"), DT[dt], DEV)
+        v = W.normal((hkv, cap, dh), std, W.stream_seed(seed, "v_cache"), DT[dt], DEV)
+        k[:, ctx + gamma:] = float("nan")       # past the block: never read
+        v[:, ctx + gamma:] = float("nan")
+        out = torch.empty_like(q)
+        n = ctx + gamma
+        kk = W.to_oracle(k[:, :n].contiguous())
+        vv = W.to_oracle(v[:, :n].contiguous())
+        if c["tree"]:
+            mask = W.ancestor_masks(c["parents"])
+            md = torch.from_numpy(mask.view(np.int64).copy()).to(DEV)
+            wf.wf_verify_attn_tree(q, k, v, out, ctx, md, num_splits=c["splits"])
+            torch.cuda.synchronize()
+            ref = oracle.verify_attn_mask(W.to_oracle(q), kk, vv, ctx, mask)
+        else:
+            wf.wf_verify_attn(q, k, v, out, ctx, num_splits=c["splits"])
+            torch.cuda.synchronize()
+            ref = oracle.verify_attn(W.to_oracle(q), kk, vv, ctx)
+        got = host64(out)
+        assert np.isfinite(got).all(), c["case"]
+        err = max_vec_rel_err(got, ref)
+        assert err <= TOL[dt], (c["case"], err)
+
+
+def test_prefill_random_shapes():
+    for c in R.prefill_cases():
+        print(f"random prefill #{c['case']}: {c['dt']} tiled={c['tiled']} "
+              f"n={c['n']} d_in={c['d_in']} hkv={c['hkv']} dh={c['dh']} "
+              f"start={c['start']} base={c['base']:g}", flush=True)
+        dt, n, d_in, hkv, dh = c["dt"], c["n"], c["d_in"], c["hkv"], c["dh"]
+        start, seed = c["start"], c["seed"]
+        xs = 1.0 if dt == "bf16" else 0.5
+        x = W.normal((n, d_in), xs, W.stream_seed(seed, "x"), DT[dt], DEV)
+        wk = W.normal((hkv * dh, d_in), 0.02, W.stream_seed(seed, "w_k"), DT[dt], DEV)
+        wv = W.normal((hkv * dh, d_in), 0.02, W.stream_seed(seed, "w_v"), DT[dt], DEV)
+        kc = torch.zeros((hkv, c["cap"], dh), dtype=DT[dt], device=DEV)
+        vc = torch.zeros_like(kc)
+        wkp = wf.tile_weights(wk) if c["tiled"] else wk
+        wvp = wf.tile_weights(wv) if c["tiled"] else wv
+        wf.wf_kv_only_prefill(x, wkp, wvp, kc, vc, start, c["base"])
+        torch.cuda.synchronize()
+        kr, vr = oracle.kv_only_prefill(W.to_oracle(x), W.to_oracle(wk),
+                                        W.to_oracle(wv), start, hkv, dh, c["base"])
+        ek = max_vec_rel_err(host64(kc[:, start:start + n]), kr)
+        ev = max_vec_rel_err(host64(vc[:, start:start + n]), vr)
+        assert ek <= TOL[dt] and ev <= TOL[dt], (c["case"], ek, ev)
+        # rows outside the catch-up stay untouched
+        assert not kc[:, :start].any() and not kc[:, start + n:].any(), c["case"]
+        assert not vc[:, :start].any() and not vc[:, start + n:].any(), c["case"]
+
+
+def test_lmhead_random_shapes():
+    for c in R.lmhead_cases():
+        print(f"random lmhead #{c['case']}: {c['dt']} tiled={c['tiled']} "
+              f"gamma={c['gamma']} d={c['d']} vocab={c['vocab']} "
+              f"w_std={c['w_std']}", flush=True)
+        dt, gamma, d, vocab, seed = c["dt"], c["gamma"], c["d"], c["vocab"], c["seed"]
+        h = W.normal((gamma, d), 1.0, W.stream_seed(seed, "h"), DT[dt], DEV)
+        w = W.normal((vocab, d), c["w_std"], W.stream_seed(seed, "w_lm"), DT[dt], DEV)
+        am_ref, ent_ref, margin, z = oracle.lmhead_rows(W.to_oracle(h), W.to_oracle(w),
+                                                        want_logits=True)
+        k = W.geometric_prefix(0.3, gamma, seed)
+        draft = W.make_drafts(am_ref, k, vocab, seed)
+        tau = float(np.median(ent_ref))
+        am = torch.empty(gamma, dtype=torch.int32, device=DEV)
+        ent = torch.empty(gamma, dtype=torch.float32, device=DEV)
+        acc = torch.empty(3, dtype=torch.int32, device=DEV)
+        dr = torch.as_tensor(draft, device=DEV) if gamma > 1 else None
+        wl = wf.tile_weights(w) if c["tiled"] else w
+        wf.wf_lmhead_accept_entropy(h, wl, None, dr, tau, am, ent, acc)
+        torch.cuda.synchronize()
+        am, ent, acc = am.cpu().numpy(), ent.cpu().numpy(), acc.cpu().numpy()
+        check_argmax(am, am_ref, margin, z, dt)
+        assert entropy_rel_err(ent, ent_ref) <= TOL[dt], c["case"]
+        assert accept_is_consistent(acc[0], acc[1], acc[2], am, ent, draft, tau), c["case"]
+        bar = 1e-2 if dt == "bf16" else 1e-6
+        if all(margin[j] > bar for j in range(min(k, gamma - 1) + 1)):
+            n_ref, bonus_ref, route_ref, _ = oracle.accept(am_ref, ent_ref, draft, tau)
+            assert (acc[0], acc[1]) == (n_ref, bonus_ref), c["case"]
+            if abs(ent_ref[n_ref] - tau) > TOL[dt] * max(abs(ent_ref[n_ref]), 1e-3):
+                assert acc[2] == route_ref, c["case"]

@@ -1,0 +1,44 @@
+"""Host-side check of the GPU random-shape sweep's cases (tests/random_cases.py):
+every drawn shape lies in the ranges the C ABI accepts, so the sweep tests
+the kernels rather than argument validation.  No GPU call is made."""
+import pytest
+
+import random_cases as R
+
+wf = pytest.importorskip("paper_2606_07710_amd")
+
+
+def test_attention_cases_are_accepted():
+    cases = R.attn_cases()
+    assert any(c["tree"] for c in cases) and any(not c["tree"] for c in cases)
+    assert {c["dh"] for c in cases} == {64, 128}
+    assert {c["dt"] for c in cases} == {"f32", "bf16"}
+    for c in cases:
+        code = wf.WF_F32 if c["dt"] == "f32" else wf.WF_BF16
+        assert 1 <= c["gamma"] <= 64 and c["ctx"] + c["gamma"] <= c["cap"]
+        assert wf.wf_verify_attn_workspace_bytes(code, c["gamma"], c["ctx"], c["hq"],
+                                                 c["hkv"], c["dh"], c["splits"]) > 0, c
+
+
+def test_prefill_cases_are_accepted():
+    for c in R.prefill_cases():
+        if c["dt"] == "f32":
+            code = wf.WF_F32
+        else:
+            code = wf.WF_BF16_TILED if c["tiled"] else wf.WF_BF16
+            assert c["d_in"] % 32 == 0
+            # bf16 plans need their exchange slots to fit: the query says 0 otherwise
+            assert wf.wf_kv_only_prefill_workspace_bytes(code, c["n"], c["d_in"], c["hkv"],
+                                                         c["dh"]) > 0, c
+        assert c["start"] + c["n"] <= c["cap"]
+
+
+def test_lmhead_cases_are_accepted():
+    cases = R.lmhead_cases()
+    assert any(c["tiled"] for c in cases)
+    for c in cases:
+        assert wf.wf_lmhead_workspace_bytes(c["gamma"], c["vocab"]) > 0, c
+        if c["dt"] == "bf16":
+            assert c["d"] % 32 == 0
+        if c["tiled"]:
+            assert c["d"] % 512 == 0 or (c["gamma"] <= 16 and c["d"] in (4096, 5120))
