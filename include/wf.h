@@ -49,7 +49,8 @@
  * Conventions shared by every call
  *   - Every tensor pointer is DEVICE memory owned by the caller, 16-byte
  *     aligned, densely packed in the layout stated.  The library never
- *     allocates, frees or synchronises, and keeps no global state.
+ *     allocates, frees or synchronises, and keeps no global state (the one
+ *     exception, wf_verify_attn_noalloc, holds a static device array).
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
  *     stream).  Outputs are valid once the stream reaches that point.
  *   - Arguments are validated on the host before anything is launched; on a
@@ -153,6 +154,35 @@ size_t wf_verify_attn_workspace_bytes(wf_dtype_t dt, int32_t gamma,
                                       int32_t ctx_len, int32_t n_q_heads,
                                       int32_t n_kv_heads, int32_t head_dim,
                                       int32_t num_splits);
+
+/* ------------------------------------------------------------------------
+ * wf_verify_attn_noalloc -- wf_verify_attn without a workspace argument,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ *
+ * Same arguments, limits, kernels and results as wf_verify_attn (bit for bit
+ * at the same num_splits), minus the workspace.  The split partials go to a
+ * static device array of WF_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends; a call whose workspace query
+ * (wf_verify_attn_workspace_bytes, same arguments) exceeds that size returns
+ * WF_ERR_WORKSPACE without launching anything (the 32 MiB below hold the
+ * 4 MiB zero block and 28 MiB of partials: 16 rows x 64 query heads at
+ * head_dim 128 take 264 KiB per key split, so up to 108 splits; the
+ * automatic plan uses 32).  The first
+ * call on a device looks up the array's address there (with that device
+ * current) and clears its zero block with a kernel on `stream`; no call
+ * allocates or frees.  Every call on one GPU uses that GPU's single array:
+ * calls that overlap in time on one GPU (different streams, threads) race,
+ * so the caller orders them.
+ * ---------------------------------------------------------------------- */
+#define WF_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+wf_status_t wf_verify_attn_noalloc(wf_dtype_t dt, const void *q, const void *k_cache,
+                                   const void *v_cache, void *out, int32_t gamma,
+                                   int32_t ctx_len, int32_t cap, int32_t n_q_heads,
+                                   int32_t n_kv_heads, int32_t head_dim,
+                                   float softmax_scale, int32_t num_splits,
+                                   void *stream);
 
 /* ------------------------------------------------------------------------
  * wf_verify_attn_tree -- target attention over a draft tree (Sec. 3.1: an

@@ -28,8 +28,9 @@ EXPORTED_SYMBOLS = (
     "wf_drafter_forward_workspace_bytes", "wf_drafter_catchup",
     "wf_drafter_catchup_workspace_bytes", "wf_switch_init", "wf_switch_commit",
     "wf_kv_only_prefill_layers", "wf_kv_only_prefill_layers_workspace_bytes",
-    "wf_tiled_weight_bytes", "wf_tile_weights",
+    "wf_tiled_weight_bytes", "wf_tile_weights", "wf_verify_attn_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 32 << 20     # WF_NOALLOC_SCRATCH_BYTES
 WF_DRAFTER_AR, WF_DRAFTER_DIFFUSION = 0, 1
 
 DECODER_WEIGHTS = ("attn_norm", "w_q", "w_k", "w_v", "w_o", "mlp_norm",
@@ -74,6 +75,9 @@ def _load():
     lib.wf_verify_attn.argtypes = [i32, p, p, p, p, i32, i32, i32, i32, i32,
                                    i32, f32, i32, p, sz, p]
     lib.wf_verify_attn.restype = i32
+    lib.wf_verify_attn_noalloc.argtypes = [i32, p, p, p, p, i32, i32, i32, i32, i32,
+                                           i32, f32, i32, p]
+    lib.wf_verify_attn_noalloc.restype = i32
     lib.wf_verify_attn_workspace_bytes.argtypes = [i32, i32, i32, i32, i32,
                                                    i32, i32]
     lib.wf_verify_attn_workspace_bytes.restype = sz
@@ -260,6 +264,27 @@ def wf_verify_attn(q, k_cache, v_cache, out, ctx_len, softmax_scale=None,
                             _dev(workspace, "workspace"), workspace.numel(),
                             _stream(stream))
     _check(st, "wf_verify_attn")
+    return out
+
+
+def wf_verify_attn_noalloc(q, k_cache, v_cache, out, ctx_len, softmax_scale=None,
+                           num_splits=0, stream=None):
+    """wf_verify_attn with the library's static device scratch instead of a
+    workspace: nothing is allocated (for graph capture and callers that
+    cannot allocate).  Calls that overlap in time on one GPU race."""
+    gamma, hq, dh = q.shape
+    hkv, cap, dh2 = k_cache.shape
+    if dh2 != dh or tuple(v_cache.shape) != tuple(k_cache.shape):
+        raise ValueError("cache shapes do not match q")
+    if tuple(out.shape) != tuple(q.shape) or out.dtype != q.dtype:
+        raise ValueError("out must match q in shape and dtype")
+    if softmax_scale is None:
+        softmax_scale = dh ** -0.5
+    st = lib.wf_verify_attn_noalloc(_dtype_code(q), _dev(q, "q"), _dev(k_cache, "k_cache"),
+                                    _dev(v_cache, "v_cache"), _dev(out, "out"), gamma,
+                                    int(ctx_len), cap, hq, hkv, dh, float(softmax_scale),
+                                    int(num_splits), _stream(stream))
+    _check(st, "wf_verify_attn_noalloc")
     return out
 
 

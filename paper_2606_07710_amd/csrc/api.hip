@@ -51,7 +51,7 @@ wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
 
 extern "C" {
 
-int32_t wf_abi_version(void) { return 6; }
+int32_t wf_abi_version(void) { return 7; }
 
 const char *wf_status_string(wf_status_t s) {
     switch (s) {
@@ -76,15 +76,16 @@ size_t wf_verify_attn_workspace_bytes(wf_dtype_t dt, int32_t gamma,
     return wf::attn_workspace_bytes(p, gamma, n_q_heads, head_dim);
 }
 
-namespace {
-wf_status_t verify_attn_common(wf_dtype_t dt, const void *q, const void *k_cache,
-                               const void *v_cache, void *out,
-                               const uint64_t *tree_mask, int32_t gamma,
-                               int32_t ctx_len, int32_t cap, int32_t n_q_heads,
-                               int32_t n_kv_heads, int32_t head_dim,
-                               float softmax_scale, int32_t num_splits,
-                               void *workspace, size_t workspace_bytes,
-                               void *stream) {
+}  // extern "C"
+
+namespace wf {
+// Host-side checks of a verify-attention call, everything but the
+// workspace; on WF_OK *plan holds the call's split plan.
+wf_status_t validate_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
+                                 const void *v_cache, const void *out, int32_t gamma,
+                                 int32_t ctx_len, int32_t cap, int32_t n_q_heads,
+                                 int32_t n_kv_heads, int32_t head_dim, float softmax_scale,
+                                 int32_t num_splits, AttnPlan *plan) {
     wf_status_t st = check_attn(dt, gamma, ctx_len, n_q_heads, n_kv_heads,
                                 head_dim, num_splits);
     if (st != WF_OK)
@@ -98,8 +99,28 @@ wf_status_t verify_attn_common(wf_dtype_t dt, const void *q, const void *k_cache
         return WF_ERR_INVALID_ARG;
     if (!std::isfinite(softmax_scale) || softmax_scale <= 0.f)
         return WF_ERR_INVALID_ARG;
-    const wf::AttnPlan p = wf::plan_attn(dt, gamma, ctx_len, n_q_heads,
-                                         n_kv_heads, head_dim, num_splits);
+    *plan = plan_attn(dt, gamma, ctx_len, n_q_heads, n_kv_heads, head_dim, num_splits);
+    return WF_OK;
+}
+}  // namespace wf
+
+extern "C" {
+
+namespace {
+wf_status_t verify_attn_common(wf_dtype_t dt, const void *q, const void *k_cache,
+                               const void *v_cache, void *out,
+                               const uint64_t *tree_mask, int32_t gamma,
+                               int32_t ctx_len, int32_t cap, int32_t n_q_heads,
+                               int32_t n_kv_heads, int32_t head_dim,
+                               float softmax_scale, int32_t num_splits,
+                               void *workspace, size_t workspace_bytes,
+                               void *stream) {
+    wf::AttnPlan p{};
+    const wf_status_t st = wf::validate_verify_attn(dt, q, k_cache, v_cache, out, gamma,
+                                                    ctx_len, cap, n_q_heads, n_kv_heads,
+                                                    head_dim, softmax_scale, num_splits, &p);
+    if (st != WF_OK)
+        return st;
     const size_t need = wf::attn_workspace_bytes(p, gamma, n_q_heads, head_dim);
     if (!workspace || workspace_bytes < need || !aligned16(workspace))
         return WF_ERR_WORKSPACE;

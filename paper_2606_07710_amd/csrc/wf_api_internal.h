@@ -36,6 +36,13 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
                    int n_kv_heads, int head_dim, int num_splits);
 size_t attn_workspace_bytes(const AttnPlan &p, int gamma, int n_q_heads,
                             int head_dim);
+// Host-side checks of a verify-attention call (api.hip), everything but the
+// workspace; on WF_OK *plan holds the split plan of the call.
+wf_status_t validate_verify_attn(wf_dtype_t dt, const void *q, const void *k_cache,
+                                 const void *v_cache, const void *out, int32_t gamma,
+                                 int32_t ctx_len, int32_t cap, int32_t n_q_heads,
+                                 int32_t n_kv_heads, int32_t head_dim, float softmax_scale,
+                                 int32_t num_splits, AttnPlan *plan);
 wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
                         const void *v_cache, void *out, int gamma, int ctx_len,
                         int cap, int n_q_heads, int n_kv_heads, int head_dim,

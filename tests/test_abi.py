@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert wf.abi_version() == 6
+    assert wf.abi_version() == 7
     assert wf.status_string(wf.WF_OK) == "ok"
     assert "workspace" in wf.status_string(wf.WF_ERR_WORKSPACE)
     assert wf.status_string(99) == "unknown status"
@@ -65,6 +65,31 @@ def _attn(**kw):
 ])
 def test_verify_attn_rejects(kw, status):
     assert _attn(**kw) == status
+
+
+def _attn_noalloc(**kw):
+    a = dict(dt=1, q=FAKE, k=FAKE, v=FAKE, out=FAKE, gamma=16, ctx=100,
+             cap=116, hq=32, hkv=8, dh=128, scale=0.088, splits=0)
+    a.update(kw)
+    return wf.lib.wf_verify_attn_noalloc(a["dt"], a["q"], a["k"], a["v"], a["out"],
+                                         a["gamma"], a["ctx"], a["cap"], a["hq"],
+                                         a["hkv"], a["dh"], a["scale"], a["splits"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), 1), (dict(gamma=65), 1), (dict(cap=115), 1), (dict(hq=30), 1),
+    (dict(dh=96), 2), (dict(q=ODD), 1), (dict(scale=0.0), 1), (dict(splits=5000), 1),
+    # partials beyond the static scratch: 64 rows x 256 heads x 64 splits
+    (dict(gamma=64, hq=256, ctx=4096, cap=4160, splits=64), 3),
+])
+def test_verify_attn_noalloc_rejects(kw, status):
+    assert _attn_noalloc(**kw) == status
+
+
+def test_noalloc_scratch_size_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define WF_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == wf.NOALLOC_SCRATCH_BYTES
 
 
 # every workspace starts with the same block of arrival counters
