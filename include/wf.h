@@ -82,13 +82,17 @@ typedef enum {
     WF_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad size or range  */
     WF_ERR_UNSUPPORTED = 2,   /* valid but not implemented (e.g. head_dim)    */
     WF_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required   */
-    WF_ERR_HIP = 4            /* the HIP runtime rejected a kernel launch     */
+    WF_ERR_HIP = 4,           /* the HIP runtime rejected a kernel launch     */
+    /* not statuses: they make every int32 value a valid wf_status_t, so a
+     * caller may pass any int (unknown codes have a status string too) */
+    WF_STATUS_RANGE_MIN_ = -2147483647 - 1,
+    WF_STATUS_RANGE_MAX_ = 2147483647
 } wf_status_t;
 
 typedef enum {
     WF_F32 = 0,               /* IEEE fp32 storage and arithmetic             */
     WF_BF16 = 1,              /* bf16 storage, fp32 accumulation              */
-    WF_BF16_TILED = 2         /* as WF_BF16, with the WEIGHT matrices (W_k,
+    WF_BF16_TILED = 2,        /* as WF_BF16, with the WEIGHT matrices (W_k,
                                  W_v, W_lm, the drafter layer's projections)
                                  in the tiled layout that wf_tile_weights
                                  writes; activations, norm gains, caches and
@@ -100,6 +104,10 @@ typedef enum {
                                  WF_ERR_UNSUPPORTED) and nowhere else
                                  (WF_ERR_INVALID_ARG).  Results are bit-for-bit
                                  those of WF_BF16 on the untiled weights.     */
+    /* not dtypes: every int32 value is a valid wf_dtype_t (an unknown code
+     * is rejected with WF_ERR_INVALID_ARG) */
+    WF_DTYPE_RANGE_MIN_ = -2147483647 - 1,
+    WF_DTYPE_RANGE_MAX_ = 2147483647
 } wf_dtype_t;
 
 /* Version of this ABI (bumped on any signature or semantic change). */
@@ -475,12 +483,14 @@ size_t wf_drafter_forward_workspace_bytes(wf_dtype_t dt,
 
 /* Lazy catch-up over a backlog of n_backlog tokens whose layer inputs are
  * r [n_backlog][hidden], starting at cache row pos: RMSNorm(r[t]) *
- * attn_norm and KV-only prefill for the whole backlog in one batch each
- * (cache rows pos .. pos+n_backlog-1), then the rest of the layer --
- * attention, W_o, the MLP -- for the last token only; out [hidden] is its
- * output.  The cache rows and out equal those of wf_drafter_forward over
- * the whole backlog (to rounding).  Limits as for wf_drafter_forward, with
- * 1 <= n_backlog <= 4096 and pos + n_backlog <= cap.
+ * attn_norm for the whole backlog in one batch and KV-only prefill in one
+ * batch per 4096 tokens (cache rows pos .. pos+n_backlog-1), then the rest
+ * of the layer -- attention, W_o, the MLP -- for the last token only;
+ * out [hidden] is its output.  The cache rows and out equal those of
+ * wf_drafter_forward over the whole backlog (to rounding).  Limits as for
+ * wf_drafter_forward, with 1 <= n_backlog <= 2^20 and pos + n_backlog <= cap,
+ * so any backlog wf_switch_commit hands out (up to the cache capacity) is
+ * accepted.
  * workspace >= wf_drafter_catchup_workspace_bytes(...) bytes. */
 wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer,
                                const void *r, int32_t n_backlog, int32_t pos,

@@ -42,7 +42,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "libwfref.so")
+# WFREF_LIB names another build of wfref.c (the sanitizer run of the tests)
+_LIB_PATH = os.environ.get("WFREF_LIB") or os.path.join(_HERE, "libwfref.so")
 _lib = None
 
 _CODES = {np.dtype(np.float32): 0, np.dtype(np.uint16): 1,

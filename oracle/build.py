@@ -11,16 +11,24 @@ SRC = os.path.join(HERE, "wfref.c")
 LIB = os.path.join(HERE, "libwfref.so")
 
 
-def build(verbose: bool = False) -> str:
-    """Compile the oracle; returns the path of the shared library."""
-    tmp = LIB + ".tmp"
+SAN_FLAGS = ["-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=undefined"]
+
+
+def build(verbose: bool = False, out: str = None, sanitize: bool = False) -> str:
+    """Compile the oracle; returns the path of the shared library.  With
+    sanitize=True the library is built with AddressSanitizer and
+    UndefinedBehaviorSanitizer (run it with gcc's libasan preloaded)."""
+    lib = out or LIB
+    tmp = lib + ".tmp"
     cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared",
-           "-Wall", "-Wextra", "-o", tmp, SRC, "-lm"]
+           "-Wall", "-Wextra"] + (SAN_FLAGS if sanitize else []) + \
+        ["-o", tmp, SRC, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

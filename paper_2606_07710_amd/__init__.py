@@ -13,7 +13,8 @@ import os
 import torch  # loaded first so libwf binds to the same HIP runtime as torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libwf.so")
+# WF_LIB names another build of the library (the host-sanitizer CPU run)
+LIB_PATH = os.environ.get("WF_LIB") or os.path.join(_HERE, "libwf.so")
 
 WF_OK, WF_ERR_INVALID_ARG, WF_ERR_UNSUPPORTED, WF_ERR_WORKSPACE, WF_ERR_HIP = range(5)
 WF_F32, WF_BF16, WF_BF16_TILED = 0, 1, 2

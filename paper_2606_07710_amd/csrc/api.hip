@@ -13,6 +13,7 @@ constexpr int kMaxGamma = 64;
 constexpr int kMaxQHeads = 256;
 constexpr int kMaxSplits = 1024;
 constexpr int kMaxPrefillTokens = 4096;
+constexpr int kMaxBacklog = 1 << 20;        // drafter catch-up, in 4096-token batches
 constexpr int kMaxLayers = 1024;
 constexpr int kMaxRouterHidden = 1 << 16;
 
@@ -60,6 +61,7 @@ const char *wf_status_string(wf_status_t s) {
     case WF_ERR_UNSUPPORTED: return "unsupported configuration";
     case WF_ERR_WORKSPACE: return "workspace missing or too small";
     case WF_ERR_HIP: return "HIP kernel launch failed";
+    default: break;
     }
     return "unknown status";
 }
@@ -470,12 +472,22 @@ wf_status_t wf_drafter_forward(wf_dtype_t dt, const wf_decoder_layer_t *layer, c
                                       dt == WF_BF16_TILED);
 }
 
+namespace {
+// Every KV-only prefill batch of a catch-up (full 4096-token batches and the
+// last, shorter one) fits the prefill plan.
+bool catchup_fits(int n, const wf_decoder_layer_t &L) {
+    const int full = std::min(n, wf::kCatchupChunk), tail = n % wf::kCatchupChunk;
+    return wf::prefill_fits(full, L.hidden, L.n_kv_heads, L.head_dim) &&
+           (tail == 0 || wf::prefill_fits(tail, L.hidden, L.n_kv_heads, L.head_dim));
+}
+}  // namespace
+
 size_t wf_drafter_catchup_workspace_bytes(wf_dtype_t dt, const wf_decoder_layer_t *layer,
                                           int32_t n_backlog, int32_t pos) {
-    if (n_backlog < 1 || n_backlog > kMaxPrefillTokens ||
+    if (n_backlog < 1 || n_backlog > kMaxBacklog ||
         check_drafter(dt, layer, pos, pos + n_backlog - 1, pos + n_backlog) != WF_OK)
         return 0;
-    if (!wf::prefill_fits(n_backlog, layer->hidden, layer->n_kv_heads, layer->head_dim))
+    if (!catchup_fits(n_backlog, *layer))
         return 0;
     return wf::drafter_catchup_workspace_bytes(*layer, n_backlog, pos);
 }
@@ -484,7 +496,7 @@ wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer, c
                                int32_t n_backlog, int32_t pos, void *k_cache, void *v_cache,
                                int32_t cap, void *out, void *workspace,
                                size_t workspace_bytes, void *stream) {
-    if (n_backlog < 1 || n_backlog > kMaxPrefillTokens)
+    if (n_backlog < 1 || n_backlog > kMaxBacklog)
         return WF_ERR_INVALID_ARG;
     const wf_status_t st = check_drafter(dt, layer, pos, pos + n_backlog - 1, cap);
     if (st != WF_OK)
@@ -492,7 +504,7 @@ wf_status_t wf_drafter_catchup(wf_dtype_t dt, const wf_decoder_layer_t *layer, c
     if (!r || !k_cache || !v_cache || !out || !aligned16(r) || !aligned16(k_cache) ||
         !aligned16(v_cache) || !aligned16(out))
         return WF_ERR_INVALID_ARG;
-    if (!wf::prefill_fits(n_backlog, layer->hidden, layer->n_kv_heads, layer->head_dim))
+    if (!catchup_fits(n_backlog, *layer))
         return WF_ERR_UNSUPPORTED;
     const size_t need = wf::drafter_catchup_workspace_bytes(*layer, n_backlog, pos);
     if (!workspace || workspace_bytes < need || !aligned16(workspace))

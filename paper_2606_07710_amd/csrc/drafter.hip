@@ -318,11 +318,17 @@ wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, i
         static_cast<char *>(workspace) + align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)));
     rmsnorm_bf16<<<n, kNormThreads, 0, stream>>>(rb, static_cast<const uint16_t *>(L.attn_norm),
                                                  L.rms_eps, xnb, d);
-    const wf_status_t st = launch_prefill(tiled ? WF_BF16_TILED : WF_BF16, xnb, L.w_k, L.w_v,
-                                          k_cache, v_cache, n, pos, cap, d, L.n_kv_heads,
-                                          L.head_dim, L.rope_base, workspace, stream);
-    if (st != WF_OK)
-        return st;
+    // the whole backlog's K/V in batches of at most kCatchupChunk tokens
+    // (one KV-only prefill each; a single batch for any backlog up to that)
+    for (int c0 = 0; c0 < n; c0 += kCatchupChunk) {
+        const int m = std::min(kCatchupChunk, n - c0);
+        const wf_status_t st = launch_prefill(tiled ? WF_BF16_TILED : WF_BF16,
+                                              xnb + (size_t)c0 * d, L.w_k, L.w_v, k_cache,
+                                              v_cache, m, pos + c0, cap, d, L.n_kv_heads,
+                                              L.head_dim, L.rope_base, workspace, stream);
+        if (st != WF_OK)
+            return st;
+    }
     return drafter_forward(L, rb + (size_t)(n - 1) * d, 1, pos + n - 1, k_cache, v_cache, cap,
                            out, workspace, stream, tiled, xnb + (size_t)(n - 1) * d);
 }

@@ -81,6 +81,9 @@ wf_status_t launch_router(wf_dtype_t dt, const void *h, const void *w1,
 
 // Drafter layer and lazy catch-up (drafter.hip); bf16 only, the weight
 // matrices row-major or (tiled) in 16x32 tiles.
+// Backlogs longer than this are caught up in several KV-only prefill
+// batches of at most this many tokens (the prefill's own limit).
+constexpr int kCatchupChunk = 4096;
 size_t drafter_forward_workspace_bytes(const wf_decoder_layer_t &L, int M, int pos);
 size_t drafter_catchup_workspace_bytes(const wf_decoder_layer_t &L, int n, int pos);
 wf_status_t launch_drafter_forward(const wf_decoder_layer_t &L, const void *r, int M, int pos,

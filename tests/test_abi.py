@@ -321,7 +321,11 @@ def test_drafter_rejects(fn, kw, lay, status):
 
 def test_drafter_token_limits():
     assert _drafter("wf_drafter_forward", n=65, cap=5000) == 1
-    assert _drafter("wf_drafter_catchup", n=4097, cap=9000) == 1
+    # the catch-up takes backlogs up to 2^20 tokens (KV-only prefill in
+    # 4096-token batches); one more is rejected before anything is launched
+    assert _drafter("wf_drafter_catchup", n=(1 << 20) + 1, pos=0, cap=(1 << 20) + 8) == 1
+    lay = _layer()
+    assert wf.lib.wf_drafter_catchup_workspace_bytes(1, ctypes.byref(lay), 4097, 4096) > 0
     lay = _layer()
     assert wf.lib.wf_drafter_forward_workspace_bytes(1, ctypes.byref(lay), 1, 4096) > COUNTER_BLOCK
     assert wf.lib.wf_drafter_catchup_workspace_bytes(1, ctypes.byref(lay), 80, 4096) > COUNTER_BLOCK

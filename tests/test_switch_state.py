@@ -2,6 +2,7 @@
 of Sec. 4): which backlog of the autoregressive drafter's KV cache is due
 after each verify round.  Checked against the scheme written out round by
 round, on random round sequences, with no GPU."""
+import ctypes
 import random
 
 import pytest
@@ -95,3 +96,27 @@ def test_rejects():
         wf.wf_switch_commit(s, 10, AR)         # sequence length past INT32_MAX
     assert wf.wf_switch_commit(s, 9, AR) == (2**31 - 10, 9)
     assert wf.lib.wf_switch_commit(None, 1, AR, None, None) == wf.WF_ERR_INVALID_ARG
+
+
+def _fake_layer(hidden=4096, hq=32, hkv=8, hd=128, inter=12288):
+    fake = 1 << 20                        # 16-byte aligned, never dereferenced
+    return wf.DecoderLayer(*([fake] * len(wf.DECODER_WEIGHTS)), hidden, hq, hkv, hd, inter,
+                           1e-6, 1e6)
+
+
+def test_a_long_lazy_backlog_is_accepted_by_the_catchup():
+    """Rounds on the diffusion drafter pile up a backlog far beyond one
+    KV-only prefill batch (4096 tokens); the switch back hands it out in one
+    piece, and the catch-up takes it (in 4096-token prefill batches)."""
+    s = wf.wf_switch_init(AR, 1, 100)
+    for _ in range(700):
+        assert wf.wf_switch_commit(s, 16, DIFF) == (100, 0)
+    start, count = wf.wf_switch_commit(s, 16, AR)
+    assert (start, count) == (100, 701 * 16) and count > 4096
+    layer = _fake_layer()
+    for code in (wf.WF_BF16, wf.WF_BF16_TILED):
+        need = int(wf.lib.wf_drafter_catchup_workspace_bytes(code, ctypes.byref(layer),
+                                                             count, start))
+        assert need >= count * 4096 * 2     # the normalised backlog is staged
+    assert int(wf.lib.wf_drafter_catchup_workspace_bytes(
+        wf.WF_BF16, ctypes.byref(layer), (1 << 20) + 1, 0)) == 0
