@@ -130,7 +130,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     // padded by 4 floats so the 16 rows of a wave's accumulator tile fall in
     // distinct banks.
     constexpr int OST = DH + 4;
-    constexpr int REGION_BYTES = ROWS_WG * OST * 4;
+    constexpr int REGION_BYTES = KS > 1 ? ROWS_WG * OST * 4 : 0;
     constexpr int MAX_RS = STAGE_BYTES > REGION_BYTES ? STAGE_BYTES : REGION_BYTES;
     // Streams 1..KS-1 hand their accumulators to stream 0 through NREG
     // regions: two (fewer merge rounds) when there are two or more such
@@ -515,12 +515,14 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
         l += __shfl_xor(l, 16, kWave);
         l += __shfl_xor(l, 32, kWave);
         lrow[nb] = l;
-        if (c4 == 0) {
+        if (KS > 1 && c4 == 0) {
             mls[stream][rgi * ROWS_W + nb * 16 + m16][0] = mref[nb];
             mls[stream][rgi * ROWS_W + nb * 16 + m16][1] = l;
         }
     }
-    __syncthreads();
+    // (one key stream: each row's state is complete in its wave's registers)
+    if constexpr (KS > 1)
+        __syncthreads();
 
     // ---- merge the KS streams of each row ------------------------------------
     // Stream s >= 1 adds its rescaled accumulator into region (s-1) % NREG in
@@ -531,6 +533,10 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     float fac[NBW];
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
+        if constexpr (KS == 1) {
+            fac[nb] = 1.f;               // a row without visible keys has o == 0
+            continue;
+        }
         const int r = rgi * ROWS_W + nb * 16 + m16;
         float mm = -INFINITY;
 #pragma unroll
@@ -586,7 +592,10 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             // the output is rounded to bf16 anyway
             dst[md * 4 + c4] = uint2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
         }
-        if (c4 == 0) {
+        if (KS == 1 && c4 == 0) {
+            a.ws_ml[pr * 2] = mref[nb];
+            a.ws_ml[pr * 2 + 1] = lrow[nb];
+        } else if (c4 == 0) {
             float mm = -INFINITY, ll = 0.f;
 #pragma unroll
             for (int st = 0; st < KS; ++st)
@@ -796,11 +805,17 @@ AttnPlan plan_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
         // at 64K keys with two 64-row ones; more rows, e.g. a draft tree's
         // 244: 64-row workgroups in several row groups, 26.1 against
         // 27.8 us at 8K keys with 128-row ones)
+        // (up to 64 rows: one key stream of four 16-row waves, 31.3 against
+        // 32.2 us with two streams at 32K keys; up to 32 rows: two streams
+        // and a three-stage ring, 13.5 against 14.9 us with four streams at
+        // 8K keys, 30.1 against 31.7 us at 32K keys for 16 rows)
         if (rows <= 16) {
-            p.nb = 1; p.rg = 1; p.ks = 4; p.nbuf = 2;
+            p.nb = 1; p.rg = 1; p.ks = 2; p.nbuf = 3;
         } else if (rows <= 32) {
-            p.nb = 1; p.rg = 2; p.ks = 4; p.nbuf = 2;
-        } else if (rows <= 64 || rows > 128) {
+            p.nb = 1; p.rg = 2; p.ks = 2; p.nbuf = 3;
+        } else if (rows <= 64) {
+            p.nb = 1; p.rg = 4; p.ks = 1; p.nbuf = 3;
+        } else if (rows > 128) {
             p.nb = 1; p.rg = 4; p.ks = 2; p.nbuf = 3;
         } else {
             p.nb = 2; p.rg = 4; p.ks = 2; p.nbuf = 3;
@@ -883,10 +898,12 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
         p.nbuf == NBUFV) {                                                            \
         attn_partial_bf16<DHV, NBV, RGV, KSV, NBUFV><<<grid, block, 0, stream>>>(a);  \
     } else
-        WF_ATTN_CASE(128, 1, 1, 4, 2) WF_ATTN_CASE(128, 1, 2, 4, 2)
-        WF_ATTN_CASE(128, 1, 4, 2, 3) WF_ATTN_CASE(128, 2, 4, 2, 3)
-        WF_ATTN_CASE(64, 1, 1, 4, 2) WF_ATTN_CASE(64, 1, 2, 4, 2)
-        WF_ATTN_CASE(64, 1, 4, 2, 3) WF_ATTN_CASE(64, 2, 4, 2, 3)
+        WF_ATTN_CASE(128, 1, 1, 2, 3) WF_ATTN_CASE(128, 1, 2, 2, 3)
+        WF_ATTN_CASE(128, 1, 4, 1, 3) WF_ATTN_CASE(128, 1, 4, 2, 3)
+        WF_ATTN_CASE(128, 2, 4, 2, 3)
+        WF_ATTN_CASE(64, 1, 1, 2, 3) WF_ATTN_CASE(64, 1, 2, 2, 3)
+        WF_ATTN_CASE(64, 1, 4, 1, 3) WF_ATTN_CASE(64, 1, 4, 2, 3)
+        WF_ATTN_CASE(64, 2, 4, 2, 3)
         { return WF_ERR_UNSUPPORTED; }
 #undef WF_ATTN_CASE
     } else {
