@@ -77,7 +77,12 @@ def parse():
                     help="cap on the layers the cpu baseline runs")
     ap.add_argument("--copy-probe-mib", type=int, default=1024,
                     help="size of the plain device copy run after timing "
-                         "(reference for HBM traffic counters); 0 = off")
+                         "(the known-size reference that scales the HBM "
+                         "traffic counters of a profiling run; not timed "
+                         "for the roofline); 0 = off")
+    ap.add_argument("--read-probe-mib", type=int, default=1024,
+                    help="buffer the streaming-read ceiling is measured on "
+                         "(larger than the 256 MB last-level cache); 0 = off")
     return ap.parse_args()
 
 
@@ -239,26 +244,68 @@ class Step:
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "verify_attn_8b_ctx32k_hbm_traffic.md")
 
 
+MFMA_PROFILE = os.path.join(ROOT, "profiles", "verify_step_8b_ctx32k_sq_counters.md")
+
+
+def profile_field(path, key, prefix):
+    """A value recorded in a committed counter summary (`prefix`_`key`: ...),
+    or None when the summary is missing or the kernel sources it names have
+    changed since the counters were taken (their SHA-256 is recorded)."""
+    import hashlib
+    try:
+        text = open(path).read()
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines()
+                  if line.startswith(prefix + "_"))
+    try:
+        h = hashlib.sha256()
+        for src in fields[prefix + "_sources"].split():
+            h.update(open(os.path.join(ROOT, src), "rb").read())
+        if h.hexdigest() != fields[prefix + "_sources_sha256"].strip():
+            return None
+        return fields[prefix + "_" + key].strip()
+    except (KeyError, OSError, ValueError):
+        return None
+
+
 def measured_traffic():
     """HBM bytes per wf_verify_attn call from the committed counter summary
     (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), or None when the
     summary is missing or the kernel sources changed since it was taken."""
-    import hashlib
-    try:
-        text = open(TRAFFIC_PROFILE).read()
-    except OSError:
-        return None
-    fields = dict(line.split(": ", 1) for line in text.splitlines()
-                  if line.startswith("traffic_"))
-    try:
-        h = hashlib.sha256()
-        for src in fields["traffic_sources"].split():
-            h.update(open(os.path.join(ROOT, src), "rb").read())
-        if h.hexdigest() != fields["traffic_sources_sha256"].strip():
-            return None
-        return int(fields["traffic_bytes_per_call"])
-    except (KeyError, OSError, ValueError):
-        return None
+    v = profile_field(TRAFFIC_PROFILE, "bytes_per_call", "traffic")
+    return int(v) if v is not None else None
+
+
+def measured_mfma_busy():
+    """MFMA busy fraction of attn_partial_bf16 (SQ_VALU_MFMA_BUSY_CYCLES over
+    GRBM_GUI_ACTIVE x SIMDs) from the committed counter summary, or None."""
+    v = profile_field(MFMA_PROFILE, "attn_partial_mfma_busy", "sq")
+    return float(v) if v is not None else None
+
+
+def read_ceiling(wf, dev, mib, reps=3):
+    """Best rate (GB/s) of the library's plain streaming-read probe over a
+    `mib` MiB buffer, at a few grid sizes; each launch reads the whole
+    buffer, which the 256 MB last-level cache cannot hold."""
+    import torch
+    buf = torch.ones(mib << 20, dtype=torch.uint8, device=dev)
+    rates = {}
+    for wgs in (1024, 2048, 4096, 8192):
+        sink = torch.empty(wgs * 4096, dtype=torch.uint8, device=dev)
+        wf.wf_read_probe(buf, sink, wgs)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            wf.wf_read_probe(buf, sink, wgs)
+        e1.record()
+        torch.cuda.synchronize()
+        rates[wgs] = reps * buf.numel() / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        del sink
+    del buf
+    return max(rates.values()), rates
 
 
 def cpu_baseline(w, layers, head, budget_s, max_layers=None, tree_mask=None):
@@ -719,8 +766,15 @@ def main():
         c1.record()
         torch.cuda.synchronize()
         copy_gbps = 4 * 2 * n / (c0.elapsed_time(c1) * 1e-3) / 1e9
-        log(f"device copy: {copy_gbps:.0f} GB/s (read + write)")
+        log(f"device copy: {copy_gbps:.0f} GB/s (read + write; counter reference only)")
         del src, dst
+
+    # ---- streaming-read ceiling (not timed with the step) -------------------
+    ceiling = None
+    if args.read_probe_mib:
+        ceiling, rates = read_ceiling(wf, dev, args.read_probe_mib)
+        log("read ceiling: " + ", ".join(f"{k} WGs {v:.0f}" for k, v in rates.items())
+            + f" GB/s -> {ceiling:.0f}")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -779,13 +833,18 @@ def main():
             "traffic": measured_traffic() if w.cfg == 3 else None,
             "bytes_per_launch": by["attn_per_layer"],
             "avg_launch_us": round(attn_avg_ms * 1e3, 2),
-            # a plain device copy in the same run (bytes read + written per
-            # second): what plain streaming reaches on this part
-            "copy_gbps": round(copy_gbps, 1) if copy_gbps else None,
-            "frac_of_copy": round(achieved / copy_gbps, 4) if copy_gbps else None,
-            # secondary: the call's flops against the dense bf16 MFMA peak
-            "mfma_util": round(w.flops()["attn_per_layer"] / (attn_avg_ms * 1e-3)
-                               / PEAK_BF16_FLOPS, 4),
+            # the best rate of a plain streaming read over a buffer larger
+            # than the last-level cache, measured in this run
+            "read_ceiling_gbps": round(ceiling, 1) if ceiling else None,
+            "frac_of_read_ceiling": round(achieved / ceiling, 4) if ceiling else None,
+            # secondary, derived (not a counter): the call's flops over its
+            # time, against the dense bf16 MFMA peak
+            "mfma_util_from_flops": round(w.flops()["attn_per_layer"] / (attn_avg_ms * 1e-3)
+                                          / PEAK_BF16_FLOPS, 4),
+            # counter-based: MFMA busy cycles of attn_partial_bf16 over its
+            # active cycles x SIMDs (committed rocprofv3 summary; None when
+            # the kernel sources changed since it was taken)
+            "mfma_busy_counter": measured_mfma_busy() if w.cfg == 3 else None,
         },
         "cpu_baseline": cpu,
     }

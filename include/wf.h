@@ -527,6 +527,20 @@ wf_status_t wf_tile_weights(const void *w, int32_t rows, int32_t cols,
                             void *tiled, size_t tiled_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
+ * wf_read_probe -- measurement support, not a step of the method: reads
+ * [src, src + bytes) once with a plain streaming kernel (workgroups x 256
+ * threads, each workgroup one contiguous share, 16-byte loads, 8 in flight
+ * per thread) and writes an XOR of what it read to sink, so the loads cannot
+ * be dropped.  Timing it over a buffer larger than the 256 MB last-level
+ * cache gives the HBM read rate a plain stream reaches, the ceiling the
+ * benchmark compares the kernels with.  src, sink: device, 16-byte aligned;
+ * bytes a positive multiple of 16; 1 <= workgroups <= 65536;
+ * sink_bytes >= workgroups * 4096 (else WF_ERR_WORKSPACE).
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_read_probe(const void *src, size_t bytes, void *sink, size_t sink_bytes,
+                          int32_t workgroups, void *stream);
+
+/* ------------------------------------------------------------------------
  * Lazy catch-up bookkeeping (Sec. 3.4 and its lazy catch-up study in
  * Sec. 4): a host-side record of how far the autoregressive drafter's KV
  * cache lags the committed sequence.  Only that drafter's cache can fall

@@ -30,6 +30,7 @@ EXPORTED_SYMBOLS = (
     "wf_drafter_catchup_workspace_bytes", "wf_switch_init", "wf_switch_commit",
     "wf_kv_only_prefill_layers", "wf_kv_only_prefill_layers_workspace_bytes",
     "wf_tiled_weight_bytes", "wf_tile_weights", "wf_verify_attn_noalloc",
+    "wf_read_probe",
 )
 NOALLOC_SCRATCH_BYTES = 32 << 20     # WF_NOALLOC_SCRATCH_BYTES
 WF_DRAFTER_AR, WF_DRAFTER_DIFFUSION = 0, 1
@@ -122,6 +123,8 @@ def _load():
     lib.wf_tiled_weight_bytes.restype = sz
     lib.wf_tile_weights.argtypes = [p, i32, i32, p, sz, p]
     lib.wf_tile_weights.restype = i32
+    lib.wf_read_probe.argtypes = [p, sz, p, sz, i32, p]
+    lib.wf_read_probe.restype = i32
     lib.wf_switch_init.argtypes = [p, i32, i32, i32]
     lib.wf_switch_init.restype = i32
     lib.wf_switch_commit.argtypes = [p, i32, i32, p, p]
@@ -536,6 +539,14 @@ def wf_drafter_catchup(layer, r, pos, k_cache, v_cache, out, workspace=None,
                                 _stream(stream))
     _check(st, "wf_drafter_catchup")
     return out
+
+
+def wf_read_probe(src, sink, workgroups, stream=None):
+    """Measurement support: one plain streaming read of the whole device
+    tensor src (sink: device tensor of at least workgroups * 4 KB)."""
+    _check(lib.wf_read_probe(_dev(src, "src"), src.numel() * src.element_size(),
+                             _dev(sink, "sink"), sink.numel() * sink.element_size(),
+                             int(workgroups), _stream(stream)), "wf_read_probe")
 
 
 def wf_switch_init(active, lazy, prompt_len) -> SwitchState:

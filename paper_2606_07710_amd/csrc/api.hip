@@ -52,7 +52,7 @@ wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
 
 extern "C" {
 
-int32_t wf_abi_version(void) { return 7; }
+int32_t wf_abi_version(void) { return 8; }
 
 const char *wf_status_string(wf_status_t s) {
     switch (s) {
@@ -560,6 +560,16 @@ wf_status_t wf_tile_weights(const void *w, int32_t rows, int32_t cols, void *til
     if (a < b + need && b < a + in_bytes)
         return WF_ERR_INVALID_ARG;                  // overlapping copies
     return wf::launch_tile_weights(w, rows, cols, tiled, static_cast<hipStream_t>(stream));
+}
+
+wf_status_t wf_read_probe(const void *src, size_t bytes, void *sink, size_t sink_bytes,
+                          int32_t workgroups, void *stream) {
+    if (!src || !sink || !aligned16(src) || !aligned16(sink) || bytes < 16 || bytes % 16 != 0 ||
+        workgroups < 1 || workgroups > 65536)
+        return WF_ERR_INVALID_ARG;
+    if (sink_bytes < (size_t)workgroups * 4096)
+        return WF_ERR_WORKSPACE;
+    return wf::launch_read_probe(src, bytes, sink, workgroups, static_cast<hipStream_t>(stream));
 }
 
 wf_status_t wf_switch_init(wf_switch_state_t *s, int32_t active, int32_t lazy,

@@ -124,6 +124,11 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            void *workspace, hipStream_t stream, int n_layers = 1,
                            long long x_ls = 0, long long w_ls = 0, long long c_ls = 0);
 
+// Streaming-read probe (probe.hip): `workgroups` workgroups of 256 threads
+// read [src, src + bytes) once; sink takes workgroups * 4 KB.
+wf_status_t launch_read_probe(const void *src, size_t bytes, void *sink, int workgroups,
+                              hipStream_t stream);
+
 // Tiled bf16 weights (16x32 tiles of 1 KB, one wave operand load each).
 size_t tiled_weight_bytes(int rows, int cols);
 wf_status_t launch_tile_weights(const void *w, int rows, int cols, void *tiled,

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert wf.abi_version() == 7
+    assert wf.abi_version() == 8
     assert wf.status_string(wf.WF_OK) == "ok"
     assert "workspace" in wf.status_string(wf.WF_ERR_WORKSPACE)
     assert wf.status_string(99) == "unknown status"
@@ -84,6 +84,16 @@ def _attn_noalloc(**kw):
 ])
 def test_verify_attn_noalloc_rejects(kw, status):
     assert _attn_noalloc(**kw) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    ((None, 1 << 20, FAKE, 1 << 20, 16), 1), ((FAKE, 1 << 20, None, 1 << 20, 16), 1),
+    ((ODD, 1 << 20, FAKE, 1 << 20, 16), 1), ((FAKE, 1000, FAKE, 1 << 20, 16), 1),
+    ((FAKE, 0, FAKE, 1 << 20, 16), 1), ((FAKE, 1 << 20, FAKE, 1 << 20, 0), 1),
+    ((FAKE, 1 << 20, FAKE, 1 << 20, 70000), 1), ((FAKE, 1 << 20, FAKE, 4095, 1), 3),
+])
+def test_read_probe_rejects(args, status):
+    assert wf.lib.wf_read_probe(*args, None) == status
 
 
 def test_noalloc_scratch_size_matches_header():
