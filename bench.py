@@ -180,15 +180,28 @@ class Step:
                              w.ctx_len, w.cap, w.n_kv_heads, w.head_dim,
                              ka.shape[0], ka[0].numel(), s)]
             return
-        self.lm_fn = wf.lib.wf_lmhead_accept_entropy
-        self.lm = [(lcode, P(self.head["h"]), P(w_lm), None,
-                    P(self.draft), w.gamma, w.hidden, w.vocab, self.tau, P(am),
-                    P(ent), P(acc), P(self.ws_lm), self.ws_lm.numel(), s)]
+        # (each LM-head entry is (C function, arguments...))
+        self.lm_fn = lambda fn, *a: fn(*a)
+        if rt:
+            # the neural policy in the LM-head pass: one call forms the
+            # logits' row states and the router's hidden layer from h
+            m = rt["w1"].shape[0]
+            w1 = rt.get("w1_tiled", rt["w1"])
+            self.lm = [(wf.lib.wf_lmhead_accept_route_neural, lcode, P(self.head["h"]),
+                        P(w_lm), P(self.draft), w.gamma, w.hidden, w.vocab, P(w1),
+                        P(rt["b1"]), P(rt["w2"]), P(rt["b2"]), m, 1.0, P(am), P(ent),
+                        P(acc), P(rt["delta"]), P(self.ws_lm), self.ws_lm.numel(), s)]
+            self.route = []
+        else:
+            self.lm = [(wf.lib.wf_lmhead_accept_entropy, lcode, P(self.head["h"]),
+                        P(w_lm), None, P(self.draft), w.gamma, w.hidden, w.vocab,
+                        self.tau, P(am), P(ent), P(acc), P(self.ws_lm),
+                        self.ws_lm.numel(), s)]
         if w.router_logits:
             am2, ent2, acc2 = self.lmouts[1]
-            self.lm.append((code, None, None, P(self.head["router_logits"]),
-                            P(self.draft), w.gamma, 0, w.vocab, self.tau,
-                            P(am2), P(ent2), P(acc2), P(self.ws_lm),
+            self.lm.append((wf.lib.wf_lmhead_accept_entropy, code, None, None,
+                            P(self.head["router_logits"]), P(self.draft), w.gamma, 0,
+                            w.vocab, self.tau, P(am2), P(ent2), P(acc2), P(self.ws_lm),
                             self.ws_lm.numel(), s))
 
     def run(self, check=False):
@@ -291,7 +304,7 @@ def read_ceiling(wf, dev, mib, reps=3):
     import torch
     buf = torch.ones(mib << 20, dtype=torch.uint8, device=dev)
     rates = {}
-    for wgs in (1024, 2048, 4096, 8192):
+    for wgs in (256, 512, 1024, 2048):
         sink = torch.empty(wgs * 4096, dtype=torch.uint8, device=dev)
         wf.wf_read_probe(buf, sink, wgs)
         e0 = torch.cuda.Event(enable_timing=True)
@@ -649,6 +662,15 @@ def main():
         router["route"] = torch.empty(1, dtype=torch.int32, device=dev)
         router["ws"] = wf.alloc_workspace(int(wf.lib.wf_router_workspace_bytes(
             1 if w.dtype == "bf16" else 0, w.gamma, w.hidden, m)), dev)
+        if not tree:
+            # chain/block rounds: the router rides in the LM-head call, its
+            # W1 in the LM head's layout
+            if w_lm_tiled is not None:
+                router["w1_tiled"] = wf.tile_weights(router["w1"])
+            code = (wf.WF_BF16_TILED if w_lm_tiled is not None else
+                    wf.WF_BF16 if w.dtype == "bf16" else wf.WF_F32)
+            ws_lm = wf.alloc_workspace(int(wf.lib.wf_lmhead_route_neural_workspace_bytes(
+                code, w.gamma, w.vocab, w.hidden, m)), dev)
     step = Step(w, layers, head, outs, lmouts, draft, tau, ws_attn, ws_pre,
                 ws_lm, wf, tree, router, pre_stack, w_lm_tiled)
     stream = torch.cuda.current_stream()

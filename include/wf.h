@@ -427,6 +427,41 @@ size_t wf_router_workspace_bytes(wf_dtype_t dt, int32_t gamma, int32_t d,
                                  int32_t m);
 
 /* ------------------------------------------------------------------------
+ * wf_lmhead_accept_route_neural -- the LM-head call of a chain/block round
+ * (wf_lmhead_accept_entropy: argmax, entropy, greedy acceptance) with the
+ * neural routing policy of Sec. 3.3.2 in place of the entropy rule: both
+ * read the same final hidden states h, so the router's hidden layer W1 h is
+ * formed in the same pass as the logits -- W1's m rows stream after the
+ * vocabulary as extra 16-row blocks of the LM-head kernel -- and the finish
+ * forms delta[r] = w2 . GELU(W1 h[r] + b1) + b2 (exact erf GELU) for every
+ * row and routes on the final accepted row n: accept_out[2] = delta[n] >
+ * tau_neural (strict), so routing adds no launch of its own.
+ *
+ * Arguments as wf_lmhead_accept_entropy (h, w_lm, draft, gamma, d, vocab,
+ * argmax_out, entropy_out, accept_out; no logits-only mode) and as
+ * wf_router_neural (w1 [m][d] in the layout dt names for the weights -- tiled
+ * for WF_BF16_TILED, like w_lm -- b1, w2 [m], b2 [1] in the activations'
+ * storage; delta_out [gamma] fp32).  The pass carries the router for bf16
+ * weights with gamma <= 16, d in {4096, 5120} and m % 16 == 0; other shapes
+ * run the LM head and then wf_router_neural's kernels on row n (not for
+ * WF_BF16_TILED: WF_ERR_UNSUPPORTED).
+ * workspace >= wf_lmhead_route_neural_workspace_bytes(...) bytes, zeroed
+ * before first use (as every workspace).
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_lmhead_accept_route_neural(wf_dtype_t dt, const void *h, const void *w_lm,
+                                          const int32_t *draft, int32_t gamma, int32_t d,
+                                          int32_t vocab, const void *w1, const void *b1,
+                                          const void *w2, const void *b2, int32_t m,
+                                          float tau_neural, int32_t *argmax_out,
+                                          float *entropy_out, int32_t *accept_out,
+                                          float *delta_out, void *workspace,
+                                          size_t workspace_bytes, void *stream);
+
+/* Workspace for wf_lmhead_accept_route_neural (0 for invalid arguments). */
+size_t wf_lmhead_route_neural_workspace_bytes(wf_dtype_t dt, int32_t gamma, int32_t vocab,
+                                              int32_t d, int32_t m);
+
+/* ------------------------------------------------------------------------
  * Drafter layer and lazy catch-up (Sec. 3.4: "Lazy Catch-up" defers the
  * inactive drafter's cache updates until the router switches to it, then
  * processes the backlog in one batch; "KV-only Prefill" forms only the
@@ -529,9 +564,9 @@ wf_status_t wf_tile_weights(const void *w, int32_t rows, int32_t cols,
 /* ------------------------------------------------------------------------
  * wf_read_probe -- measurement support, not a step of the method: reads
  * [src, src + bytes) once with a plain streaming kernel (workgroups x 256
- * threads, each workgroup one contiguous share, 16-byte loads, 8 in flight
- * per thread) and writes an XOR of what it read to sink, so the loads cannot
- * be dropped.  Timing it over a buffer larger than the 256 MB last-level
+ * threads striding through the buffer together, 32 KB per workgroup and
+ * round, 16-byte loads, 8 in flight per thread) and writes an XOR of what it
+ * read to sink, so the loads cannot be dropped.  Timing it over a buffer larger than the 256 MB last-level
  * cache gives the HBM read rate a plain stream reaches, the ceiling the
  * benchmark compares the kernels with.  src, sink: device, 16-byte aligned;
  * bytes a positive multiple of 16; 1 <= workgroups <= 65536;

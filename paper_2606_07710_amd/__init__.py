@@ -30,7 +30,8 @@ EXPORTED_SYMBOLS = (
     "wf_drafter_catchup_workspace_bytes", "wf_switch_init", "wf_switch_commit",
     "wf_kv_only_prefill_layers", "wf_kv_only_prefill_layers_workspace_bytes",
     "wf_tiled_weight_bytes", "wf_tile_weights", "wf_verify_attn_noalloc",
-    "wf_read_probe",
+    "wf_read_probe", "wf_lmhead_accept_route_neural",
+    "wf_lmhead_route_neural_workspace_bytes",
 )
 NOALLOC_SCRATCH_BYTES = 32 << 20     # WF_NOALLOC_SCRATCH_BYTES
 WF_DRAFTER_AR, WF_DRAFTER_DIFFUSION = 0, 1
@@ -123,6 +124,11 @@ def _load():
     lib.wf_tiled_weight_bytes.restype = sz
     lib.wf_tile_weights.argtypes = [p, i32, i32, p, sz, p]
     lib.wf_tile_weights.restype = i32
+    lib.wf_lmhead_accept_route_neural.argtypes = [i32, p, p, p, i32, i32, i32, p, p, p, p,
+                                                  i32, f32, p, p, p, p, p, sz, p]
+    lib.wf_lmhead_accept_route_neural.restype = i32
+    lib.wf_lmhead_route_neural_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
+    lib.wf_lmhead_route_neural_workspace_bytes.restype = sz
     lib.wf_read_probe.argtypes = [p, sz, p, sz, i32, p]
     lib.wf_read_probe.restype = i32
     lib.wf_switch_init.argtypes = [p, i32, i32, i32]
@@ -404,6 +410,29 @@ def wf_verify_attn_tree(q, k_cache, v_cache, out, ctx_len, tree_mask,
                                  workspace.numel(), _stream(stream))
     _check(st, "wf_verify_attn_tree")
     return out
+
+
+def wf_lmhead_accept_route_neural(h, w_lm, draft, w1, b1, w2, b2, tau_neural, argmax_out,
+                                  entropy_out, accept_out, delta_out, workspace=None,
+                                  stream=None):
+    """h [gamma][d]; w_lm [vocab][d] and w1 [m][d] (both tiled or both
+    row-major); b1, w2 [m], b2 [1]; draft [gamma-1] int32 (None when gamma
+    == 1); outputs int32 [gamma], fp32 [gamma], int32 [3] (route: the neural
+    policy), fp32 [gamma] (predicted gain per row)."""
+    gamma, d = h.shape
+    vocab = w_lm.shape[0]
+    m = w1.shape[0]
+    code = _weight_code(h, w_lm, w1)
+    need = int(lib.wf_lmhead_route_neural_workspace_bytes(code, gamma, vocab, d, m))
+    if workspace is None:
+        workspace = alloc_workspace(need, h.device)
+    st = lib.wf_lmhead_accept_route_neural(
+        code, _dev(h, "h"), _dev(w_lm, "w_lm"), _dev(draft, "draft"), gamma, d, vocab,
+        _dev(w1, "w1"), _dev(b1, "b1"), _dev(w2, "w2"), _dev(b2, "b2"), m, float(tau_neural),
+        _dev(argmax_out, "argmax_out"), _dev(entropy_out, "entropy_out"),
+        _dev(accept_out, "accept_out"), _dev(delta_out, "delta_out"),
+        _dev(workspace, "workspace"), workspace.numel(), _stream(stream))
+    _check(st, "wf_lmhead_accept_route_neural")
 
 
 def wf_lmhead_accept_tree(h, w_lm, logits, tokens, parents, tau, argmax_out,

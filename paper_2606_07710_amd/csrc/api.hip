@@ -52,7 +52,7 @@ wf_status_t check_attn(wf_dtype_t dt, int gamma, int ctx_len, int n_q_heads,
 
 extern "C" {
 
-int32_t wf_abi_version(void) { return 8; }
+int32_t wf_abi_version(void) { return 9; }
 
 const char *wf_status_string(wf_status_t s) {
     switch (s) {
@@ -370,6 +370,66 @@ wf_status_t wf_lmhead_accept_tree(wf_dtype_t dt, const void *h,
                              vocab, tau_entropy, argmax_out, entropy_out,
                              accept_out, path_out, workspace,
                              static_cast<hipStream_t>(stream));
+}
+
+namespace {
+size_t route_neural_ws(wf_dtype_t dt, int gamma, int vocab, int d, int m) {
+    if (wf::lmhead_router_fusable(dt, gamma, d, m))
+        return wf::lmhead_router_workspace_bytes(gamma, vocab, m);
+    return std::max(wf::lmhead_workspace_bytes(gamma, vocab),
+                    wf::router_workspace_bytes(storage(dt), gamma, d, m));
+}
+}  // namespace
+
+size_t wf_lmhead_route_neural_workspace_bytes(wf_dtype_t dt, int32_t gamma, int32_t vocab,
+                                              int32_t d, int32_t m) {
+    if (!weight_dtype_ok(dt) || gamma < 1 || gamma > kMaxGamma || vocab < 1 ||
+        vocab > (1 << 30) || d < 1 || m < 1 || m > kMaxRouterHidden)
+        return 0;
+    return route_neural_ws(dt, gamma, vocab, d, m);
+}
+
+wf_status_t wf_lmhead_accept_route_neural(wf_dtype_t dt, const void *h, const void *w_lm,
+                                          const int32_t *draft, int32_t gamma, int32_t d,
+                                          int32_t vocab, const void *w1, const void *b1,
+                                          const void *w2, const void *b2, int32_t m,
+                                          float tau_neural, int32_t *argmax_out,
+                                          float *entropy_out, int32_t *accept_out,
+                                          float *delta_out, void *workspace,
+                                          size_t workspace_bytes, void *stream) {
+    if (m < 1 || m > kMaxRouterHidden || !w1 || !b1 || !w2 || !b2 || !delta_out ||
+        !aligned16(w1))
+        return WF_ERR_INVALID_ARG;
+    // the LM-head checks, with a workspace large enough for either schedule
+    // (they are repeated below with the size this call needs)
+    wf_status_t st = check_lmhead(dt, h, w_lm, nullptr, gamma, d, vocab, tau_neural,
+                                  argmax_out, entropy_out, accept_out, workspace,
+                                  ~(size_t)0);
+    if (st != WF_OK)
+        return st;
+    if (gamma > 1 && !draft)
+        return WF_ERR_INVALID_ARG;
+    if (is_bf16(dt) && m % 16 != 0)
+        return WF_ERR_UNSUPPORTED;
+    if (!workspace || workspace_bytes < route_neural_ws(dt, gamma, vocab, d, m) ||
+        !aligned16(workspace))
+        return WF_ERR_WORKSPACE;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (wf::lmhead_router_fusable(dt, gamma, d, m)) {
+        const wf::LmRouter r{w1, b1, w2, b2, m, tau_neural, delta_out};
+        return wf::launch_lmhead(dt, h, w_lm, nullptr, draft, nullptr, gamma, d, vocab, 0.f,
+                                 argmax_out, entropy_out, accept_out, nullptr, workspace, s, &r);
+    }
+    // other shapes: the LM head, then the separate router on row n (its
+    // route replaces the entropy rule's in accept_out[2])
+    if (dt == WF_BF16_TILED)
+        return WF_ERR_UNSUPPORTED;
+    st = wf::launch_lmhead(dt, h, w_lm, nullptr, draft, nullptr, gamma, d, vocab, 0.f,
+                           argmax_out, entropy_out, accept_out, nullptr, workspace, s);
+    if (st != WF_OK)
+        return st;
+    return wf::launch_router(dt, h, w1, b1, w2, b2, accept_out, gamma, d, m, tau_neural,
+                             delta_out, accept_out + 2, workspace, s);
 }
 
 namespace {

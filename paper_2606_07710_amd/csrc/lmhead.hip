@@ -72,7 +72,22 @@ struct LmFinish {
     int32_t *accept_out;
     int gamma, n_tiles;
     float tau;
+    // Neural routing policy folded into the pass (nullptr w1: the entropy
+    // rule).  W1 [m][d] streams as m/16 extra 16-row blocks after the
+    // vocabulary; their "logits" z = W1 h go to zr [gamma][m], and the
+    // finish forms delta[r] = w2 . GELU(z[r] + b1) + b2 and routes on
+    // delta[n] > tau_neural.
+    const uint16_t *w1;
+    const uint16_t *b1, *w2, *b2;   // bf16
+    float *zr;
+    float *delta_out;
+    int m;
+    float tau_neural;
 };
+
+__device__ __forceinline__ float gelu_erf(float x) {
+    return 0.5f * x * (1.f + erff(x * 0.70710678118654752f));
+}
 
 // Greedy acceptance on a draft tree, run by the last row workgroup once
 // every row's argmax is out.  Node j (one lane each, gamma <= 64) walks its
@@ -151,6 +166,27 @@ __global__ __launch_bounds__(kFinishThreads) void lm_finish_rows(LmFinish f) {
         f.argmax_out[r] = m.a;
         f.entropy_out[r] = state_entropy(m);
     }
+    if (f.w1) {
+        // delta[r] = b2 + sum_u w2[u] GELU(z[r][u] + b1[u]): thread t takes
+        // units t, t + 256, ... in order, then a fixed butterfly and the
+        // waves in order
+        __shared__ float dsum[kFinishThreads / kWave];
+        float acc = 0.f;
+        for (int u = threadIdx.x; u < f.m; u += kFinishThreads)
+            acc = fmaf(bf16_to_f32(f.w2[u]),
+                       gelu_erf(f.zr[(size_t)r * f.m + u] + bf16_to_f32(f.b1[u])), acc);
+        acc = wave_sum(acc);
+        if (lane == 0)
+            dsum[wave] = acc;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            float dl = bf16_to_f32(f.b2[0]);
+#pragma unroll
+            for (int w = 0; w < kFinishThreads / kWave; ++w)
+                dl += dsum[w];
+            f.delta_out[r] = dl;
+        }
+    }
     if (!arrive_last(f.fcnt, (unsigned)f.gamma))
         return;
     if (f.parents) {
@@ -163,7 +199,8 @@ __global__ __launch_bounds__(kFinishThreads) void lm_finish_rows(LmFinish f) {
             ++n;
         f.accept_out[0] = n;
         f.accept_out[1] = f.argmax_out[n];
-        f.accept_out[2] = (f.entropy_out[n] > f.tau) ? 1 : 0;
+        f.accept_out[2] = f.w1 ? (f.delta_out[n] > f.tau_neural ? 1 : 0)
+                               : (f.entropy_out[n] > f.tau ? 1 : 0);
         *f.fcnt = 0u;
     }
 }
@@ -299,7 +336,8 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
     const int m16 = lane & 15;
     const int c4 = lane >> 4;
 
-    const int nblk = (vocab + 15) / 16;
+    const int nblk_v = (vocab + 15) / 16;
+    const int nblk = nblk_v + (f.w1 ? f.m / 16 : 0);   // + the router's W1 blocks
     // block j of this workgroup (j = kLmMB * t + mb) is blockIdx.x + G*j
     const int GB = gridDim.x;
     const int nmine = (nblk - (int)blockIdx.x + GB - 1) / GB;
@@ -321,11 +359,18 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
     const int cs = tiled ? 512 : 32;               // elements between chunks
     const int last_blk = (int)blockIdx.x + GB * (nmine - 1);
     auto wrow = [&](int t, int mb) {
-        const int blk = min((int)blockIdx.x + GB * (kLmMB * t + mb), last_blk);
+        int blk = min((int)blockIdx.x + GB * (kLmMB * t + mb), last_blk);
+        const uint16_t *base = w;
+        int rows = vocab;
+        if (blk >= nblk_v) {                       // a router block: W1 rows
+            blk -= nblk_v;
+            base = f.w1;
+            rows = f.m;
+        }
         if (tiled)
-            return w + ((size_t)blk * (D / 32) + wave * CPW) * 512 + lane * 8;
-        const int row = min(blk * 16 + m16, vocab - 1);
-        return w + (size_t)row * D + wave * CPW * 32 + c4 * 8;
+            return base + ((size_t)blk * (D / 32) + wave * CPW) * 512 + lane * 8;
+        const int row = min(blk * 16 + m16, rows - 1);
+        return base + (size_t)row * D + wave * CPW * 32 + c4 * 8;
     };
 
     bf16x8 wb[P][kLmMB];
@@ -383,7 +428,8 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
         const int j = kLmMB * t + lane / 16;
         const int blk = (int)blockIdx.x + GB * j;
         const int v = blk * 16 + (lane & 15);
-        const bool valid = j < nmine && v < vocab;
+        const bool valid = j < nmine && blk < nblk_v && v < vocab;
+        const bool hidden = j < nmine && blk >= nblk_v;   // router unit v - 16 nblk_v
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
             const int r = wave + kLmWaves * k;
@@ -392,6 +438,8 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
 #pragma unroll
                 for (int ww = 1; ww < kLmWaves; ++ww)
                     z += zs[buf][ww][r][lane];
+                if (hidden)
+                    f.zr[(size_t)r * f.m + (v - 16 * nblk_v)] = z;
                 RowState st = valid ? state_single(z, v) : state_empty();
                 st = wave_merge(st);
                 run[k] = state_merge(run[k], st);
@@ -678,12 +726,23 @@ size_t lmhead_workspace_bytes(int gamma, int vocab) {
 }
 
 
+bool lmhead_router_fusable(wf_dtype_t dt, int gamma, int d, int m) {
+    return (dt == WF_BF16 || dt == WF_BF16_TILED) && gamma <= 16 && (d == 4096 || d == 5120) &&
+           m >= 16 && m % 16 == 0;
+}
+
+size_t lmhead_router_workspace_bytes(int gamma, int vocab, int m) {
+    return lmhead_workspace_bytes(gamma, vocab) + (size_t)gamma * m * sizeof(float);
+}
+
 wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
                           const float *logits, const int32_t *draft,
                           const int32_t *parents, int gamma, int d, int vocab,
                           float tau, int32_t *argmax_out, float *entropy_out,
                           int32_t *accept_out, int32_t *path_out,
-                          void *workspace, hipStream_t stream) {
+                          void *workspace, hipStream_t stream, const LmRouter *router) {
+    if (router && (logits || parents || !lmhead_router_fusable(dt, gamma, d, router->m)))
+        return WF_ERR_UNSUPPORTED;
     const int tiled = dt == WF_BF16_TILED ? 1 : 0;
     if (tiled)
         dt = WF_BF16;
@@ -699,6 +758,22 @@ wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
     f.accept_out = accept_out;
     f.gamma = gamma;
     f.tau = tau;
+    f.w1 = nullptr;
+    f.b1 = f.w2 = f.b2 = nullptr;
+    f.zr = nullptr;
+    f.delta_out = nullptr;
+    f.m = 0;
+    f.tau_neural = 0.f;
+    if (router) {
+        f.w1 = static_cast<const uint16_t *>(router->w1);
+        f.b1 = static_cast<const uint16_t *>(router->b1);
+        f.w2 = static_cast<const uint16_t *>(router->w2);
+        f.b2 = static_cast<const uint16_t *>(router->b2);
+        f.m = router->m;
+        f.tau_neural = router->tau;
+        f.delta_out = router->delta_out;
+        f.zr = reinterpret_cast<float *>(ws + lmhead_workspace_bytes(gamma, vocab));
+    }
     if (logits) {
         f.n_tiles = cdiv(vocab, kLogitsTile);
         lm_tiles_logits<<<f.n_tiles, 256, 0, stream>>>(logits, f, vocab);

@@ -50,15 +50,27 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
                         const AttnPlan &p, void *workspace, hipStream_t stream);
 
 size_t lmhead_workspace_bytes(int gamma, int vocab);
+// The neural routing policy folded into the LM-head pass (bf16 weights in
+// the LM head's layout; b1, w2, b2 bf16): route = delta[n] > tau.
+struct LmRouter {
+    const void *w1, *b1, *w2, *b2;
+    int m;
+    float tau;
+    float *delta_out;
+};
+// Shapes whose persistent LM-head kernel carries the router's W1 blocks.
+bool lmhead_router_fusable(wf_dtype_t dt, int gamma, int d, int m);
+size_t lmhead_router_workspace_bytes(int gamma, int vocab, int m);
 // Chain mode: draft [gamma-1], parents == path_out == nullptr, accept_out
 // [3].  Tree mode: draft = node tokens [gamma], parents [gamma], accept_out
-// [4], path_out [gamma].
+// [4], path_out [gamma].  router: chain mode on a fusable shape only.
 wf_status_t launch_lmhead(wf_dtype_t dt, const void *h, const void *w_lm,
                           const float *logits, const int32_t *draft,
                           const int32_t *parents, int gamma, int d, int vocab,
                           float tau, int32_t *argmax_out, float *entropy_out,
                           int32_t *accept_out, int32_t *path_out,
-                          void *workspace, hipStream_t stream);
+                          void *workspace, hipStream_t stream,
+                          const LmRouter *router = nullptr);
 
 // Skinny linear layer (gemv.hip): zpart[k][f][r] = sum over the k-th input
 // slice of W[f] . x[r] for rows <= 64, features n_a + n_b (a multiple of

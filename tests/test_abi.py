@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert wf.abi_version() == 8
+    assert wf.abi_version() == 9
     assert wf.status_string(wf.WF_OK) == "ok"
     assert "workspace" in wf.status_string(wf.WF_ERR_WORKSPACE)
     assert wf.status_string(99) == "unknown status"
@@ -94,6 +94,34 @@ def test_verify_attn_noalloc_rejects(kw, status):
 ])
 def test_read_probe_rejects(args, status):
     assert wf.lib.wf_read_probe(*args, None) == status
+
+
+def _route(**kw):
+    a = dict(dt=1, h=FAKE, w=FAKE, draft=FAKE, gamma=16, d=4096, vocab=151936, w1=FAKE,
+             b1=FAKE, w2=FAKE, b2=FAKE, m=512, tau=0.5, am=FAKE, ent=FAKE, acc=FAKE,
+             delta=FAKE, ws=FAKE, ws_bytes=1 << 34)
+    a.update(kw)
+    return wf.lib.wf_lmhead_accept_route_neural(
+        a["dt"], a["h"], a["w"], a["draft"], a["gamma"], a["d"], a["vocab"], a["w1"], a["b1"],
+        a["w2"], a["b2"], a["m"], a["tau"], a["am"], a["ent"], a["acc"], a["delta"], a["ws"],
+        a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(w1=None), 1), (dict(b2=None), 1), (dict(delta=None), 1), (dict(w1=ODD), 1),
+    (dict(m=0), 1), (dict(m=70000), 1), (dict(draft=None), 1), (dict(gamma=65), 1),
+    (dict(tau=float("nan")), 1), (dict(m=500), 2), (dict(ws=None), 3), (dict(ws_bytes=4096), 3),
+    (dict(dt=2, gamma=24, d=512), 2),      # tiled weights outside the fused shapes
+])
+def test_route_neural_rejects(kw, status):
+    assert _route(**kw) == status
+
+
+def test_route_neural_workspace_query():
+    fused = wf.lib.wf_lmhead_route_neural_workspace_bytes(2, 16, 151936, 4096, 512)
+    assert fused == wf.wf_lmhead_workspace_bytes(16, 151936) + 16 * 512 * 4
+    assert wf.lib.wf_lmhead_route_neural_workspace_bytes(1, 24, 5000, 512, 64) > 0
+    assert wf.lib.wf_lmhead_route_neural_workspace_bytes(1, 0, 5000, 512, 64) == 0
 
 
 def test_noalloc_scratch_size_matches_header():
