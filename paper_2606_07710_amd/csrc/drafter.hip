@@ -17,6 +17,13 @@
 //
 // Activations are rounded to bf16 between the steps, as a bf16 model stores
 // them; every sum runs in fp32 in a fixed order.
+//
+// For a single token (the catch-up's last) each projection carries its
+// epilogue instead: q = RoPE(Wq xn) on the KV-only prefill kernel (its
+// split-K exchange tree spreads the 32 MB over the chip), h1 = r + Wo a and
+// out = h1 + Wd act in one kernel each, and [Wg; Wu] with the MLP's RMSNorm
+// folded into its loads and SwiGLU into its epilogue -- 8 launches per
+// catch-up instead of 13.
 #include <cmath>
 
 #include "wf_api_internal.h"
@@ -260,6 +267,27 @@ wf_status_t drafter_forward(const wf_decoder_layer_t &L, const uint16_t *rb, int
                             L.n_kv_heads, L.head_dim, L.rope_base, workspace, stream);
         if (st != WF_OK)
             return st;
+    }
+    if (M == 1) {
+        // One token (the catch-up's last): every projection carries its
+        // epilogue -- RoPE, a residual, or the MLP's RMSNorm and SwiGLU --
+        // so the layer is five launches after the K/V: W_q, attention (two),
+        // W_o, [W_gate; W_up], W_down.
+        if ((st = launch_q_rope(xn, W(L.w_q), q, d, L.n_q_heads, L.head_dim, pos,
+                                L.rope_base, workspace, stream, tiled)) != WF_OK)
+            return st;
+        st = launch_attn(WF_BF16, q, k_cache, v_cache, a, 1, pos, cap, L.n_q_heads,
+                         L.n_kv_heads, L.head_dim, (float)(1.0 / std::sqrt((double)L.head_dim)),
+                         nullptr, o.plan, workspace, stream);
+        if (st != WF_OK)
+            return st;
+        if ((st = launch_linear_resid(a, W(L.w_o), rb, qd, d, h1, stream, tiled)) != WF_OK)
+            return st;
+        if ((st = launch_linear_norm_swiglu(h1, W(L.mlp_norm), L.rms_eps, W(L.w_gate),
+                                            W(L.w_up), d, I, act, stream, tiled)) != WF_OK)
+            return st;
+        return launch_linear_resid(act, W(L.w_down), h1, I, d, static_cast<uint16_t *>(out),
+                                   stream, tiled);
     }
     // q = RoPE(Wq xn)
     if ((st = launch_linear_partial(xn, W(L.w_q), nullptr, qd, 0, M, d, zp, stream, tiled)) != WF_OK)

@@ -100,9 +100,191 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     }
 }
 
+// Skinny linear layer with its epilogue in the same kernel, for a single
+// token (one row): workgroup t owns one or two 16-feature blocks and the
+// whole input dimension, so no partial sums leave the workgroup.  The 8
+// waves take interleaved 32-wide chunks (all loads of a batch issued before
+// its first MFMA), their sums meet in LDS in wave order, and the epilogue
+// writes bf16 outputs:
+//   kEpiResid   y = res + W x                      (block t)
+//   kEpiSwiglu  act = SiLU(Wg x') * (Wu x')       (gate block t, up block t),
+//               x' = RMSNorm(x) * gain, folded in: W (x * gain) is formed from
+//               x * gain in bf16 and scaled by the row's 1/rms, whose sum of
+//               squares the workgroup forms from the same loads of x.
+enum EpiMode { kEpiResid = 0, kEpiSwiglu = 1 };
+
+struct EpiParams {
+    const uint16_t *x;      // [k_in] (kEpiSwiglu: the un-normalised row)
+    const uint16_t *w_a;    // blocks A
+    const uint16_t *w_b;    // kEpiSwiglu: the up projection
+    const uint16_t *res;    // kEpiResid: [n_out]
+    const uint16_t *gain;   // kEpiSwiglu: RMSNorm gains [k_in]
+    uint16_t *y;            // [n_out]
+    float eps;
+    int k_in, n_out, tiled;
+};
+
+template <int MODE>
+__global__ __launch_bounds__(kGemvWaves * kWave) void linear_epi_bf16(EpiParams a) {
+    constexpr int NBLK = MODE == kEpiResid ? 1 : 2;
+    __shared__ float zs[kGemvWaves][16 * NBLK];
+    __shared__ float sq[kGemvWaves];
+    const int wave = wave_id();
+    const int lane = threadIdx.x % kWave;
+    const int m16 = lane & 15;
+    const int c4 = lane >> 4;
+    const int n_c = a.k_in / 32;
+
+    // blocks of this workgroup and their matrices
+    int blk[NBLK];
+    const uint16_t *wm[NBLK];
+    if constexpr (MODE == kEpiResid) {
+        blk[0] = blockIdx.x;
+        wm[0] = a.w_a;
+    } else {
+        blk[0] = blk[1] = blockIdx.x;
+        wm[0] = a.w_a;
+        wm[1] = a.w_b;
+    }
+    const uint16_t *wp[NBLK];
+    int wstep;
+#pragma unroll
+    for (int j = 0; j < NBLK; ++j)
+        wp[j] = a.tiled ? wm[j] + (size_t)blk[j] * n_c * 512 + lane * 8
+                        : wm[j] + (size_t)(16 * blk[j] + m16) * a.k_in + c4 * 8;
+    wstep = a.tiled ? 512 : 32;
+    const uint16_t *xp = a.x + c4 * 8;          // the row, as the B operand (column 0..15 alike)
+    const uint16_t *gp = a.gain + c4 * 8;
+
+    f32x4 acc[NBLK];
+#pragma unroll
+    for (int j = 0; j < NBLK; ++j)
+        acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float ss = 0.f;
+    // (two blocks: half the batch, so the same bytes are in flight and the
+    // registers leave room for two workgroups per compute unit)
+    constexpr int BATCH = NBLK == 1 ? kGemvBatch : kGemvBatch / 2;
+    for (int cb = wave; cb < n_c; cb += kGemvWaves * BATCH) {
+        bf16x8 wr[BATCH][NBLK], xr[BATCH];
+        u32x4 gr[BATCH];
+#pragma unroll
+        for (int u = 0; u < BATCH; ++u) {
+            const int c = cb + kGemvWaves * u;
+            if (c < n_c) {
+#pragma unroll
+                for (int j = 0; j < NBLK; ++j)
+                    wr[u][j] = load_bf16x8(wp[j] + (size_t)c * wstep);
+                xr[u] = load_bf16x8(xp + c * 32);
+                if constexpr (MODE == kEpiSwiglu)
+                    gr[u] = *reinterpret_cast<const u32x4 *>(gp + c * 32);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < BATCH; ++u) {
+            if (cb + kGemvWaves * u < n_c) {
+                bf16x8 xo = xr[u];
+                if constexpr (MODE == kEpiSwiglu) {
+                    // x * gain in bf16, and the row's sum of squares (each
+                    // lane of column 0 counts its 8 elements once)
+                    const u32x4 xv = __builtin_bit_cast(u32x4, xr[u]);
+                    u32x4 o;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float x0 = __uint_as_float(xv[e] << 16);
+                        const float x1 = __uint_as_float(xv[e] & 0xffff0000u);
+                        const float g0 = __uint_as_float(gr[u][e] << 16);
+                        const float g1 = __uint_as_float(gr[u][e] & 0xffff0000u);
+                        if (m16 == 0) {
+                            ss = fmaf(x0, x0, ss);
+                            ss = fmaf(x1, x1, ss);
+                        }
+                        o[e] = pack_bf16x2(x0 * g0, x1 * g1);
+                    }
+                    xo = __builtin_bit_cast(bf16x8, o);
+                }
+#pragma unroll
+                for (int j = 0; j < NBLK; ++j)
+                    acc[j] = mfma16x16x32(wr[u][j], xo, acc[j]);
+            }
+        }
+    }
+    // lane (m16, c4) holds features 4*c4 + i of column m16 (every column
+    // is the same row; column 0 is kept)
+    if (m16 == 0) {
+#pragma unroll
+        for (int j = 0; j < NBLK; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                zs[wave][16 * j + 4 * c4 + i] = acc[j][i];
+    }
+    if constexpr (MODE == kEpiSwiglu) {
+        ss += __shfl_xor(ss, 16, kWave);
+        ss += __shfl_xor(ss, 32, kWave);
+        if (lane == 0)
+            sq[wave] = ss;
+    }
+    __syncthreads();
+    const int e = threadIdx.x;
+    if (e >= 16)
+        return;
+    float z[NBLK];
+#pragma unroll
+    for (int j = 0; j < NBLK; ++j) {
+        z[j] = zs[0][16 * j + e];
+#pragma unroll
+        for (int ww = 1; ww < kGemvWaves; ++ww)
+            z[j] += zs[ww][16 * j + e];
+    }
+    if constexpr (MODE == kEpiResid) {
+        const int f = 16 * blk[0] + e;
+        a.y[f] = f32_to_bf16(z[0] + bf16_to_f32(a.res[f]));
+    } else {
+        float tot = sq[0];
+#pragma unroll
+        for (int ww = 1; ww < kGemvWaves; ++ww)
+            tot += sq[ww];
+        const float inv = 1.f / sqrtf(tot / (float)a.k_in + a.eps);
+        const float gt = z[0] * inv, up = z[1] * inv;
+        a.y[16 * blk[0] + e] = f32_to_bf16(gt / (1.f + expf(-gt)) * up);
+    }
+}
+
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
+
+wf_status_t launch_linear_resid(const uint16_t *x, const uint16_t *w, const uint16_t *res,
+                                int k_in, int n_out, uint16_t *y, hipStream_t stream,
+                                bool tiled) {
+    EpiParams a{};
+    a.x = x;
+    a.w_a = w;
+    a.res = res;
+    a.y = y;
+    a.k_in = k_in;
+    a.n_out = n_out;
+    a.tiled = tiled ? 1 : 0;
+    linear_epi_bf16<kEpiResid><<<n_out / 16, kGemvWaves * kWave, 0, stream>>>(a);
+    return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
+}
+
+wf_status_t launch_linear_norm_swiglu(const uint16_t *x, const uint16_t *gain, float eps,
+                                      const uint16_t *w_gate, const uint16_t *w_up, int k_in,
+                                      int inter, uint16_t *act, hipStream_t stream,
+                                      bool tiled) {
+    EpiParams a{};
+    a.x = x;
+    a.gain = gain;
+    a.eps = eps;
+    a.w_a = w_gate;
+    a.w_b = w_up;
+    a.y = act;
+    a.k_in = k_in;
+    a.n_out = inter;
+    a.tiled = tiled ? 1 : 0;
+    linear_epi_bf16<kEpiSwiglu><<<inter / 16, kGemvWaves * kWave, 0, stream>>>(a);
+    return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
+}
 
 int linear_slices(int k_in, int n_out) {
     const int chunks = k_in / 32;

@@ -42,6 +42,8 @@ struct PrefillParams {
     int token_blocks;          // blockIdx.z = layer * token_blocks + token block
     long long x_ls, w_ls, c_ls; // element strides between layers (x, W_k|W_v, caches)
     int w_tiled;               // W_k, W_v in 16x32 tiles of 1 KB (bf16 path)
+    int kinds;                 // 2: K and V; 1: K only (a rotated projection, e.g. q)
+    int rope_shift;            // RoPE position = cache row position + rope_shift
 };
 
 // Rotation of the pair (lo, hi) = (k_i, k_{i+D/2}) by pos * theta_i, with
@@ -77,8 +79,8 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
     const int tb = blockIdx.z % a.token_blocks;
     const int layer = blockIdx.z / a.token_blocks;
     const int pair = unit % PAIRS;
-    const int kind = (unit / PAIRS) % 2; // 0 = K, 1 = V
-    const int g = unit / (2 * PAIRS);
+    const int kind = a.kinds == 2 ? (unit / PAIRS) % 2 : 0;   // 0 = K, 1 = V
+    const int g = unit / (a.kinds * PAIRS);
     const int t0 = tb * TOK;
 
     const int wave = wave_id();
@@ -205,7 +207,7 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
             continue;
         const int pos = a.start_pos + t;
         if (kind == 0)
-            rope_pair(lo, hi, a.theta[16 * pair + e], pos);
+            rope_pair(lo, hi, a.theta[16 * pair + e], pos + a.rope_shift);
         uint16_t *row = cache + ((size_t)g * a.cap + pos) * DH;
         row[16 * pair + e] = f32_to_bf16(lo);
         row[DH / 2 + 16 * pair + e] = f32_to_bf16(hi);
@@ -254,11 +256,12 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
-PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers) {
+PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers,
+                         int kinds) {
     PrefillPlan p{};
     p.nbt = std::min(4, std::max(1, cdiv(n_tok, 16)));
     p.token_blocks = std::max(1, cdiv(n_tok, 16 * p.nbt));
-    p.units = n_kv_heads * 2 * (head_dim / 32);
+    p.units = n_kv_heads * kinds * (head_dim / 32);
     const int chunks = d_in / 32;
     // a power-of-two number of k-slices: enough to cover the chip, at least
     // 4 chunks per slice.  layers * units * token_blocks * (ksplit - 1) <
@@ -304,7 +307,7 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
     if (tiled)
         dt = WF_BF16;
     PrefillParams a{x, w_k, w_v, k_cache, v_cache, n_tok, start_pos, cap, d_in,
-                    n_kv_heads, {}, nullptr, 0, 1, x_ls, w_ls, c_ls, tiled ? 1 : 0};
+                    n_kv_heads, {}, nullptr, 0, 1, x_ls, w_ls, c_ls, tiled ? 1 : 0, 2, 0};
     for (int i = 0; i < head_dim / 2; ++i)
         a.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
     if (dt == WF_BF16) {
@@ -337,6 +340,33 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
     if (hipGetLastError() != hipSuccess)
         return WF_ERR_HIP;
     return WF_OK;
+}
+
+// q = RoPE(W_q x) for one token: the K half of the kernel above with the
+// query heads as its heads, written to q [n_heads][head_dim] (a one-row
+// "cache") and rotated at position pos.  The split over the input
+// dimension and the exchange tree spread its units over the whole chip.
+wf_status_t launch_q_rope(const uint16_t *x, const uint16_t *w_q, uint16_t *q, int d_in,
+                          int n_heads, int head_dim, int pos, double rope_base,
+                          void *workspace, hipStream_t stream, bool tiled) {
+    PrefillParams a{x, w_q, w_q, q, q, 1, 0, 1, d_in, n_heads, {}, nullptr, 0, 1, 0, 0, 0,
+                    tiled ? 1 : 0, 1, pos};
+    for (int i = 0; i < head_dim / 2; ++i)
+        a.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
+    const PrefillPlan p = plan_prefill(1, d_in, n_heads, head_dim, 1, 1);
+    if (prefill_slot_bytes(p, 1) > kCounterBytes)
+        return WF_ERR_UNSUPPORTED;
+    a.chunks_per_split = p.chunks_per_split;
+    a.token_blocks = p.token_blocks;
+    a.slots = static_cast<unsigned long long *>(workspace);
+    dim3 grid(p.units, p.ksplit, p.token_blocks), block(256);
+    if (head_dim == 128)
+        prefill_bf16<128, 1><<<grid, block, 0, stream>>>(a);
+    else if (head_dim == 64)
+        prefill_bf16<64, 1><<<grid, block, 0, stream>>>(a);
+    else
+        return WF_ERR_UNSUPPORTED;
+    return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
 }
 
 }  // namespace wf

@@ -82,6 +82,17 @@ wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
                                   int k_in, float *zpart, hipStream_t stream,
                                   bool tiled = false);
 
+// Single-token skinny linear layers with their epilogue in the kernel
+// (gemv.hip): y = res + W x; act = SiLU(Wg x') * (Wu x') with
+// x' = RMSNorm(x) * gain.  n_out, inter multiples of 16, k_in of 32.
+wf_status_t launch_linear_resid(const uint16_t *x, const uint16_t *w, const uint16_t *res,
+                                int k_in, int n_out, uint16_t *y, hipStream_t stream,
+                                bool tiled);
+wf_status_t launch_linear_norm_swiglu(const uint16_t *x, const uint16_t *gain, float eps,
+                                      const uint16_t *w_gate, const uint16_t *w_up, int k_in,
+                                      int inter, uint16_t *act, hipStream_t stream,
+                                      bool tiled);
+
 // Neural routing policy: delta = w2 . GELU(W1 h + b1) + b2 for every row,
 // route at the row *row names.
 size_t router_workspace_bytes(wf_dtype_t dt, int gamma, int d, int m);
@@ -121,7 +132,8 @@ struct PrefillPlan {
     int chunks_per_split;
 };
 
-PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers = 1);
+PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers = 1,
+                         int kinds = 2);
 size_t prefill_workspace_bytes(wf_dtype_t dt, int n_tok, int d_in, int n_kv_heads,
                                int head_dim);
 // Whether the bf16 plan's exchange slots fit the workspace zero block (and
@@ -140,6 +152,13 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
 // read [src, src + bytes) once; sink takes workgroups * 4 KB.
 wf_status_t launch_read_probe(const void *src, size_t bytes, void *sink, int workgroups,
                               hipStream_t stream);
+
+// q = RoPE(W_q x) for one token at position pos, q [n_heads][head_dim],
+// on the KV-only prefill kernel (its exchange slots live in the workspace's
+// zero block).
+wf_status_t launch_q_rope(const uint16_t *x, const uint16_t *w_q, uint16_t *q, int d_in,
+                          int n_heads, int head_dim, int pos, double rope_base,
+                          void *workspace, hipStream_t stream, bool tiled);
 
 // Tiled bf16 weights (16x32 tiles of 1 KB, one wave operand load each).
 size_t tiled_weight_bytes(int rows, int cols);
