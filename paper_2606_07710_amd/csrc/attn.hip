@@ -582,6 +582,20 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
         const int h = g * a.group + (r % a.group);
         const size_t pr = (size_t)split * pairs + (size_t)i * a.n_q_heads + h;
         uint2 *dst = reinterpret_cast<uint2 *>(static_cast<uint16_t *>(a.ws_o) + pr * DH);
+        if constexpr (KS == 1 && NBW == 1) {
+            // one key stream, 16 rows per wave: stage the bf16 rows in the
+            // (idle) ring so they leave in 16-byte pieces below
+            constexpr int RB = DH * 2 + 16;              // padded row bytes
+            static_assert(2 * 16 * RB <= STAGE_BYTES, "staging exceeds a ring slot");
+            static_assert(RG <= 4, "two waves per ring buffer");
+            WF_LDS(char) *stg = (WF_LDS(char) *)(rgi < 2 ? ring0 : ring1) + (rgi & 1) * 16 * RB;
+#pragma unroll
+            for (int md = 0; md < MD; ++md) {
+                f32x4 v = o[md][nb] * fac[nb];
+                *(WF_LDS(u32x2) *)(stg + m16 * RB + (md * 16 + 4 * c4) * 2) =
+                    u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+            }
+        } else {
 #pragma unroll
         for (int md = 0; md < MD; ++md) {
             f32x4 v = o[md][nb] * fac[nb];
@@ -591,6 +605,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             // bf16 partials: the split merge weighs them by at most 1 and
             // the output is rounded to bf16 anyway
             dst[md * 4 + c4] = uint2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        }
         }
         if (KS == 1 && c4 == 0) {
             a.ws_ml[pr * 2] = mref[nb];
@@ -609,6 +624,26 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             }
             a.ws_ml[pr * 2] = mm;
             a.ws_ml[pr * 2 + 1] = ll;
+        }
+    }
+    if constexpr (KS == 1 && NBW == 1) {
+        // the wave's 16 staged rows leave as 16-byte pieces: each store
+        // writes whole rows of consecutive (row, head) pairs
+        constexpr int RB = DH * 2 + 16;
+        constexpr int PPR = DH / 8;                    // 16-byte pieces per row
+        const WF_LDS(char) *stg = (const WF_LDS(char) *)(rgi < 2 ? ring0 : ring1) + (rgi & 1) * 16 * RB;
+        const int pairs2 = a.gamma * a.n_q_heads;
+#pragma unroll
+        for (int pc = lane; pc < 16 * PPR; pc += kWave) {
+            const int row = pc / PPR, col = pc % PPR;
+            const int r = rgw * ROWS_WG + rgi * ROWS_W + row;
+            if (r < a.rows) {
+                const int i = r / a.group;
+                const int h = g * a.group + (r % a.group);
+                const size_t pr = (size_t)split * pairs2 + (size_t)i * a.n_q_heads + h;
+                reinterpret_cast<u32x4 *>(static_cast<uint16_t *>(a.ws_o) + pr * DH)[col] =
+                    *(const WF_LDS(u32x4) *)(stg + row * RB + col * 16);
+            }
         }
     }
 }
