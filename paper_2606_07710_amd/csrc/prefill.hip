@@ -170,47 +170,74 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
     // climbs on.  Whoever leaves the root finishes the pair: RoPE for K,
     // bf16 cache write.  Slot 0 means empty; a parked pair is stored as
     // (bits(hi) << 32) | (bits(lo) + 1), never 0 for arithmetic results.
+    // A thread holds NI pairs (idx = tid + 256 i) and climbs with all of
+    // them at once: one exchange round trip per tree level, not per pair.
+    constexpr int NI = 16 * TOK / 256;
+    static_assert(16 * TOK % 256 == 0, "pairs per workgroup must fill the 256 threads");
     const int ksplit = gridDim.y;
     const size_t ub =                                          // (layer, unit, token block)
         ((size_t)layer * gridDim.x + unit) * a.token_blocks + tb;
     unsigned long long *slots = a.slots + ub * (size_t)(ksplit - 1) * (16 * TOK);
     uint16_t *cache = static_cast<uint16_t *>(kind ? a.v_cache : a.k_cache) + layer * a.c_ls;
-    for (int idx = threadIdx.x; idx < 16 * TOK; idx += blockDim.x) {
+    float lo[NI], hi[NI];
+    bool mine[NI];
+#pragma unroll
+    for (int n = 0; n < NI; ++n) {
+        const int idx = threadIdx.x + 256 * n;
         const int e = idx / TOK;
         const int tl = idx % TOK;
-        float lo = zs[0][0][e][tl], hi = zs[0][1][e][tl];
+        lo[n] = zs[0][0][e][tl];
+        hi[n] = zs[0][1][e][tl];
 #pragma unroll
         for (int ww = 1; ww < WAVES; ++ww) {
-            lo += zs[ww][0][e][tl];
-            hi += zs[ww][1][e][tl];
+            lo[n] += zs[ww][0][e][tl];
+            hi[n] += zs[ww][1][e][tl];
         }
-        unsigned node = (unsigned)(ksplit + ks);
-        bool mine = true;
-        while (node > 1) {
-            unsigned long long *slot = slots + (size_t)(node / 2 - 1) * (16 * TOK) + idx;
+        mine[n] = true;
+    }
+    for (unsigned node = (unsigned)(ksplit + ks); node > 1; node /= 2) {
+        unsigned long long *level = slots + (size_t)(node / 2 - 1) * (16 * TOK) + threadIdx.x;
+        unsigned long long old[NI];
+#pragma unroll
+        for (int n = 0; n < NI; ++n) {
             const unsigned long long packed =
-                ((unsigned long long)__float_as_uint(hi) << 32) |
-                (unsigned long long)(__float_as_uint(lo) + 1u);
-            const unsigned long long old =
-                __hip_atomic_exchange(slot, packed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (old == 0ull) {
-                mine = false;          // the sibling finishes this node
-                break;
-            }
-            lo += __uint_as_float((unsigned)old - 1u);
-            hi += __uint_as_float((unsigned)(old >> 32));
-            __hip_atomic_store(slot, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            node /= 2;
+                ((unsigned long long)__float_as_uint(hi[n]) << 32) |
+                (unsigned long long)(__float_as_uint(lo[n]) + 1u);
+            old[n] = mine[n] ? __hip_atomic_exchange(level + 256 * n, packed, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)
+                             : 0ull;
         }
-        const int t = t0 + tl;
-        if (!mine || t >= a.n_tok)
+        bool any = false;
+#pragma unroll
+        for (int n = 0; n < NI; ++n) {
+            if (!mine[n])
+                continue;
+            if (old[n] == 0ull) {
+                mine[n] = false;       // the sibling finishes this node
+                continue;
+            }
+            lo[n] += __uint_as_float((unsigned)old[n] - 1u);
+            hi[n] += __uint_as_float((unsigned)(old[n] >> 32));
+            __hip_atomic_store(level + 256 * n, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            any = true;
+        }
+        if (!any)
+            break;
+    }
+#pragma unroll
+    for (int n = 0; n < NI; ++n) {
+        const int idx = threadIdx.x + 256 * n;
+        const int e = idx / TOK;
+        const int t = t0 + idx % TOK;
+        if (!mine[n] || t >= a.n_tok)
             continue;
         const int pos = a.start_pos + t;
+        float l = lo[n], h = hi[n];
         if (kind == 0)
-            rope_pair(lo, hi, a.theta[16 * pair + e], pos + a.rope_shift);
+            rope_pair(l, h, a.theta[16 * pair + e], pos + a.rope_shift);
         uint16_t *row = cache + ((size_t)g * a.cap + pos) * DH;
-        row[16 * pair + e] = f32_to_bf16(lo);
-        row[DH / 2 + 16 * pair + e] = f32_to_bf16(hi);
+        row[16 * pair + e] = f32_to_bf16(l);
+        row[DH / 2 + 16 * pair + e] = f32_to_bf16(h);
     }
 }
 
