@@ -326,7 +326,10 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
                             const int j = kb + 16 * mb + 4 * c4 + i - a.ctx_len;
-                            const bool vis = j < 0 || (j < a.gamma && ((tm[nb] >> j) & 1ull));
+                            // branch-free (selects, no exec-mask branches):
+                            // j < gamma <= 64 bounds the shift
+                            const bool bit = ((tm[nb] >> (j & 63)) & 1ull) != 0;
+                            const bool vis = (j < 0) | ((j < a.gamma) & bit);
                             s[mb][nb][i] = vis ? s[mb][nb][i] : -INFINITY;
                         }
             }
