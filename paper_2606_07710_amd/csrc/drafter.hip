@@ -54,12 +54,19 @@ __device__ __forceinline__ u32x4 load_u32x4(const uint16_t *p) {
 __device__ __forceinline__ float lo_f32(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_f32(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// Workgroup r normalises row min(r, n_rows - 1); y (row-major) gets rows
+// below n_rows, y_tiled (if given) every row of the grid in 16-token x
+// 32-dim tiles of 1 KB in the MFMA operand's lane order -- the layout the
+// KV-only prefill reads with one contiguous load per tile (the grid then
+// covers n_rows rounded up to 16; the pad rows repeat the last row).
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_bf16(const uint16_t *__restrict__ x,
                                                              const uint16_t *__restrict__ g,
                                                              float eps, uint16_t *__restrict__ y,
-                                                             int d) {
+                                                             int d, int n_rows,
+                                                             uint16_t *__restrict__ y_tiled) {
     __shared__ float part[kNormThreads / kWave];
-    const uint16_t *xr = x + (size_t)blockIdx.x * d;
+    const int row = blockIdx.x;
+    const uint16_t *xr = x + (size_t)min(row, n_rows - 1) * d;
     const int n_chunks = d / 8;
     float ss = 0.f;
     for (int c0 = threadIdx.x; c0 < n_chunks; c0 += kNormThreads * kRowBatch) {
@@ -88,7 +95,11 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_bf16(const uint16_t *__r
     for (int w = 1; w < kNormThreads / kWave; ++w)
         tot += part[w];
     const float inv = 1.f / sqrtf(tot / (float)d + eps);
-    uint16_t *yr = y + (size_t)blockIdx.x * d;
+    uint16_t *yr = row < n_rows ? y + (size_t)row * d : nullptr;
+    // tile (row / 16, chunk c) holds lane (row % 16) + 16 * (8-dim group
+    // within the chunk) at 16 bytes per lane
+    uint16_t *yt = y_tiled ? y_tiled + (size_t)(row / 16) * (d / 32) * 512 + (row % 16) * 8
+                           : nullptr;
     for (int c0 = threadIdx.x; c0 < n_chunks; c0 += kNormThreads * kRowBatch) {
         u32x4 v[kRowBatch], gv[kRowBatch];
 #pragma unroll
@@ -105,7 +116,11 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_bf16(const uint16_t *__r
                 for (int e = 0; e < 4; ++e)
                     o[e] = pack_bf16x2(lo_f32(v[u][e]) * inv * lo_f32(gv[u][e]),
                                        hi_f32(v[u][e]) * inv * hi_f32(gv[u][e]));
-                *reinterpret_cast<u32x4 *>(yr + 8 * (c0 + u * kNormThreads)) = o;
+                const int cc = c0 + u * kNormThreads;          // 8-element chunk
+                if (yr)
+                    *reinterpret_cast<u32x4 *>(yr + 8 * cc) = o;
+                if (yt)
+                    *reinterpret_cast<u32x4 *>(yt + (size_t)(cc / 4) * 512 + (cc % 4) * 128) = o;
             }
     }
 }
@@ -231,9 +246,12 @@ size_t drafter_forward_workspace_bytes(const wf_decoder_layer_t &L, int M, int p
     return drafter_layout(L, M, pos).total;
 }
 
+// Catch-up workspace: the last token's full-layer workspace, then the
+// backlog's normalised rows (row-major, for the last token's projections),
+// then the same rows in 16 x 32 tiles for the KV-only prefill.
 size_t drafter_catchup_workspace_bytes(const wf_decoder_layer_t &L, int n, int pos) {
     return align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)) +
-           (size_t)n * L.hidden * 2;
+           align256((size_t)n * L.hidden * 2) + (size_t)((n + 15) / 16) * 16 * L.hidden * 2;
 }
 
 namespace {
@@ -262,7 +280,8 @@ wf_status_t drafter_forward(const wf_decoder_layer_t &L, const uint16_t *rb, int
     if (xn_given) {
         xn = const_cast<uint16_t *>(xn_given);
     } else {
-        rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(rb, W(L.attn_norm), L.rms_eps, xn, d);
+        rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(rb, W(L.attn_norm), L.rms_eps, xn, d, M,
+                                                      nullptr);
         st = launch_prefill(wdt, xn, L.w_k, L.w_v, k_cache, v_cache, M, pos, cap, d,
                             L.n_kv_heads, L.head_dim, L.rope_base, workspace, stream);
         if (st != WF_OK)
@@ -310,7 +329,8 @@ wf_status_t drafter_forward(const wf_decoder_layer_t &L, const uint16_t *rb, int
         return st;
     reduce_store_bf16<<<blocks_for((long long)M * d), 256, 0, stream>>>(
         zp, linear_slices(qd, d), d, M, rb, h1);
-    rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(h1, W(L.mlp_norm), L.rms_eps, xn2, d);
+    rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(h1, W(L.mlp_norm), L.rms_eps, xn2, d, M,
+                                                  nullptr);
     // act = SiLU(Wg xn2) * (Wu xn2)
     if ((st = launch_linear_partial(xn2, W(L.w_gate), W(L.w_up), I, I, M, d, zp, stream,
                                     tiled)) != WF_OK)
@@ -342,18 +362,22 @@ wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, i
                                    void *workspace, hipStream_t stream, bool tiled) {
     const int d = L.hidden;
     const auto *rb = static_cast<const uint16_t *>(r);
-    auto *xnb = reinterpret_cast<uint16_t *>(
-        static_cast<char *>(workspace) + align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1)));
-    rmsnorm_bf16<<<n, kNormThreads, 0, stream>>>(rb, static_cast<const uint16_t *>(L.attn_norm),
-                                                 L.rms_eps, xnb, d);
+    char *tail = static_cast<char *>(workspace) +
+                 align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1));
+    auto *xnb = reinterpret_cast<uint16_t *>(tail);
+    auto *xnt = reinterpret_cast<uint16_t *>(tail + align256((size_t)n * d * 2));
+    rmsnorm_bf16<<<(n + 15) / 16 * 16, kNormThreads, 0, stream>>>(
+        rb, static_cast<const uint16_t *>(L.attn_norm), L.rms_eps, xnb, d, n, xnt);
     // the whole backlog's K/V in batches of at most kCatchupChunk tokens
-    // (one KV-only prefill each; a single batch for any backlog up to that)
+    // (one KV-only prefill each; a single batch for any backlog up to that),
+    // reading the tiled rows (a batch starts on a 16-row tile boundary)
     for (int c0 = 0; c0 < n; c0 += kCatchupChunk) {
         const int m = std::min(kCatchupChunk, n - c0);
         const wf_status_t st = launch_prefill(tiled ? WF_BF16_TILED : WF_BF16,
-                                              xnb + (size_t)c0 * d, L.w_k, L.w_v, k_cache,
+                                              xnt + (size_t)c0 * d, L.w_k, L.w_v, k_cache,
                                               v_cache, m, pos + c0, cap, d, L.n_kv_heads,
-                                              L.head_dim, L.rope_base, workspace, stream);
+                                              L.head_dim, L.rope_base, workspace, stream,
+                                              1, 0, 0, 0, true);
         if (st != WF_OK)
             return st;
     }

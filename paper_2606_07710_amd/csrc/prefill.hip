@@ -44,6 +44,8 @@ struct PrefillParams {
     int w_tiled;               // W_k, W_v in 16x32 tiles of 1 KB (bf16 path)
     int kinds;                 // 2: K and V; 1: K only (a rotated projection, e.g. q)
     int rope_shift;            // RoPE position = cache row position + rope_shift
+    int x_tiled;               // x in 16-token x 32-dim tiles of 1 KB, token rows
+                               // padded to a multiple of 16 (bf16 path)
 };
 
 // Rotation of the pair (lo, hi) = (k_i, k_{i+D/2}) by pos * theta_i, with
@@ -110,12 +112,26 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
         wp1 = w + (size_t)(f_lo + DH / 2 + m16) * a.d_in + c4 * 8;
         wstep = 32;
     }
-    // Tokens past n_tok read the last token instead: they only feed MFMA
-    // output columns that are never stored.
+    // Tokens past n_tok read the last token (row-major) or the padded
+    // rows of the last 16-token tile (tiled) instead: they only feed MFMA
+    // output columns that are never stored.  A tiled x gives every load one
+    // contiguous 1 KB tile (16 tokens x 32 dims in the operand's lane order)
+    // instead of 64 bytes from each of 16 rows.
     const uint16_t *xp[NBT];
+    int xstep;
+    if (a.x_tiled) {
+        const size_t kch = (size_t)(a.d_in / 32);
+        const int last_blk = (a.n_tok + 15) / 16 - 1;
 #pragma unroll
-    for (int nb = 0; nb < NBT; ++nb)
-        xp[nb] = x + (size_t)min(t0 + nb * 16 + m16, a.n_tok - 1) * a.d_in + c4 * 8;
+        for (int nb = 0; nb < NBT; ++nb)
+            xp[nb] = x + (size_t)min(t0 / 16 + nb, last_blk) * kch * 512 + lane * 8;
+        xstep = 512;
+    } else {
+#pragma unroll
+        for (int nb = 0; nb < NBT; ++nb)
+            xp[nb] = x + (size_t)min(t0 + nb * 16 + m16, a.n_tok - 1) * a.d_in + c4 * 8;
+        xstep = 32;
+    }
 
     f32x4 acc[2][NBT];
 #pragma unroll
@@ -131,7 +147,7 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
         for (int u = 0; u < MAXC; ++u) {
             const int c = cb + WAVES * u;
             if (c < n_c) {
-                const int off = (c_begin + c) * 32;
+                const size_t off = (size_t)(c_begin + c) * xstep;
                 const size_t woff = (size_t)(c_begin + c) * wstep;
                 wr[u][0] = load_bf16x8(wp0 + woff);
                 wr[u][1] = load_bf16x8(wp1 + woff);
@@ -329,12 +345,15 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            int n_tok, int start_pos, int cap, int d_in,
                            int n_kv_heads, int head_dim, double rope_base,
                            void *workspace, hipStream_t stream, int n_layers,
-                           long long x_ls, long long w_ls, long long c_ls) {
+                           long long x_ls, long long w_ls, long long c_ls, bool x_tiled) {
     const bool tiled = dt == WF_BF16_TILED;
     if (tiled)
         dt = WF_BF16;
+    if (x_tiled && dt != WF_BF16)
+        return WF_ERR_UNSUPPORTED;
     PrefillParams a{x, w_k, w_v, k_cache, v_cache, n_tok, start_pos, cap, d_in,
-                    n_kv_heads, {}, nullptr, 0, 1, x_ls, w_ls, c_ls, tiled ? 1 : 0, 2, 0};
+                    n_kv_heads, {}, nullptr, 0, 1, x_ls, w_ls, c_ls, tiled ? 1 : 0, 2, 0,
+                    x_tiled ? 1 : 0};
     for (int i = 0; i < head_dim / 2; ++i)
         a.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
     if (dt == WF_BF16) {
@@ -377,7 +396,7 @@ wf_status_t launch_q_rope(const uint16_t *x, const uint16_t *w_q, uint16_t *q, i
                           int n_heads, int head_dim, int pos, double rope_base,
                           void *workspace, hipStream_t stream, bool tiled) {
     PrefillParams a{x, w_q, w_q, q, q, 1, 0, 1, d_in, n_heads, {}, nullptr, 0, 1, 0, 0, 0,
-                    tiled ? 1 : 0, 1, pos};
+                    tiled ? 1 : 0, 1, pos, 0};
     for (int i = 0; i < head_dim / 2; ++i)
         a.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
     const PrefillPlan p = plan_prefill(1, d_in, n_heads, head_dim, 1, 1);

@@ -146,7 +146,8 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
                            int n_tok, int start_pos, int cap, int d_in,
                            int n_kv_heads, int head_dim, double rope_base,
                            void *workspace, hipStream_t stream, int n_layers = 1,
-                           long long x_ls = 0, long long w_ls = 0, long long c_ls = 0);
+                           long long x_ls = 0, long long w_ls = 0, long long c_ls = 0,
+                           bool x_tiled = false);
 
 // Streaming-read probe (probe.hip): `workgroups` workgroups of 256 threads
 // read [src, src + bytes) once; sink takes workgroups * 4 KB.
