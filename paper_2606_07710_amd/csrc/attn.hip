@@ -820,6 +820,84 @@ __global__ __launch_bounds__(64) void attn_merge(const void *__restrict__ ws_o,
     }
 }
 
+// Split merge for up to G*kMergeBatch splits (every plan of the bf16 path
+// at head_dim 128 uses at most 32): WPB waves per workgroup, one per
+// (row, q head).  Lane (group grp, column d4) loads, in one batch, the
+// partial columns of its splits grp, grp + G, ... together with their
+// (max, sum) pairs, so the whole merge is one memory round trip: the group
+// maxima meet in a butterfly over the G groups, each lane weighs its own
+// splits in ascending order, and the weighted columns and sums meet in a
+// second fixed butterfly (every lane of a column ends with the same bits).
+template <int DH, bool BF16, int WPB>
+__global__ __launch_bounds__(64 * WPB) void attn_merge_one(const void *__restrict__ ws_o,
+                                                           const float *__restrict__ ws_ml,
+                                                           void *out, int pairs, int splits,
+                                                           float sl2) {
+    constexpr int Q = DH / 4;
+    constexpr int G = kWave / Q;
+    constexpr int B = kMergeBatch;
+    const int pr = blockIdx.x * WPB + wave_id();
+    if (pr >= pairs)
+        return;
+    const int lane = threadIdx.x % kWave;
+    const int d4 = lane % Q;
+    const int grp = lane / Q;
+    const size_t sstride = (size_t)pairs * Q;
+    f32x4 v[B];
+    float2 ml[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        const int sp = min(grp + G * b, splits - 1);
+        const size_t idx = (size_t)sp * sstride + (size_t)pr * Q + d4;
+        if constexpr (BF16) {
+            const uint2 pk = reinterpret_cast<const uint2 *>(ws_o)[idx];
+            v[b] = f32x4{bf16_to_f32((uint16_t)pk.x), bf16_to_f32((uint16_t)(pk.x >> 16)),
+                         bf16_to_f32((uint16_t)pk.y), bf16_to_f32((uint16_t)(pk.y >> 16))};
+        } else {
+            v[b] = reinterpret_cast<const f32x4 *>(ws_o)[idx];
+        }
+        ml[b] = reinterpret_cast<const float2 *>(ws_ml)[(size_t)sp * pairs + pr];
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+        if (grp + G * b < splits)
+            mx = fmaxf(mx, ml[b].x);
+#pragma unroll
+    for (int off = Q; off < kWave; off *= 2)
+        mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+    const float muse = (mx == -INFINITY) ? 0.f : mx;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    float lsum = 0.f;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        if (grp + G * b < splits) {
+            const float w = (ml[b].x == -INFINITY) ? 0.f : fast_exp2((ml[b].x - muse) * sl2);
+            lsum = fmaf(w, ml[b].y, lsum);
+            acc += w * v[b];
+        }
+    }
+#pragma unroll
+    for (int off = Q; off < kWave; off *= 2) {
+        f32x4 o;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            o[c] = __shfl_xor(acc[c], off, kWave);
+        acc += o;
+        lsum += __shfl_xor(lsum, off, kWave);
+    }
+    if (grp == 0) {
+        const size_t oi = (size_t)pr * DH + 4 * d4;
+        const f32x4 r = acc * (1.f / lsum);
+        if constexpr (BF16) {
+            *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(out) + oi) =
+                uint2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
+        } else {
+            *reinterpret_cast<f32x4 *>(static_cast<float *>(out) + oi) = r;
+        }
+    }
+}
+
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
@@ -959,8 +1037,24 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
     if (hipGetLastError() != hipSuccess)
         return WF_ERR_HIP;
 
-    dim3 mgrid((unsigned)pairs), mblock(64);
     const bool ob = (dt == WF_BF16);
+    constexpr int kMergeWpb = 1;
+    if (p.splits <= (kWave / (head_dim / 4)) * kMergeBatch) {
+        dim3 g1((unsigned)cdiv((int)pairs, kMergeWpb)), b1(64 * kMergeWpb);
+        if (head_dim == 128) {
+            if (ob)
+                attn_merge_one<128, true, kMergeWpb><<<g1, b1, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
+            else
+                attn_merge_one<128, false, kMergeWpb><<<g1, b1, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
+        } else {
+            if (ob)
+                attn_merge_one<64, true, kMergeWpb><<<g1, b1, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
+            else
+                attn_merge_one<64, false, kMergeWpb><<<g1, b1, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
+        }
+        return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
+    }
+    dim3 mgrid((unsigned)pairs), mblock(64);
     if (head_dim == 128) {
         if (ob)
             attn_merge<128, true><<<mgrid, mblock, 0, stream>>>(a.ws_o, a.ws_ml, out, (int)pairs, p.splits, a.sl2);
