@@ -326,10 +326,17 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
                             const int j = kb + 16 * mb + 4 * c4 + i - a.ctx_len;
-                            // branch-free (selects, no exec-mask branches):
-                            // j < gamma <= 64 bounds the shift
-                            const bool bit = ((tm[nb] >> (j & 63)) & 1ull) != 0;
-                            const bool vis = (j < 0) | ((j < a.gamma) & bit);
+                            bool vis;
+                            if constexpr (NBW == 1) {
+                                // branch-free (selects, no exec-mask
+                                // branches): j < gamma <= 64 bounds the shift
+                                const bool bit = ((tm[nb] >> (j & 63)) & 1ull) != 0;
+                                vis = (j < 0) | ((j < a.gamma) & bit);
+                            } else {
+                                // (the select form's extra registers make
+                                // the two-block waves spill)
+                                vis = j < 0 || (j < a.gamma && ((tm[nb] >> j) & 1ull));
+                            }
                             s[mb][nb][i] = vis ? s[mb][nb][i] : -INFINITY;
                         }
             }
