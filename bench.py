@@ -321,6 +321,35 @@ def read_ceiling(wf, dev, mib, reps=3):
     return max(rates.values()), rates
 
 
+def size_matched_read_us(wf, dev, nbytes, total_mib=640, reps=5):
+    """Per-call time (us) of the library's plain streaming read of `nbytes`,
+    the reads launched back to back over consecutive pieces of a buffer that
+    together exceed the 256 MB last-level cache: the best over a few grid
+    sizes and load depths.  It is the time any kernel needs just to move
+    that many bytes in one launch on this part (launch, first-byte latency
+    and drain included)."""
+    import torch
+    n_bufs = max(1, -(-(total_mib << 20) // nbytes))
+    buf = torch.ones(n_bufs * nbytes, dtype=torch.uint8, device=dev)
+    best = None
+    for wgs in (256, 512, 1024, 2048):
+        sink = torch.empty(wgs * 4096, dtype=torch.uint8, device=dev)
+        for depth in (4, 8):
+            wf.wf_read_probe_series(buf, nbytes, n_bufs, 1, sink, wgs, depth)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            wf.wf_read_probe_series(buf, nbytes, n_bufs, reps, sink, wgs, depth)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / (reps * n_bufs)
+            best = us if best is None else min(best, us)
+        del sink
+    del buf
+    return best
+
+
 def cpu_baseline(w, layers, head, budget_s, max_layers=None, tree_mask=None):
     """The oracle as it stands, on host cores, over a bounded sample of the
     step: the LM head, then as many layers of attention and prefill as fit
@@ -499,6 +528,21 @@ def bench_switch(args, w):
                  "per_round_us": round(per * 1e3, 1)})
             log(f"{nb} tokens: lazy {lazy * 1e3:.1f} us, per round over {rounds} "
                 f"rounds {per * 1e3:.1f} us")
+
+    # ---- size-matched read floors (not timed with the step) -----------------
+    # a plain read of each kernel's bytes, one launch per call: what the
+    # step would take if every launch only streamed its bytes
+    floors = None
+    if args.read_probe_mib and by["attn_per_layer"] >= (16 << 20):
+        floors = {"attention": size_matched_read_us(wf, dev, by["attn_per_layer"]),
+                  "lmhead": size_matched_read_us(wf, dev, by["lmhead"])}
+        if by["prefill_per_layer"]:
+            floors["prefill"] = size_matched_read_us(wf, dev, by["prefill_per_layer"])
+        floors["step"] = (w.n_layers * (floors["attention"] + floors.get("prefill", 0.0))
+                          + floors["lmhead"])
+        floors = {k: round(v, 2) for k, v in floors.items()}
+        log("size-matched plain reads (us per launch): "
+            + ", ".join(f"{k} {v:.2f}" for k, v in floors.items()))
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -798,6 +842,21 @@ def main():
         log("read ceiling: " + ", ".join(f"{k} WGs {v:.0f}" for k, v in rates.items())
             + f" GB/s -> {ceiling:.0f}")
 
+    # ---- size-matched read floors (not timed with the step) -----------------
+    # a plain read of each kernel's bytes, one launch per call: what the
+    # step would take if every launch only streamed its bytes
+    floors = None
+    if args.read_probe_mib and by["attn_per_layer"] >= (16 << 20):
+        floors = {"attention": size_matched_read_us(wf, dev, by["attn_per_layer"]),
+                  "lmhead": size_matched_read_us(wf, dev, by["lmhead"])}
+        if by["prefill_per_layer"]:
+            floors["prefill"] = size_matched_read_us(wf, dev, by["prefill_per_layer"])
+        floors["step"] = (w.n_layers * (floors["attention"] + floors.get("prefill", 0.0))
+                          + floors["lmhead"])
+        floors = {k: round(v, 2) for k, v in floors.items()}
+        log("size-matched plain reads (us per launch): "
+            + ", ".join(f"{k} {v:.2f}" for k, v in floors.items()))
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"cpu baseline: about {args.cpu_budget_s:.0f}s of oracle work ...")
@@ -844,6 +903,11 @@ def main():
         "prefill_share": round(breakdown.get("prefill", 0.0) / (ms_per_step * 1e3), 4),
         "step_algorithmic_bytes": by["total"],
         "breakdown_us": breakdown,   # each phase run alone, back to back
+        # a plain read of each launch's algorithmic bytes, one launch per
+        # call, back to back (the step row: all of the step's launches)
+        "size_matched_read_us": floors,
+        "step_frac_of_size_matched": round(floors["step"] / (ms_per_step * 1e3), 4)
+                                     if floors else None,
         "roofline": {
             "kernel": ("wf_verify_attn_tree" if tree else "wf_verify_attn")
                       + ", one layer (attn_partial_bf16 + attn_merge)",
@@ -859,6 +923,9 @@ def main():
             # than the last-level cache, measured in this run
             "read_ceiling_gbps": round(ceiling, 1) if ceiling else None,
             "frac_of_read_ceiling": round(achieved / ceiling, 4) if ceiling else None,
+            # a plain read of the launch's bytes on its own over the call time
+            "frac_of_size_matched_read": round(floors["attention"] / (attn_avg_ms * 1e3), 4)
+                                         if floors else None,
             # secondary, derived (not a counter): the call's flops over its
             # time, against the dense bf16 MFMA peak
             "mfma_util_from_flops": round(w.flops()["attn_per_layer"] / (attn_avg_ms * 1e-3)

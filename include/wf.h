@@ -576,6 +576,24 @@ wf_status_t wf_read_probe(const void *src, size_t bytes, void *sink, size_t sink
                           int32_t workgroups, void *stream);
 
 /* ------------------------------------------------------------------------
+ * wf_read_probe_series -- measurement support, not a step of the method:
+ * reps rounds over the n_bufs buffers [base + i * stride, + bytes),
+ * i = 0 .. n_bufs - 1, each read once per round by the kernel of
+ * wf_read_probe with `depth` (4 or 8) loads in flight per thread, all
+ * launched back to back from the library (a caller's own launch rate would
+ * otherwise limit short reads).  Timed over buffers that together exceed
+ * the 256 MB last-level cache, it gives the time a plain read of `bytes`
+ * takes on its own: the floor for a kernel that must move that many bytes,
+ * launch, first-byte latency and drain included.  base, sink: device,
+ * 16-byte aligned; bytes a positive multiple of 16; stride >= bytes and a
+ * multiple of 16; n_bufs, reps >= 1; 1 <= workgroups <= 65536; sink_bytes
+ * >= workgroups * 4096 (else WF_ERR_WORKSPACE).  Asynchronous on stream.
+ * ---------------------------------------------------------------------- */
+wf_status_t wf_read_probe_series(const void *base, size_t bytes, size_t stride,
+                                 int32_t n_bufs, int32_t reps, void *sink, size_t sink_bytes,
+                                 int32_t workgroups, int32_t depth, void *stream);
+
+/* ------------------------------------------------------------------------
  * Lazy catch-up bookkeeping (Sec. 3.4 and its lazy catch-up study in
  * Sec. 4): a host-side record of how far the autoregressive drafter's KV
  * cache lags the committed sequence.  Only that drafter's cache can fall

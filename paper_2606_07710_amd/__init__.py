@@ -30,7 +30,7 @@ EXPORTED_SYMBOLS = (
     "wf_drafter_catchup_workspace_bytes", "wf_switch_init", "wf_switch_commit",
     "wf_kv_only_prefill_layers", "wf_kv_only_prefill_layers_workspace_bytes",
     "wf_tiled_weight_bytes", "wf_tile_weights", "wf_verify_attn_noalloc",
-    "wf_read_probe", "wf_lmhead_accept_route_neural",
+    "wf_read_probe", "wf_read_probe_series", "wf_lmhead_accept_route_neural",
     "wf_lmhead_route_neural_workspace_bytes",
 )
 NOALLOC_SCRATCH_BYTES = 32 << 20     # WF_NOALLOC_SCRATCH_BYTES
@@ -131,6 +131,8 @@ def _load():
     lib.wf_lmhead_route_neural_workspace_bytes.restype = sz
     lib.wf_read_probe.argtypes = [p, sz, p, sz, i32, p]
     lib.wf_read_probe.restype = i32
+    lib.wf_read_probe_series.argtypes = [p, sz, sz, i32, i32, p, sz, i32, i32, p]
+    lib.wf_read_probe_series.restype = i32
     lib.wf_switch_init.argtypes = [p, i32, i32, i32]
     lib.wf_switch_init.restype = i32
     lib.wf_switch_commit.argtypes = [p, i32, i32, p, p]
@@ -576,6 +578,18 @@ def wf_read_probe(src, sink, workgroups, stream=None):
     _check(lib.wf_read_probe(_dev(src, "src"), src.numel() * src.element_size(),
                              _dev(sink, "sink"), sink.numel() * sink.element_size(),
                              int(workgroups), _stream(stream)), "wf_read_probe")
+
+
+def wf_read_probe_series(buf, nbytes, n_bufs, reps, sink, workgroups, depth, stream=None):
+    """Measurement support: reps rounds of plain reads of the n_bufs
+    consecutive nbytes-long pieces of the device tensor buf, launched back
+    to back by the library."""
+    if n_bufs * nbytes > buf.numel() * buf.element_size():
+        raise ValueError("wf_read_probe_series: buf holds fewer than n_bufs pieces")
+    _check(lib.wf_read_probe_series(_dev(buf, "buf"), int(nbytes), int(nbytes), int(n_bufs),
+                                    int(reps), _dev(sink, "sink"),
+                                    sink.numel() * sink.element_size(), int(workgroups),
+                                    int(depth), _stream(stream)), "wf_read_probe_series")
 
 
 def wf_switch_init(active, lazy, prompt_len) -> SwitchState:

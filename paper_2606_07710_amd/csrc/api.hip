@@ -632,6 +632,19 @@ wf_status_t wf_read_probe(const void *src, size_t bytes, void *sink, size_t sink
     return wf::launch_read_probe(src, bytes, sink, workgroups, static_cast<hipStream_t>(stream));
 }
 
+wf_status_t wf_read_probe_series(const void *base, size_t bytes, size_t stride,
+                                 int32_t n_bufs, int32_t reps, void *sink, size_t sink_bytes,
+                                 int32_t workgroups, int32_t depth, void *stream) {
+    if (!base || !sink || !aligned16(base) || !aligned16(sink) || bytes < 16 ||
+        bytes % 16 != 0 || stride < bytes || stride % 16 != 0 || n_bufs < 1 || reps < 1 ||
+        workgroups < 1 || workgroups > 65536 || (depth != 4 && depth != 8))
+        return WF_ERR_INVALID_ARG;
+    if (sink_bytes < (size_t)workgroups * 4096)
+        return WF_ERR_WORKSPACE;
+    return wf::launch_read_probe_series(base, bytes, stride, n_bufs, reps, sink, workgroups,
+                                        depth, static_cast<hipStream_t>(stream));
+}
+
 wf_status_t wf_switch_init(wf_switch_state_t *s, int32_t active, int32_t lazy,
                            int32_t prompt_len) {
     if (!s || prompt_len < 0 || (active != WF_DRAFTER_AR && active != WF_DRAFTER_DIFFUSION) ||

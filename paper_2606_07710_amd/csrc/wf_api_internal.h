@@ -153,6 +153,9 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
 // read [src, src + bytes) once; sink takes workgroups * 4 KB.
 wf_status_t launch_read_probe(const void *src, size_t bytes, void *sink, int workgroups,
                               hipStream_t stream);
+wf_status_t launch_read_probe_series(const void *base, size_t bytes, size_t stride, int n_bufs,
+                                     int reps, void *sink, int workgroups, int depth,
+                                     hipStream_t stream);
 
 // q = RoPE(W_q x) for one token at position pos, q [n_heads][head_dim],
 // on the KV-only prefill kernel (its exchange slots live in the workspace's

@@ -96,6 +96,21 @@ def test_read_probe_rejects(args, status):
     assert wf.lib.wf_read_probe(*args, None) == status
 
 
+@pytest.mark.parametrize("kw,status", [
+    (dict(base=None), 1), (dict(sink=None), 1), (dict(base=ODD), 1), (dict(nbytes=1000), 1),
+    (dict(nbytes=0), 1), (dict(stride=1 << 19), 1), (dict(stride=(1 << 20) + 8), 1),
+    (dict(n_bufs=0), 1), (dict(reps=0), 1), (dict(wgs=0), 1), (dict(wgs=70000), 1),
+    (dict(depth=16), 1), (dict(depth=0), 1), (dict(sink_bytes=4095), 3),
+])
+def test_read_probe_series_rejects(kw, status):
+    a = dict(base=FAKE, nbytes=1 << 20, stride=1 << 20, n_bufs=4, reps=2, sink=FAKE,
+             sink_bytes=1 << 20, wgs=16, depth=4)
+    a.update(kw)
+    assert wf.lib.wf_read_probe_series(a["base"], a["nbytes"], a["stride"], a["n_bufs"],
+                                       a["reps"], a["sink"], a["sink_bytes"], a["wgs"],
+                                       a["depth"], None) == status
+
+
 def _route(**kw):
     a = dict(dt=1, h=FAKE, w=FAKE, draft=FAKE, gamma=16, d=4096, vocab=151936, w1=FAKE,
              b1=FAKE, w2=FAKE, b2=FAKE, m=512, tau=0.5, am=FAKE, ent=FAKE, acc=FAKE,
