@@ -113,6 +113,17 @@ __device__ __forceinline__ void lds_dma16(const void *src, unsigned lds) {
                  : "memory", "m0");
 }
 
+// The same copy addressed as a wave-uniform 64-bit base (SGPRs) plus a
+// 32-bit per-lane byte offset: no per-lane address arithmetic at issue.
+__device__ __forceinline__ void lds_dma16_so(const char *base, unsigned voff, unsigned lds) {
+    asm volatile("s_mov_b32 m0, %2\n\t"
+                 "s_nop 0\n\t"
+                 "global_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(voff), "s"(base), "s"(lds)
+                 : "memory", "m0");
+}
+
 template <int DH, int NBW, int RG, int KS, int NBUF>
 __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) {
     using TG = TileGeom<DH>;
@@ -207,29 +218,58 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     // (j' = j mod kLoadsPerHalf).  A stream whose tile lies past the split
     // (ragged last stage) loads the split's last tile again, so every wave
     // issues the same number of loads per stage; that copy is never used.
+    // Each lane's byte offset within a tile is the same for every tile, so
+    // it is formed once; only a tile reaching past the last key clamps its
+    // keys one by one.
+    auto src_off = [&](int jr, int kl_cap) -> unsigned {
+        const int j = rgi + jr * RG;
+        const bool is_v = j >= TG::kLoadsPerHalf;
+        const int jj = is_v ? j - TG::kLoadsPerHalf : j;
+        const int gidx = jj * kWave + lane;            // granule in the half
+        const int kl = gidx / TG::kGran;                // local key
+        const int pg = gidx % TG::kGran;                // physical granule
+        int lg;                                         // logical granule
+        if (!is_v) {
+            lg = pg ^ (kl & (TG::kGran - 1));
+        } else {
+            const int seg = (pg >> 1) ^ (kl & (TG::kSegs - 1));
+            lg = 2 * seg + (pg & 1);
+        }
+        return (unsigned)(min(kl, kl_cap) * TG::kRowBytes + lg * 16);
+    };
+    // (kept in registers only for up to 8 loads per wave and stage; with
+    // more, the extra registers cost more than the address arithmetic)
+    constexpr bool kKeepOff = LPW <= 8;
+    unsigned voff[kKeepOff ? LPW : 1];
+#pragma unroll
+    for (int jr = 0; jr < (kKeepOff ? LPW : 1); ++jr)
+        voff[jr] = src_off(jr, kTileKeys - 1);
     auto issue = [&](auto bi, int st) __attribute__((always_inline)) {
         const int t = min(KS * st + stream, n_tiles - 1);
         const int kb = k_begin + t * kTileKeys;
         const unsigned slot = lds_addr(ring(bi)) + stream * TG::kTileBytes;
+        const size_t tile_off = (size_t)kb * TG::kRowBytes;
+        auto go = [&](auto clamp_tag) __attribute__((always_inline)) {
 #pragma unroll
-        for (int jr = 0; jr < LPW; ++jr) {
-            const int j = rgi + jr * RG;
-            const bool is_v = j >= TG::kLoadsPerHalf;
-            const int jj = is_v ? j - TG::kLoadsPerHalf : j;
-            const int gidx = jj * kWave + lane;            // granule in the half
-            const int kl = gidx / TG::kGran;                // local key
-            const int pg = gidx % TG::kGran;                // physical granule
-            int lg;                                         // logical granule
-            if (!is_v) {
-                lg = pg ^ (kl & (TG::kGran - 1));
-            } else {
-                const int seg = (pg >> 1) ^ (kl & (TG::kSegs - 1));
-                lg = 2 * seg + (pg & 1);
+            for (int jr = 0; jr < LPW; ++jr) {
+                const int j = rgi + jr * RG;
+                const bool is_v = j >= TG::kLoadsPerHalf;
+                const int jj = is_v ? j - TG::kLoadsPerHalf : j;
+                unsigned off;
+                if constexpr (decltype(clamp_tag)::value)
+                    off = src_off(jr, last_key - kb);
+                else if constexpr (kKeepOff)
+                    off = voff[jr];
+                else
+                    off = src_off(jr, kTileKeys - 1);
+                lds_dma16_so((is_v ? vg : kg) + tile_off, off,
+                             slot + (is_v ? TG::kHalfBytes : 0) + jj * 1024);
             }
-            const int key = min(kb + kl, last_key);
-            const char *src = (is_v ? vg : kg) + (size_t)key * TG::kRowBytes + lg * 16;
-            lds_dma16(src, slot + (is_v ? TG::kHalfBytes : 0) + jj * 1024);
-        }
+        };
+        if (kb + kTileKeys - 1 <= last_key)
+            go(std::false_type{});
+        else
+            go(std::true_type{});
     };
 
     // ---- Q^T operands and causal limits of this wave's rows ------------------
@@ -259,6 +299,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
 
     f32x4 o[MD][NBW];
     float mref[NBW], lrow[NBW];
+    float moff[NBW];                  // -mref * sl2 (0 while mref is -inf)
 
     // Operands of a tile from LDS:
     //   K: ds_read_b128 of (key 16*mb + m16, granule 4*kk + c4).
@@ -352,11 +393,10 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                     }
         }
         // lane-local maxima over the lane's 8 keys of each row
-        float lmx[NBW];
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
-            lmx[nb] = fmaxf(fmaxf(fmaxf(s[0][nb][0], s[0][nb][1]), fmaxf(s[0][nb][2], s[0][nb][3])),
-                            fmaxf(fmaxf(s[1][nb][0], s[1][nb][1]), fmaxf(s[1][nb][2], s[1][nb][3])));
+        auto lane_max = [&](int nb) {
+            return fmaxf(fmaxf(fmaxf(s[0][nb][0], s[0][nb][1]), fmaxf(s[0][nb][2], s[0][nb][3])),
+                         fmaxf(fmaxf(s[1][nb][0], s[1][nb][1]), fmaxf(s[1][nb][2], s[1][nb][3])));
+        };
         auto row_max = [&](float m) {
             m = fmaxf(m, __shfl_xor(m, 16, kWave));
             return fmaxf(m, __shfl_xor(m, 32, kWave));
@@ -365,7 +405,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             float mx[NBW];
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
-                mx[nb] = row_max(lmx[nb]);
+                mx[nb] = row_max(lane_max(nb));
             bool grow = false;
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
@@ -380,12 +420,14 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                     for (int md = 0; md < MD; ++md)
                         o[md][nb] *= alpha;
                     mref[nb] = nr;
+                    moff[nb] = (nr == -INFINITY) ? 0.f : -nr * sl2;
                 }
             }
         } else {
             // The reference maximum of a row is its maximum over the first
             // tile with a visible key (O and l are still zero until then);
-            // only that tile needs the cross-lane reduction.
+            // only that tile needs the lane maxima and the cross-lane
+            // reduction.
             bool unset = false;
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
@@ -393,39 +435,44 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
             if (__ballot(unset)) {
 #pragma unroll
                 for (int nb = 0; nb < NBW; ++nb) {
-                    const float m = row_max(lmx[nb]);
-                    if (mref[nb] == -INFINITY)
+                    const float m = row_max(lane_max(nb));
+                    if (mref[nb] == -INFINITY) {
                         mref[nb] = m;
+                        moff[nb] = (m == -INFINITY) ? 0.f : -m * sl2;
+                    }
                 }
             }
-            // all lanes of a row share its reference, so a lane-local test
-            // catches any growth of the row maximum
-            bool over = false;
-#pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                over |= (lmx[nb] - mref[nb]) * sl2 > 64.f;
-            if (__ballot(over))
-                overflow = 1;                // the workgroup reruns rescaling
         }
         // P = exp2((S - mref) * scale * log2 e) in the P^T operand layout
         bf16x8 pb[NBW];
+        bool over = false;
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb) {
-            const float moff = (mref[nb] == -INFINITY) ? 0.f : -mref[nb] * sl2;
             float p[8];
             float psum = 0.f;
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float e = fast_exp2(fmaf(s[mb][nb][i], sl2, moff));
+                    const float e = fast_exp2(fmaf(s[mb][nb][i], sl2, moff[nb]));
                     p[4 * mb + i] = e;
                     psum += e;
                 }
+            // Without rescaling, a weight above 2^64 means a score outgrew
+            // the row's reference maximum by more than 64 log2 units; the
+            // lane's sum of its non-negative weights exceeds 2^64 whenever
+            // one of them does (and is +inf if one overflowed), so testing
+            // the sum catches every such growth.
+            if constexpr (!RESCALE)
+                over |= psum > 0x1p64f;
             lrow[nb] += psum;
             u32x4 pv = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
                         pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
             pb[nb] = __builtin_bit_cast(bf16x8, pv);
+        }
+        if constexpr (!RESCALE) {
+            if (__ballot(over))
+                overflow = 1;                // the workgroup reruns rescaling
         }
         // O^T += V^T P^T
 #pragma unroll
@@ -466,6 +513,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb) {
             mref[nb] = -INFINITY;
+            moff[nb] = 0.f;
             lrow[nb] = 0.f;
 #pragma unroll
             for (int md = 0; md < MD; ++md)
