@@ -529,21 +529,6 @@ def bench_switch(args, w):
             log(f"{nb} tokens: lazy {lazy * 1e3:.1f} us, per round over {rounds} "
                 f"rounds {per * 1e3:.1f} us")
 
-    # ---- size-matched read floors (not timed with the step) -----------------
-    # a plain read of each kernel's bytes, one launch per call: what the
-    # step would take if every launch only streamed its bytes
-    floors = None
-    if args.read_probe_mib and by["attn_per_layer"] >= (16 << 20):
-        floors = {"attention": size_matched_read_us(wf, dev, by["attn_per_layer"]),
-                  "lmhead": size_matched_read_us(wf, dev, by["lmhead"])}
-        if by["prefill_per_layer"]:
-            floors["prefill"] = size_matched_read_us(wf, dev, by["prefill_per_layer"])
-        floors["step"] = (w.n_layers * (floors["attention"] + floors.get("prefill", 0.0))
-                          + floors["lmhead"])
-        floors = {k: round(v, 2) for k, v in floors.items()}
-        log("size-matched plain reads (us per launch): "
-            + ", ".join(f"{k} {v:.2f}" for k, v in floors.items()))
-
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
