@@ -68,12 +68,11 @@ __device__ __forceinline__ void rope_pair(float &lo, float &hi, double theta, in
 // over its slice of the input dimension for the unit's two 16-feature blocks
 // (f and f + head_dim/2 of one head, K or V); the slices then meet through
 // the exchange tree below.
-template <int DH, int NBT>
+template <int DH, int NBT, int MAXC = kPfMaxChunksPerWave>
 __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
     constexpr int PAIRS = DH / 32;       // 16-feature block pairs per head
     constexpr int TOK = 16 * NBT;
     constexpr int WAVES = 4;
-    constexpr int MAXC = kPfMaxChunksPerWave;
     __shared__ float zs[WAVES][2][16][TOK + 1];
 
     const int unit = blockIdx.x;         // (g, kind, pair)
@@ -140,7 +139,9 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
         for (int nb = 0; nb < NBT; ++nb)
             acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     // wave-strided chunks c = wave, wave + 4, ...; batches of MAXC chunks
-    // whose loads are all issued before the batch's first MFMA
+    // whose loads are all issued before the batch's first MFMA (a single
+    // token's projection takes all of a wave's chunks in one batch: one
+    // memory round trip instead of two)
     for (int cb = wave; cb < n_c; cb += WAVES * MAXC) {
         bf16x8 wr[MAXC][2], xr[MAXC][NBT];
 #pragma unroll
@@ -406,8 +407,13 @@ wf_status_t launch_q_rope(const uint16_t *x, const uint16_t *w_q, uint16_t *q, i
     a.token_blocks = p.token_blocks;
     a.slots = static_cast<unsigned long long *>(workspace);
     dim3 grid(p.units, p.ksplit, p.token_blocks), block(256);
-    if (head_dim == 128)
+    const bool wide = p.chunks_per_split > 4 * kPfMaxChunksPerWave;   // > 8 chunks per wave
+    if (head_dim == 128 && wide)
+        prefill_bf16<128, 1, 2 * kPfMaxChunksPerWave><<<grid, block, 0, stream>>>(a);
+    else if (head_dim == 128)
         prefill_bf16<128, 1><<<grid, block, 0, stream>>>(a);
+    else if (head_dim == 64 && wide)
+        prefill_bf16<64, 1, 2 * kPfMaxChunksPerWave><<<grid, block, 0, stream>>>(a);
     else if (head_dim == 64)
         prefill_bf16<64, 1><<<grid, block, 0, stream>>>(a);
     else
