@@ -350,24 +350,56 @@ def size_matched_read_us(wf, dev, nbytes, total_mib=640, reps=5):
     return best
 
 
-def cpu_baseline(w, layers, head, budget_s, max_layers=None, tree_mask=None):
+def _vec_rel_err(got, ref):
+    """max over output vectors (last axis) of ||got - ref||_inf / ||ref||_inf"""
+    import numpy as np
+    num = np.abs(got - ref).max(axis=-1)
+    return float((num / np.maximum(np.abs(ref).max(axis=-1), 1e-30)).max())
+
+
+def cpu_baseline(w, layers, head, budget_s, max_layers=None, tree_mask=None,
+                 outs=None, lmouts=None, draft=None, tau=None):
     """The oracle as it stands, on host cores, over a bounded sample of the
     step: the LM head, then as many layers of attention and prefill as fit
     in about `budget_s` seconds (all of them if they fit); scaled to one
-    full step."""
+    full step.  With the step's GPU outputs (outs: attention per layer,
+    lmouts: argmax / entropy / accept, the caches in `layers` holding the
+    prefill's rows) it also compares them with the oracle's results of the
+    same inputs -> (check, baseline)."""
+    import numpy as np
+
     import oracle
     import workloads as W
     n = w.ctx_len + w.gamma
     h, wl = W.to_oracle(head["h"]), W.to_oracle(head["w_lm"])
     t0 = time.perf_counter()
-    oracle.lmhead_rows(h, wl)
+    am_ref, ent_ref, margin = oracle.lmhead_rows(h, wl)
     t_lm = time.perf_counter() - t0
     del h, wl
+    check = {}
+    bar = 2e-2 if w.dtype == "bf16" else 1e-4
+    amar = 1e-2 if w.dtype == "bf16" else 1e-6
+
+    def lm_check(key, outs3, a_ref, e_ref, mg):
+        am, ent, acc = (t.cpu().numpy() for t in outs3)
+        sure = mg > amar
+        check[key + "_argmax_mismatches"] = int((am[sure] != a_ref[sure]).sum())
+        check[key + "_entropy_rel_err"] = float(
+            (np.abs(ent - e_ref) / np.maximum(np.abs(e_ref), 1e-3)).max())
+        if tree_mask is None and draft is not None and bool(sure.all()):
+            n_ref, bonus_ref, route_ref, _ = oracle.accept(a_ref, e_ref, draft, tau)
+            check[key + "_accept_matches"] = bool(
+                (int(acc[0]), int(acc[1]), int(acc[2])) == (n_ref, bonus_ref, route_ref))
+
+    if lmouts is not None:
+        lm_check("lmhead", lmouts[0], am_ref, ent_ref, margin)
     if w.router_logits:
         z = head["router_logits"].cpu().numpy()
         t0 = time.perf_counter()
-        oracle.lmhead_rows(logits=z)
+        a2, e2, m2 = oracle.lmhead_rows(logits=z)
         t_lm += time.perf_counter() - t0
+        if lmouts is not None:
+            lm_check("logits_only", lmouts[1], a2, e2, m2)
     log(f"cpu baseline: LM head {t_lm:.2f}s")
     t_attn = t_pre = 0.0
     done = 0
@@ -379,17 +411,27 @@ def cpu_baseline(w, layers, head, budget_s, max_layers=None, tree_mask=None):
         v = W.to_oracle(t["v_cache"][:, :n].contiguous())
         t0 = time.perf_counter()
         if tree_mask is None:
-            oracle.verify_attn(q, k, v, w.ctx_len)
+            o_ref = oracle.verify_attn(q, k, v, w.ctx_len)
         else:
-            oracle.verify_attn_mask(q, k, v, w.ctx_len, tree_mask)
+            o_ref = oracle.verify_attn_mask(q, k, v, w.ctx_len, tree_mask)
         t_attn += time.perf_counter() - t0
         del q, k, v
+        if outs is not None:
+            e = _vec_rel_err(outs[done].float().cpu().numpy().astype(np.float64), o_ref)
+            check["attention_max_rel_err"] = max(check.get("attention_max_rel_err", 0.0), e)
         if w.n_prefill:
             x, wk, wv = (W.to_oracle(t[k_]) for k_ in ("x", "w_k", "w_v"))
             t0 = time.perf_counter()
-            oracle.kv_only_prefill(x, wk, wv, w.prefill_start, w.n_kv_heads,
-                                   w.head_dim, w.rope_base)
+            k_ref, v_ref = oracle.kv_only_prefill(x, wk, wv, w.prefill_start, w.n_kv_heads,
+                                                  w.head_dim, w.rope_base)
             t_pre += time.perf_counter() - t0
+            if outs is not None:
+                kc = t["drafter_k_cache"] if w.separate_drafter_cache else t["k_cache"]
+                vc = t["drafter_v_cache"] if w.separate_drafter_cache else t["v_cache"]
+                rows = slice(w.prefill_start, w.prefill_start + w.n_prefill)
+                e = max(_vec_rel_err(kc[:, rows].float().cpu().numpy().astype(np.float64), k_ref),
+                        _vec_rel_err(vc[:, rows].float().cpu().numpy().astype(np.float64), v_ref))
+                check["prefill_max_rel_err"] = max(check.get("prefill_max_rel_err", 0.0), e)
         done += 1
         spent = t_lm + t_attn + t_pre
         log(f"cpu baseline: layer {done - 1} done ({spent:.1f}s)")
@@ -397,7 +439,17 @@ def cpu_baseline(w, layers, head, budget_s, max_layers=None, tree_mask=None):
             break
     per_step_s = (t_attn + t_pre) / done * w.n_layers + t_lm
     whole = done == w.n_layers
-    return {
+    if check:
+        check["layers_checked"] = done
+        check["tolerance"] = bar
+        check["ok"] = bool(
+            check.get("attention_max_rel_err", 0.0) <= bar
+            and check.get("prefill_max_rel_err", 0.0) <= bar
+            and all(v == 0 for k_, v in check.items() if k_.endswith("_mismatches"))
+            and all(v for k_, v in check.items() if k_.endswith("_accept_matches"))
+            and all(v <= bar for k_, v in check.items() if k_.endswith("_entropy_rel_err")))
+        log("oracle check of the step's outputs: " + json.dumps(check))
+    return check or None, {
         "value": round(per_step_s * 1e6, 1),
         "unit": "us",
         "cores": oracle.num_threads(),
@@ -842,12 +894,14 @@ def main():
         log("size-matched plain reads (us per launch): "
             + ", ".join(f"{k} {v:.2f}" for k, v in floors.items()))
 
-    cpu = None
+    cpu = check = None
     if not args.no_cpu_baseline:
         log(f"cpu baseline: about {args.cpu_budget_s:.0f}s of oracle work ...")
-        cpu = cpu_baseline(w, layers, head, args.cpu_budget_s,
-                           args.cpu_sample_layers,
-                           W.ancestor_masks(tree["parents_np"]) if tree else None)
+        check, cpu = cpu_baseline(w, layers, head, args.cpu_budget_s,
+                                  args.cpu_sample_layers,
+                                  W.ancestor_masks(tree["parents_np"]) if tree else None,
+                                  outs=outs, lmouts=lmouts, draft=draft.cpu().numpy(),
+                                  tau=tau)
 
     line = {
         "metric": "verify-step us and achieved HBM GB/s (gamma=16, 32K ctx, "
@@ -921,6 +975,9 @@ def main():
             "mfma_busy_counter": measured_mfma_busy() if w.cfg == 3 else None,
         },
         "cpu_baseline": cpu,
+        # the timed step's own outputs against the oracle's for the same
+        # inputs (the layers the baseline's time budget covered)
+        "oracle_check": check,
     }
     print(json.dumps(line), flush=True)
 
