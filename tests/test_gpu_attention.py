@@ -108,14 +108,18 @@ def test_row_i_equals_decode_on_prefix_i(dt):
         assert max_vec_rel_err(a, b) <= SAME_MATH_TOL[dt], i
 
 
-@pytest.mark.parametrize("dt", ["bf16", "f32"])
-def test_split_count_invariance_and_determinism(dt):
-    gamma, ctx, hq, hkv, dh = 16, 3000, 32, 8, 128
+# split counts on both sides of the one-round-trip merge's limit (32
+# splits at head_dim 128, 64 at head_dim 64; more go to the general merge)
+@pytest.mark.parametrize("dt,dh,splits", [
+    ("bf16", 128, (2, 5, 11, 17, 32, 33, 48, 0)), ("f32", 128, (2, 5, 11, 17, 32, 33, 0)),
+    ("bf16", 64, (2, 17, 64, 65, 0))])
+def test_split_count_invariance_and_determinism(dt, dh, splits):
+    gamma, ctx, hq, hkv = 16, 3000, 32, 8
     q, k, v = _inputs(dt, gamma, ctx, hq, hkv, dh, seed=31, std=1.28)
     ref = oracle.verify_attn(W.to_oracle(q), W.to_oracle(k[:, :ctx + gamma].contiguous()),
                              W.to_oracle(v[:, :ctx + gamma].contiguous()), ctx)
     base = _run(q, k, v, ctx, splits=1)
-    for s in (2, 5, 11, 17, 0):
+    for s in splits:
         o = _run(q, k, v, ctx, splits=s)
         assert max_vec_rel_err(host64(o), ref) <= TOL[dt], s
         assert max_vec_rel_err(host64(o), host64(base)) <= SAME_MATH_TOL[dt], s
