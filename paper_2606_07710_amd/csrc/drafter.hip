@@ -262,7 +262,7 @@ namespace {
 wf_status_t drafter_forward(const wf_decoder_layer_t &L, const uint16_t *rb, int M, int pos,
                             void *k_cache, void *v_cache, int cap, void *out,
                             void *workspace, hipStream_t stream, bool tiled,
-                            const uint16_t *xn_given) {
+                            const uint16_t *xn_given, bool q_ready = false) {
     const wf_dtype_t wdt = tiled ? WF_BF16_TILED : WF_BF16;
     const DrafterLayout o = drafter_layout(L, M, pos);
     char *ws = static_cast<char *>(workspace);
@@ -292,7 +292,9 @@ wf_status_t drafter_forward(const wf_decoder_layer_t &L, const uint16_t *rb, int
         // epilogue -- RoPE, a residual, or the MLP's RMSNorm and SwiGLU --
         // so the layer is five launches after the K/V: W_q, attention (two),
         // W_o, [W_gate; W_up], W_down.
-        if ((st = launch_q_rope(xn, W(L.w_q), q, d, L.n_q_heads, L.head_dim, pos,
+        // (q_ready: the caller has already formed q in the layout's slot)
+        if (!q_ready &&
+            (st = launch_q_rope(xn, W(L.w_q), q, d, L.n_q_heads, L.head_dim, pos,
                                 L.rope_base, workspace, stream, tiled)) != WF_OK)
             return st;
         st = launch_attn(WF_BF16, q, k_cache, v_cache, a, 1, pos, cap, L.n_q_heads,
@@ -362,16 +364,30 @@ wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, i
                                    void *workspace, hipStream_t stream, bool tiled) {
     const int d = L.hidden;
     const auto *rb = static_cast<const uint16_t *>(r);
-    char *tail = static_cast<char *>(workspace) +
-                 align256(drafter_forward_workspace_bytes(L, 1, pos + n - 1));
+    const DrafterLayout lay = drafter_layout(L, 1, pos + n - 1);
+    char *tail = static_cast<char *>(workspace) + align256(lay.total);
     auto *xnb = reinterpret_cast<uint16_t *>(tail);
     auto *xnt = reinterpret_cast<uint16_t *>(tail + align256((size_t)n * d * 2));
+    const uint16_t *x_last = xnb + (size_t)(n - 1) * d;
     rmsnorm_bf16<<<(n + 15) / 16 * 16, kNormThreads, 0, stream>>>(
         rb, static_cast<const uint16_t *>(L.attn_norm), L.rms_eps, xnb, d, n, xnt);
-    // the whole backlog's K/V in batches of at most kCatchupChunk tokens
-    // (one KV-only prefill each; a single batch for any backlog up to that),
-    // reading the tiled rows (a batch starts on a 16-row tile boundary)
-    for (int c0 = 0; c0 < n; c0 += kCatchupChunk) {
+    // A backlog of one batch: its K/V and the last token's q in one launch
+    // (they only share the normalised rows).
+    bool q_ready = false;
+    if (n <= kCatchupChunk) {
+        const wf_status_t st = launch_prefill_and_q(
+            tiled, xnt, L.w_k, L.w_v, k_cache, v_cache, n, pos, cap, d, L.n_kv_heads, x_last,
+            static_cast<const uint16_t *>(L.w_q),
+            reinterpret_cast<uint16_t *>(static_cast<char *>(workspace) + lay.q), L.n_q_heads,
+            L.head_dim, pos + n - 1, L.rope_base, workspace, stream);
+        if (st != WF_OK && st != WF_ERR_UNSUPPORTED)
+            return st;
+        q_ready = st == WF_OK;
+    }
+    // otherwise the whole backlog's K/V in batches of at most kCatchupChunk
+    // tokens (one KV-only prefill each), reading the tiled rows (a batch
+    // starts on a 16-row tile boundary), and q in the layer below
+    for (int c0 = 0; !q_ready && c0 < n; c0 += kCatchupChunk) {
         const int m = std::min(kCatchupChunk, n - c0);
         const wf_status_t st = launch_prefill(tiled ? WF_BF16_TILED : WF_BF16,
                                               xnt + (size_t)c0 * d, L.w_k, L.w_v, k_cache,
@@ -382,7 +398,7 @@ wf_status_t launch_drafter_catchup(const wf_decoder_layer_t &L, const void *r, i
             return st;
     }
     return drafter_forward(L, rb + (size_t)(n - 1) * d, 1, pos + n - 1, k_cache, v_cache, cap,
-                           out, workspace, stream, tiled, xnb + (size_t)(n - 1) * d);
+                           out, workspace, stream, tiled, x_last, q_ready);
 }
 
 }  // namespace wf

@@ -68,17 +68,18 @@ __device__ __forceinline__ void rope_pair(float &lo, float &hi, double theta, in
 // over its slice of the input dimension for the unit's two 16-feature blocks
 // (f and f + head_dim/2 of one head, K or V); the slices then meet through
 // the exchange tree below.
-template <int DH, int NBT, int MAXC = kPfMaxChunksPerWave>
-__global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
+// The body takes its workgroup's grid coordinates explicitly, so one launch
+// can run two such problems side by side (prefill_pair_bf16).
+template <int DH, int NBT, int MAXC>
+__device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, int ks, int bz,
+                                             int n_units, int ksplit) {
     constexpr int PAIRS = DH / 32;       // 16-feature block pairs per head
     constexpr int TOK = 16 * NBT;
     constexpr int WAVES = 4;
     __shared__ float zs[WAVES][2][16][TOK + 1];
 
-    const int unit = blockIdx.x;         // (g, kind, pair)
-    const int ks = blockIdx.y;
-    const int tb = blockIdx.z % a.token_blocks;
-    const int layer = blockIdx.z / a.token_blocks;
+    const int tb = bz % a.token_blocks;
+    const int layer = bz / a.token_blocks;
     const int pair = unit % PAIRS;
     const int kind = a.kinds == 2 ? (unit / PAIRS) % 2 : 0;   // 0 = K, 1 = V
     const int g = unit / (a.kinds * PAIRS);
@@ -191,9 +192,8 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
     // them at once: one exchange round trip per tree level, not per pair.
     constexpr int NI = 16 * TOK / 256;
     static_assert(16 * TOK % 256 == 0, "pairs per workgroup must fill the 256 threads");
-    const int ksplit = gridDim.y;
     const size_t ub =                                          // (layer, unit, token block)
-        ((size_t)layer * gridDim.x + unit) * a.token_blocks + tb;
+        ((size_t)layer * n_units + unit) * a.token_blocks + tb;
     unsigned long long *slots = a.slots + ub * (size_t)(ksplit - 1) * (16 * TOK);
     uint16_t *cache = static_cast<uint16_t *>(kind ? a.v_cache : a.k_cache) + layer * a.c_ls;
     float lo[NI], hi[NI];
@@ -255,6 +255,32 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
         uint16_t *row = cache + ((size_t)g * a.cap + pos) * DH;
         row[16 * pair + e] = f32_to_bf16(l);
         row[DH / 2 + 16 * pair + e] = f32_to_bf16(h);
+    }
+}
+
+template <int DH, int NBT, int MAXC = kPfMaxChunksPerWave>
+__global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
+    prefill_body<DH, NBT, MAXC>(a, blockIdx.x, blockIdx.y, blockIdx.z, gridDim.x, gridDim.y);
+}
+
+// Two independent projections in one launch: workgroups [0, n1) run the
+// first problem's grid (units1 x ks1 x z1, flattened), the rest the
+// second's.  Each keeps its own exchange slots (disjoint parts of the zero
+// block).  The drafter catch-up runs the backlog's K/V and the last token's
+// q this way: one launch instead of two back to back.
+template <int DH, int NBT1, int MAXC1, int NBT2, int MAXC2>
+__global__ __launch_bounds__(256) void prefill_pair_bf16(PrefillParams a1, PrefillParams a2,
+                                                         int units1, int ks1, int z1,
+                                                         int units2, int ks2) {
+    const int b = blockIdx.x;
+    const int n1 = units1 * ks1 * z1;
+    if (b < n1) {
+        prefill_body<DH, NBT1, MAXC1>(a1, b % units1, (b / units1) % ks1, b / (units1 * ks1),
+                                      units1, ks1);
+    } else {
+        const int c = b - n1;
+        prefill_body<DH, NBT2, MAXC2>(a2, c % units2, (c / units2) % ks2, c / (units2 * ks2),
+                                      units2, ks2);
     }
 }
 
@@ -387,6 +413,56 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
     if (hipGetLastError() != hipSuccess)
         return WF_ERR_HIP;
     return WF_OK;
+}
+
+// The drafter catch-up's first two projections in one launch: the KV-only
+// prefill of the backlog's n_tok tiled rows (as launch_prefill with a tiled
+// x) and q = RoPE(W_q x_last) of the last token (as launch_q_rope), the two
+// sets of exchange slots in the lower and upper halves of the zero block.
+// WF_ERR_UNSUPPORTED when either set needs more than its half (the caller
+// then launches the two one after the other).
+wf_status_t launch_prefill_and_q(bool tiled, const uint16_t *x_rows, const void *w_k,
+                                 const void *w_v, void *k_cache, void *v_cache, int n_tok,
+                                 int start_pos, int cap, int d_in, int n_kv_heads,
+                                 const uint16_t *x_last, const uint16_t *w_q, uint16_t *q,
+                                 int n_q_heads, int head_dim, int q_pos, double rope_base,
+                                 void *workspace, hipStream_t stream) {
+    constexpr size_t kHalf = kCounterBytes / 2;
+    PrefillParams a1{x_rows, w_k, w_v, k_cache, v_cache, n_tok, start_pos, cap, d_in,
+                     n_kv_heads, {}, nullptr, 0, 1, 0, 0, 0, tiled ? 1 : 0, 2, 0, 1};
+    PrefillParams a2{x_last, w_q, w_q, q, q, 1, 0, 1, d_in, n_q_heads, {}, nullptr, 0, 1, 0, 0, 0,
+                     tiled ? 1 : 0, 1, q_pos, 0};
+    for (int i = 0; i < head_dim / 2; ++i)
+        a1.theta[i] = a2.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
+    const PrefillPlan p1 = plan_prefill(n_tok, d_in, n_kv_heads, head_dim, 1);
+    const PrefillPlan p2 = plan_prefill(1, d_in, n_q_heads, head_dim, 1, 1);
+    if (prefill_slot_bytes(p1, 1) > kHalf || prefill_slot_bytes(p2, 1) > kHalf)
+        return WF_ERR_UNSUPPORTED;
+    a1.chunks_per_split = p1.chunks_per_split;
+    a1.token_blocks = p1.token_blocks;
+    a1.slots = static_cast<unsigned long long *>(workspace);
+    a2.chunks_per_split = p2.chunks_per_split;
+    a2.token_blocks = p2.token_blocks;
+    a2.slots = reinterpret_cast<unsigned long long *>(static_cast<char *>(workspace) + kHalf);
+    const long long n1 = (long long)p1.units * p1.ksplit * p1.token_blocks;
+    const long long n2 = (long long)p2.units * p2.ksplit * p2.token_blocks;
+    const dim3 grid((unsigned)(n1 + n2)), block(256);
+    const bool wide2 = p2.chunks_per_split > 4 * kPfMaxChunksPerWave;
+    constexpr int M8 = kPfMaxChunksPerWave, M16 = 2 * kPfMaxChunksPerWave;
+#define WF_PAIR_CASE(DHV, NBV)                                                              \
+    if (head_dim == DHV && p1.nbt == NBV) {                                                 \
+        if (wide2)                                                                          \
+            prefill_pair_bf16<DHV, NBV, M8, 1, M16><<<grid, block, 0, stream>>>(            \
+                a1, a2, p1.units, p1.ksplit, p1.token_blocks, p2.units, p2.ksplit);         \
+        else                                                                                \
+            prefill_pair_bf16<DHV, NBV, M8, 1, M8><<<grid, block, 0, stream>>>(             \
+                a1, a2, p1.units, p1.ksplit, p1.token_blocks, p2.units, p2.ksplit);         \
+    } else
+    WF_PAIR_CASE(128, 1) WF_PAIR_CASE(128, 2) WF_PAIR_CASE(128, 3) WF_PAIR_CASE(128, 4)
+    WF_PAIR_CASE(64, 1) WF_PAIR_CASE(64, 2) WF_PAIR_CASE(64, 3) WF_PAIR_CASE(64, 4)
+    { return WF_ERR_UNSUPPORTED; }
+#undef WF_PAIR_CASE
+    return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
 }
 
 // q = RoPE(W_q x) for one token: the K half of the kernel above with the

@@ -164,6 +164,16 @@ wf_status_t launch_q_rope(const uint16_t *x, const uint16_t *w_q, uint16_t *q, i
                           int n_heads, int head_dim, int pos, double rope_base,
                           void *workspace, hipStream_t stream, bool tiled);
 
+// The KV-only prefill of n_tok tiled rows and q = RoPE(W_q x_last) in one
+// launch (their exchange slots in the two halves of the zero block);
+// WF_ERR_UNSUPPORTED if they do not fit there.
+wf_status_t launch_prefill_and_q(bool tiled, const uint16_t *x_rows, const void *w_k,
+                                 const void *w_v, void *k_cache, void *v_cache, int n_tok,
+                                 int start_pos, int cap, int d_in, int n_kv_heads,
+                                 const uint16_t *x_last, const uint16_t *w_q, uint16_t *q,
+                                 int n_q_heads, int head_dim, int q_pos, double rope_base,
+                                 void *workspace, hipStream_t stream);
+
 // Tiled bf16 weights (16x32 tiles of 1 KB, one wave operand load each).
 size_t tiled_weight_bytes(int rows, int cols);
 wf_status_t launch_tile_weights(const void *w, int rows, int cols, void *tiled,
