@@ -72,3 +72,31 @@ def lmhead_cases(n=30, seed=20260604):
         out.append(dict(case=case, dt=dt, tiled=tiled, gamma=gamma, d=d, vocab=vocab,
                         w_std=ws, seed=3000 + case))
     return out
+
+
+DRAFTER_HEADS = [(1, 1), (2, 1), (4, 2), (4, 4), (6, 3), (8, 2), (12, 4)]
+
+
+def drafter_cases(n=16, seed=20260605):
+    """One drafter decoder layer: the full layer over 1..64 tokens
+    (`forward`) or a lazy catch-up over a backlog of 1..400 (`catchup`);
+    hidden and SwiGLU widths multiples of 32, head_dim 64 or 128, row-major
+    or tiled projections."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for case in range(n):
+        kind = "catchup" if rng.random() < 0.6 else "forward"
+        hq, hkv = DRAFTER_HEADS[int(rng.integers(len(DRAFTER_HEADS)))]
+        dh = int(rng.choice([64, 128]))
+        hidden = 32 * int(rng.integers(4, 49))
+        inter = 32 * int(rng.integers(4, 97))
+        pos = int(rng.choice([rng.integers(0, 40), rng.integers(40, 2500)]))
+        if kind == "catchup":
+            n_tok = int(rng.choice([rng.integers(1, 17), rng.integers(17, 101),
+                                    rng.integers(101, 401)]))
+        else:
+            n_tok = int(rng.integers(1, 65))
+        tiled = bool(rng.random() < 0.5)
+        out.append(dict(case=case, kind=kind, hq=hq, hkv=hkv, dh=dh, hidden=hidden,
+                        inter=inter, pos=pos, n=n_tok, tiled=tiled, cfg=5000 + case))
+    return out

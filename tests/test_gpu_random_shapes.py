@@ -1,12 +1,15 @@
 """Seeded random-shape GPU parity sweep against the fp64 oracle: verify
 attention (block-causal and tree masks, Sec. 3.2), KV-only prefill (Sec.
-3.4) and the LM head with acceptance and entropy (Sec. 3.3.1), over shapes
+3.4), the LM head with acceptance and entropy (Sec. 3.3.1) and the drafter
+layer of the switch path (full layer and lazy catch-up, Sec. 3.4), over shapes
 drawn from the ranges the C ABI accepts (tests/random_cases.py: gamma 1..64,
 ragged context and vocabulary, head_dim 64 and 128, fp32 and bf16,
 row-major and tiled weights).  Each test runs a bounded number of cases
 from a fixed seed, prints every case before it runs, and stops at the first
 mismatch.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -113,3 +116,52 @@ def test_lmhead_random_shapes():
             assert (acc[0], acc[1]) == (n_ref, bonus_ref), c["case"]
             if abs(ent_ref[n_ref] - tau) > TOL[dt] * max(abs(ent_ref[n_ref]), 1e-3):
                 assert acc[2] == route_ref, c["case"]
+
+
+def test_drafter_random_shapes():
+    """The drafter layer (Sec. 3.4 switch path): full layer over a few
+    tokens or lazy catch-up over a backlog, against the oracle; written
+    cache rows within the bar, every other row unchanged bit for bit."""
+    for c in R.drafter_cases():
+        print(f"random drafter #{c['case']}: {c['kind']} hidden={c['hidden']} "
+              f"heads={c['hq']}/{c['hkv']}x{c['dh']} inter={c['inter']} pos={c['pos']} "
+              f"n={c['n']} tiled={c['tiled']}", flush=True)
+        hidden, hq, hkv, pos, n = c["hidden"], c["hq"], c["hkv"], c["pos"], c["n"]
+        w = dataclasses.replace(W.CONFIGS[7], cfg=c["cfg"], hidden=hidden, n_q_heads=hq,
+                                n_kv_heads=hkv, head_dim=c["dh"], inter=c["inter"],
+                                ctx_len=pos, n_prefill=n, prefill_start=pos,
+                                prefill_cap=pos + n, qkv_std=0.02 * np.sqrt(hidden))
+        t = W.generate_drafter(w, device=DEV)
+        spare = lambda x: torch.cat([x, torch.full((x.shape[0], 2, x.shape[2]), 7.0,
+                                                   dtype=x.dtype, device=DEV)], dim=1)
+        kc, vc = spare(t["k_cache"]), spare(t["v_cache"])
+        kc0, vc0 = kc.clone(), vc.clone()
+        names = W.DECODER_WEIGHTS
+        weights = {k: (t[k] if k.endswith("norm") or not c["tiled"] else wf.tile_weights(t[k]))
+                   for k in names}
+        layer = wf.decoder_layer(weights, hq, hkv, w.rms_eps, w.rope_base)
+        host = {k: W.to_oracle(t[k]) for k in names}
+        if c["kind"] == "catchup":
+            out = torch.empty(hidden, dtype=torch.bfloat16, device=DEV)
+            wf.wf_drafter_catchup(layer, t["r"], pos, kc, vc, out)
+            torch.cuda.synchronize()
+            ref, kref, vref = oracle.catchup(W.to_oracle(t["r"]), pos, host, W.to_oracle(kc0),
+                                             W.to_oracle(vc0), hq, hkv, w.rms_eps, w.rope_base)
+            got, ref = host64(out)[None], ref[None]
+        else:
+            out = torch.empty((n, hidden), dtype=torch.bfloat16, device=DEV)
+            wf.wf_drafter_forward(layer, t["r"], pos, kc, vc, out)
+            torch.cuda.synchronize()
+            ref, kref, vref = oracle.decoder_forward(
+                W.to_oracle(t["r"]), pos, host, W.to_oracle(kc0), W.to_oracle(vc0),
+                hq, hkv, w.rms_eps, w.rope_base)
+            got = host64(out)
+        assert np.isfinite(got).all(), c["case"]
+        err = max_vec_rel_err(got, ref)
+        assert err <= TOL["bf16"], (c["case"], "out", err)
+        for name, g, g0, r in (("k", kc, kc0, kref), ("v", vc, vc0, vref)):
+            e = max_vec_rel_err(host64(g)[:, pos:pos + n], r[:, pos:pos + n])
+            assert e <= TOL["bf16"], (c["case"], name, e)
+            before, after = g0.view(torch.int16).cpu(), g.view(torch.int16).cpu()
+            assert torch.equal(before[:, :pos], after[:, :pos]), (c["case"], name)
+            assert torch.equal(before[:, pos + n:], after[:, pos + n:]), (c["case"], name)

@@ -1,6 +1,8 @@
 """Host-side check of the GPU random-shape sweep's cases (tests/random_cases.py):
 every drawn shape lies in the ranges the C ABI accepts, so the sweep tests
 the kernels rather than argument validation.  No GPU call is made."""
+import ctypes
+
 import pytest
 
 import random_cases as R
@@ -42,3 +44,27 @@ def test_lmhead_cases_are_accepted():
             assert c["d"] % 32 == 0
         if c["tiled"]:
             assert c["d"] % 512 == 0 or (c["gamma"] <= 16 and c["d"] in (4096, 5120))
+
+
+def test_drafter_cases_are_accepted():
+    cases = R.drafter_cases()
+    assert {c["kind"] for c in cases} == {"catchup", "forward"}
+    assert any(c["tiled"] for c in cases) and any(not c["tiled"] for c in cases)
+    assert {c["dh"] for c in cases} == {64, 128}
+    for c in cases:
+        assert c["hidden"] % 32 == 0 and c["inter"] % 32 == 0
+        assert c["hq"] % c["hkv"] == 0
+        # the workspace queries read only the layer's shapes: stand-in
+        # pointers (never dereferenced) give its shape struct
+        fake = [4096] * len(wf.DECODER_WEIGHTS)
+        layer = wf.DecoderLayer(*fake, c["hidden"], c["hq"], c["hkv"], c["dh"],
+                                c["inter"], 1e-6, 1e6)
+        code = wf.WF_BF16_TILED if c["tiled"] else wf.WF_BF16
+        if c["kind"] == "catchup":
+            need = wf.lib.wf_drafter_catchup_workspace_bytes(code, ctypes.byref(layer),
+                                                             c["n"], c["pos"])
+        else:
+            assert 1 <= c["n"] <= 64
+            need = wf.lib.wf_drafter_forward_workspace_bytes(code, ctypes.byref(layer),
+                                                             c["n"], c["pos"])
+        assert need > 0, c
