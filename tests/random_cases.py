@@ -100,3 +100,21 @@ def drafter_cases(n=16, seed=20260605):
         out.append(dict(case=case, kind=kind, hq=hq, hkv=hkv, dh=dh, hidden=hidden,
                         inter=inter, pos=pos, n=n_tok, tiled=tiled, cfg=5000 + case))
     return out
+
+
+def router_cases(n=24, seed=20260606):
+    """The neural routing policy's MLP (d -> m -> GELU -> 1) over gamma
+    rows: bf16 with d % 32 == 0 and m % 16 == 0, or fp32 of any size."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for case in range(n):
+        dt = "bf16" if rng.random() < 0.75 else "f32"
+        gamma = int(rng.integers(1, 65))
+        if dt == "bf16":
+            d = 32 * int(rng.integers(1, 161))
+            m = 16 * int(rng.integers(1, 65))
+        else:
+            d = int(rng.integers(1, 700))
+            m = int(rng.integers(1, 300))
+        out.append(dict(case=case, dt=dt, gamma=gamma, d=d, m=m, seed=6000 + case))
+    return out

@@ -1,7 +1,8 @@
 """Seeded random-shape GPU parity sweep against the fp64 oracle: verify
 attention (block-causal and tree masks, Sec. 3.2), KV-only prefill (Sec.
-3.4), the LM head with acceptance and entropy (Sec. 3.3.1) and the drafter
-layer of the switch path (full layer and lazy catch-up, Sec. 3.4), over shapes
+3.4), the LM head with acceptance and entropy (Sec. 3.3.1), the drafter
+layer of the switch path (full layer and lazy catch-up, Sec. 3.4) and the
+neural routing policy (Sec. 3.3.2), over shapes
 drawn from the ranges the C ABI accepts (tests/random_cases.py: gamma 1..64,
 ragged context and vocabulary, head_dim 64 and 128, fp32 and bf16,
 row-major and tiled weights).  Each test runs a bounded number of cases
@@ -9,6 +10,7 @@ from a fixed seed, prints every case before it runs, and stops at the first
 mismatch.
 """
 import dataclasses
+import math
 
 import numpy as np
 import pytest
@@ -165,3 +167,42 @@ def test_drafter_random_shapes():
             before, after = g0.view(torch.int16).cpu(), g.view(torch.int16).cpu()
             assert torch.equal(before[:, :pos], after[:, :pos]), (c["case"], name)
             assert torch.equal(before[:, pos + n:], after[:, pos + n:]), (c["case"], name)
+
+
+def _router_scale(h, w1, b1, w2, b2):
+    """|b2| + sum_u |w2_u GELU(z_u)| per row: the size of the terms the
+    predicted gain sums, which bounds its rounding error."""
+    h, w1, b1, w2, b2 = (t.double().cpu().numpy() for t in (h, w1, b1, w2, b2))
+    z = h @ w1.T + b1
+    g = 0.5 * z * (1.0 + np.vectorize(math.erf)(z / math.sqrt(2.0)))
+    return np.abs(b2[0]) + np.abs(g * w2).sum(axis=1)
+
+
+def test_router_random_shapes():
+    """The neural routing policy (Sec. 3.3.2): the predicted gain of every
+    row within the router's bar (TOL x the size of the terms it sums) and
+    the route at a device-named row, against the oracle."""
+    for c in R.router_cases():
+        print(f"random router #{c['case']}: {c['dt']} gamma={c['gamma']} d={c['d']} "
+              f"m={c['m']}", flush=True)
+        dt, gamma, d, m, seed = c["dt"], c["gamma"], c["d"], c["m"], c["seed"]
+        h = W.normal((gamma, d), 1.0, W.stream_seed(seed, "h"), DT[dt], DEV)
+        w1 = W.normal((m, d), 0.02, W.stream_seed(seed, "router_w1"), DT[dt], DEV)
+        b1 = W.normal((m,), 0.02, W.stream_seed(seed, "router_b1"), DT[dt], DEV)
+        w2 = W.normal((m,), 0.05, W.stream_seed(seed, "router_w2"), DT[dt], DEV)
+        b2 = W.normal((1,), 0.05, W.stream_seed(seed, "router_b2"), DT[dt], DEV)
+        ref = oracle.router_mlp(*(W.to_oracle(t) for t in (h, w1, b1, w2, b2)))
+        scale = _router_scale(h, w1, b1, w2, b2)
+        tau = float(np.float32(np.median(ref)))
+        row = gamma - 1 - c["case"] % gamma
+        rowt = torch.tensor([row], dtype=torch.int32, device=DEV)
+        delta = torch.empty(gamma, dtype=torch.float32, device=DEV)
+        route = torch.empty(1, dtype=torch.int32, device=DEV)
+        wf.wf_router_neural(h, w1, b1, w2, b2, rowt, tau, delta, route)
+        torch.cuda.synchronize()
+        got = delta.cpu().numpy().astype(np.float64)
+        assert np.isfinite(got).all(), c["case"]
+        assert np.all(np.abs(got - ref) <= TOL[dt] * scale), (c["case"], np.abs(got - ref).max())
+        assert int(route[0]) == int(got[row] > tau), c["case"]
+        if abs(ref[row] - tau) > TOL[dt] * scale[row]:
+            assert int(route[0]) == oracle.route_neural(ref, row, tau), c["case"]

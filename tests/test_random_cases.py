@@ -68,3 +68,14 @@ def test_drafter_cases_are_accepted():
             need = wf.lib.wf_drafter_forward_workspace_bytes(code, ctypes.byref(layer),
                                                              c["n"], c["pos"])
         assert need > 0, c
+
+
+def test_router_cases_are_accepted():
+    cases = R.router_cases()
+    assert {c["dt"] for c in cases} == {"f32", "bf16"}
+    for c in cases:
+        code = wf.WF_F32 if c["dt"] == "f32" else wf.WF_BF16
+        assert 1 <= c["gamma"] <= 64 and c["d"] >= 1 and 1 <= c["m"] <= 65536
+        if c["dt"] == "bf16":
+            assert c["d"] % 32 == 0 and c["m"] % 16 == 0
+        assert wf.lib.wf_router_workspace_bytes(code, c["gamma"], c["d"], c["m"]) > 0, c
