@@ -56,3 +56,23 @@ def accept_is_consistent(n, bonus, route, argmax, entropy, draft, tau):
     while k < gamma - 1 and draft[k] == argmax[k]:
         k += 1
     return n == k and bonus == argmax[k] and route == int(entropy[k] > tau)
+
+
+def check_tree_accept(am, ent, acc, path, am_ref, ent_ref, margin, tok, par, tau, bar):
+    """Tree acceptance (Sec. 3.1 draft trees, Sec. 3.3.1 route): the GPU's
+    accept outputs follow exactly from its own argmax and entropy; and
+    wherever the oracle's margins on its accepted path exceed the bar (so
+    both sides agree on those argmaxes), they equal the oracle's.  Returns
+    the oracle's acceptance."""
+    import oracle
+    own = oracle.accept_tree(am, ent.astype(np.float64), tok, par, tau)
+    assert acc.tolist() == [own[0], own[1], own[2], own[3]]
+    assert path.tolist() == own[5].tolist()
+    ref = oracle.accept_tree(am_ref, ent_ref, tok, par, tau)
+    on_path = ref[5][:ref[0] + 1]
+    if np.all(margin[on_path] > bar):
+        assert [acc[0], acc[1], acc[3]] == [ref[0], ref[1], ref[3]]
+        assert path.tolist() == ref[5].tolist()
+        if abs(ent_ref[ref[3]] - tau) > 1e-3 * max(1.0, abs(tau)):
+            assert acc[2] == ref[2]
+    return ref

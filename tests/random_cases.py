@@ -118,3 +118,29 @@ def router_cases(n=24, seed=20260606):
             m = int(rng.integers(1, 300))
         out.append(dict(case=case, dt=dt, gamma=gamma, d=d, m=m, seed=6000 + case))
     return out
+
+
+def tree_lmhead_cases(n=20, seed=20260607):
+    """The LM head with tree acceptance: gamma 1..64 tree nodes (bushy random
+    parents), ragged vocabularies, bf16 weights row-major or tiled (the
+    tiled layout where the ABI takes it: d % 512 == 0, or gamma <= 16 with
+    d in {4096, 5120}), and the depth k of the accepted path the node
+    tokens plant."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for case in range(n):
+        gamma = int(rng.choice([rng.integers(1, 17), rng.integers(17, 65)]))
+        vocab = int(rng.choice([rng.integers(2, 500), rng.integers(500, 40000)]))
+        if gamma <= 16 and rng.random() < 0.4:
+            d = int(rng.choice([4096, 5120]))        # the persistent stream kernel's shapes
+        else:
+            d = int(rng.choice([512 * int(rng.integers(1, 5)), 32 * int(rng.integers(1, 40))]))
+        tileable = d % 512 == 0 or (gamma <= 16 and d in (4096, 5120))
+        tiled = bool(tileable and rng.random() < 0.6)
+        parents = np.full(gamma, -1, np.int32)
+        for j in range(1, gamma):
+            parents[j] = rng.integers(max(0, j - 6), j)
+        k = int(rng.integers(0, 9))
+        out.append(dict(case=case, gamma=gamma, vocab=vocab, d=d, tiled=tiled,
+                        parents=parents, k=k, seed=8000 + case))
+    return out

@@ -2,7 +2,8 @@
 attention (block-causal and tree masks, Sec. 3.2), KV-only prefill (Sec.
 3.4), the LM head with acceptance and entropy (Sec. 3.3.1), the drafter
 layer of the switch path (full layer and lazy catch-up, Sec. 3.4) and the
-neural routing policy (Sec. 3.3.2), over shapes
+neural routing policy (Sec. 3.3.2), and the LM head with tree acceptance
+(Sec. 3.1), over shapes
 drawn from the ranges the C ABI accepts (tests/random_cases.py: gamma 1..64,
 ragged context and vocabulary, head_dim 64 and 128, fp32 and bf16,
 row-major and tiled weights).  Each test runs a bounded number of cases
@@ -19,8 +20,8 @@ import torch
 import oracle
 import random_cases as R
 import workloads as W
-from parity import (TOL, accept_is_consistent, check_argmax, entropy_rel_err,
-                    host64, max_vec_rel_err)
+from parity import (TOL, accept_is_consistent, check_argmax, check_tree_accept,
+                    entropy_rel_err, host64, max_vec_rel_err)
 
 pytestmark = pytest.mark.gpu
 
@@ -206,3 +207,31 @@ def test_router_random_shapes():
         assert int(route[0]) == int(got[row] > tau), c["case"]
         if abs(ref[row] - tau) > TOL[dt] * scale[row]:
             assert int(route[0]) == oracle.route_neural(ref, row, tau), c["case"]
+
+
+def test_tree_lmhead_random_shapes():
+    """Tree verification's LM head (Sec. 3.1 draft trees verified in one
+    pass, Sec. 3.3.1 route): argmax and entropy of every node, then the
+    accepted path, its bonus token and the route, against the oracle."""
+    for c in R.tree_lmhead_cases():
+        print(f"random tree lmhead #{c['case']}: gamma={c['gamma']} d={c['d']} "
+              f"vocab={c['vocab']} tiled={c['tiled']} k={c['k']}", flush=True)
+        gamma, d, vocab, seed, par = c["gamma"], c["d"], c["vocab"], c["seed"], c["parents"]
+        h = W.normal((gamma, d), 1.0, W.stream_seed(seed, "h"), torch.bfloat16, DEV)
+        w = W.normal((vocab, d), 0.05, W.stream_seed(seed, "w_lm"), torch.bfloat16, DEV)
+        am_ref, ent_ref, margin, z = oracle.lmhead_rows(W.to_oracle(h), W.to_oracle(w),
+                                                        want_logits=True)
+        tok = W.tree_tokens(am_ref, par, c["k"], vocab, seed)
+        tau = float(np.float32(np.median(ent_ref) + 1e-3))
+        am = torch.empty(gamma, dtype=torch.int32, device=DEV)
+        ent = torch.empty(gamma, dtype=torch.float32, device=DEV)
+        acc = torch.empty(4, dtype=torch.int32, device=DEV)
+        path = torch.empty(gamma, dtype=torch.int32, device=DEV)
+        wl = wf.tile_weights(w) if c["tiled"] else w
+        wf.wf_lmhead_accept_tree(h, wl, None, torch.from_numpy(tok).to(DEV),
+                                 torch.from_numpy(par).to(DEV), tau, am, ent, acc, path)
+        torch.cuda.synchronize()
+        am, ent, acc, path = (t.cpu().numpy() for t in (am, ent, acc, path))
+        check_argmax(am, am_ref, margin, z, "bf16")
+        assert entropy_rel_err(ent, ent_ref) <= TOL["bf16"], c["case"]
+        check_tree_accept(am, ent, acc, path, am_ref, ent_ref, margin, tok, par, tau, 1e-2)

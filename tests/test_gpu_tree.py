@@ -10,7 +10,8 @@ import torch
 
 import oracle
 import workloads as W
-from parity import TOL, check_argmax, entropy_rel_err, host64, max_vec_rel_err
+from parity import (TOL, check_argmax, check_tree_accept, entropy_rel_err, host64,
+                    max_vec_rel_err)
 
 pytestmark = pytest.mark.gpu
 
@@ -135,25 +136,6 @@ def _lm_tree(h, w, logits, tok, par, tau):
     return am.cpu().numpy(), ent.cpu().numpy(), acc.cpu().numpy(), path.cpu().numpy()
 
 
-def _check_tree_accept(am, ent, acc, path, am_ref, ent_ref, margin, tok, par,
-                       tau, bar):
-    """The GPU's accept outputs follow exactly from its own argmax and
-    entropy; and wherever the oracle's margins on its accepted path exceed
-    the bar (so both sides agree on those argmaxes), they equal the
-    oracle's."""
-    own = oracle.accept_tree(am, ent.astype(np.float64), tok, par, tau)
-    assert acc.tolist() == [own[0], own[1], own[2], own[3]]
-    assert path.tolist() == own[5].tolist()
-    ref = oracle.accept_tree(am_ref, ent_ref, tok, par, tau)
-    on_path = ref[5][:ref[0] + 1]
-    if np.all(margin[on_path] > bar):
-        assert [acc[0], acc[1], acc[3]] == [ref[0], ref[1], ref[3]]
-        assert path.tolist() == ref[5].tolist()
-        if abs(ent_ref[ref[3]] - tau) > 1e-3 * max(1.0, abs(tau)):
-            assert acc[2] == ref[2]
-    return ref
-
-
 @pytest.mark.parametrize("k", [0, 2, 5, 8])
 def test_tree_accept_head_mode(k):
     """EAGLE-shaped tree, bf16 LM head; tokens put the accepted path at
@@ -171,8 +153,8 @@ def test_tree_accept_head_mode(k):
     am, ent, acc, path = _lm_tree(h, w, None, tok, par, tau)
     check_argmax(am, am_ref, margin, z, "bf16")
     assert entropy_rel_err(ent, ent_ref) <= TOL["bf16"]
-    _check_tree_accept(am, ent, acc, path, am_ref, ent_ref, margin, tok, par,
-                       tau, 1e-2)
+    check_tree_accept(am, ent, acc, path, am_ref, ent_ref, margin, tok, par,
+                      tau, 1e-2)
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -273,8 +255,8 @@ def test_eagle_tree_round_full_size():
     am, ent, acc, path = _lm_tree(head["h"], head["w_lm"], None, tok, par, tau)
     assert entropy_rel_err(ent, ent_ref) <= TOL["bf16"]
     check_argmax(am, am_ref, margin, None, "bf16")
-    _check_tree_accept(am, ent, acc, path, am_ref, ent_ref, margin, tok, par,
-                       tau, 1e-2)
+    check_tree_accept(am, ent, acc, path, am_ref, ent_ref, margin, tok, par,
+                      tau, 1e-2)
 
     kbefore, vbefore = W.to_oracle(kc), W.to_oracle(vc)
     wf.wf_kv_compact_path(kc, vc, torch.from_numpy(acc).to(DEV),

@@ -79,3 +79,15 @@ def test_router_cases_are_accepted():
         if c["dt"] == "bf16":
             assert c["d"] % 32 == 0 and c["m"] % 16 == 0
         assert wf.lib.wf_router_workspace_bytes(code, c["gamma"], c["d"], c["m"]) > 0, c
+
+
+def test_tree_lmhead_cases_are_accepted():
+    cases = R.tree_lmhead_cases()
+    assert any(c["tiled"] for c in cases) and any(not c["tiled"] for c in cases)
+    for c in cases:
+        assert 1 <= c["gamma"] <= 64 and c["d"] % 32 == 0
+        assert wf.wf_lmhead_workspace_bytes(c["gamma"], c["vocab"]) > 0, c
+        if c["tiled"]:
+            assert c["d"] % 512 == 0 or (c["gamma"] <= 16 and c["d"] in (4096, 5120))
+        par = c["parents"]
+        assert par[0] == -1 and all(0 <= par[j] < j for j in range(1, c["gamma"]))
