@@ -5,8 +5,9 @@
 //
 //   K[g][p+t] = RoPE(W_k[g] x_t, p+t),   V[g][p+t] = W_v[g] x_t
 //
-// bf16 path: the work unit is (KV head, K or V, pair of 16-feature blocks f
-// and f + head_dim/2).  Pairing the two halves of the rotate-half RoPE puts
+// bf16 path: the work unit is (KV head, K or V, one or two pairs of
+// 16-feature blocks f and f + head_dim/2).  Pairing the two halves of the
+// rotate-half RoPE puts
 // both elements of every rotation pair in the same thread after the
 // reduction, so RoPE is a register epilogue.  The input dimension is split
 // across a power-of-two number of workgroups so a handful of units still
@@ -26,6 +27,9 @@ namespace wf {
 namespace {
 
 constexpr int kPfMaxChunksPerWave = 8;   // 32-wide chunks per wave per k-slice
+constexpr int kPfWideMaxChunks = 4;      // the same for two-pair units (more operand registers)
+constexpr int kPfWideMinTokens = 65;     // two-pair units from this many tokens of one layer on
+constexpr int kPfWideNbt3Tokens = 160;   // three 16-token blocks per workgroup up to here, then four
 constexpr int kPfTargetWorkgroups = 256;
 constexpr int kMaxHalfDim = 64;          // head_dim <= 128
 
@@ -65,24 +69,29 @@ __device__ __forceinline__ void rope_pair(float &lo, float &hi, double theta, in
 }
 
 // Split-K: workgroup (unit, k-slice, token block) computes D[feature][token]
-// over its slice of the input dimension for the unit's two 16-feature blocks
-// (f and f + head_dim/2 of one head, K or V); the slices then meet through
-// the exchange tree below.
+// over its slice of the input dimension for the unit's 16-feature blocks
+// (f and f + head_dim/2 of each of its pairs, one head, K or V); the slices
+// then meet through the exchange tree below.
 // The body takes its workgroup's grid coordinates explicitly, so one launch
 // can run two such problems side by side (prefill_pair_bf16).
-template <int DH, int NBT, int MAXC>
+// A unit holds PPU consecutive pairs: its 2*PPU feature blocks are the low
+// halves of those pairs (blocks 0..PPU-1) and then their high halves.
+template <int DH, int NBT, int MAXC, int PPU>
 __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, int ks, int bz,
                                              int n_units, int ksplit) {
     constexpr int PAIRS = DH / 32;       // 16-feature block pairs per head
+    static_assert(PAIRS % PPU == 0, "a unit's pairs must tile the head");
+    constexpr int UPH = PAIRS / PPU;     // units per head and kind
+    constexpr int MB = 2 * PPU;          // 16-feature blocks per unit
     constexpr int TOK = 16 * NBT;
     constexpr int WAVES = 4;
-    __shared__ float zs[WAVES][2][16][TOK + 1];
+    __shared__ float zs[WAVES][MB][16][TOK + 1];
 
     const int tb = bz % a.token_blocks;
     const int layer = bz / a.token_blocks;
-    const int pair = unit % PAIRS;
-    const int kind = a.kinds == 2 ? (unit / PAIRS) % 2 : 0;   // 0 = K, 1 = V
-    const int g = unit / (a.kinds * PAIRS);
+    const int pair0 = (unit % UPH) * PPU;                     // the unit's first pair
+    const int kind = a.kinds == 2 ? (unit / UPH) % 2 : 0;     // 0 = K, 1 = V
+    const int g = unit / (a.kinds * UPH);
     const int t0 = tb * TOK;
 
     const int wave = wave_id();
@@ -92,7 +101,6 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
 
     const uint16_t *w = static_cast<const uint16_t *>(kind ? a.w_v : a.w_k) + layer * a.w_ls;
     const uint16_t *x = static_cast<const uint16_t *>(a.x) + layer * a.x_ls;
-    const int f_lo = g * DH + 16 * pair;           // first feature, low half
     const int c_begin = ks * a.chunks_per_split;   // 32-wide chunks of d_in
     // chunks of this slice (the last slices of a power-of-two split may be
     // short or empty)
@@ -100,17 +108,16 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
     // W operand of chunk c: row-major, lane (m16, c4) reads 16 bytes of row
     // m16 (64 contiguous bytes per row and load); tiled, the wave reads the
     // chunk's 1 KB tile contiguously
-    const uint16_t *wp0, *wp1;
-    int wstep;
-    if (a.w_tiled) {
-        const size_t kch = (size_t)(a.d_in / 32);
-        wp0 = w + (size_t)(f_lo / 16) * kch * 512 + lane * 8;
-        wp1 = w + (size_t)((f_lo + DH / 2) / 16) * kch * 512 + lane * 8;
-        wstep = 512;
-    } else {
-        wp0 = w + (size_t)(f_lo + m16) * a.d_in + c4 * 8;
-        wp1 = w + (size_t)(f_lo + DH / 2 + m16) * a.d_in + c4 * 8;
-        wstep = 32;
+    const uint16_t *wp[MB];
+    const int wstep = a.w_tiled ? 512 : 32;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+        // first feature of block mb
+        const int f = g * DH + 16 * (pair0 + mb % PPU) + (mb < PPU ? 0 : DH / 2);
+        if (a.w_tiled)
+            wp[mb] = w + (size_t)(f / 16) * (size_t)(a.d_in / 32) * 512 + lane * 8;
+        else
+            wp[mb] = w + (size_t)(f + m16) * a.d_in + c4 * 8;
     }
     // Tokens past n_tok read the last token (row-major) or the padded
     // rows of the last 16-token tile (tiled) instead: they only feed MFMA
@@ -133,9 +140,9 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
         xstep = 32;
     }
 
-    f32x4 acc[2][NBT];
+    f32x4 acc[MB][NBT];
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NBT; ++nb)
             acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -144,15 +151,16 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
     // token's projection takes all of a wave's chunks in one batch: one
     // memory round trip instead of two)
     for (int cb = wave; cb < n_c; cb += WAVES * MAXC) {
-        bf16x8 wr[MAXC][2], xr[MAXC][NBT];
+        bf16x8 wr[MAXC][MB], xr[MAXC][NBT];
 #pragma unroll
         for (int u = 0; u < MAXC; ++u) {
             const int c = cb + WAVES * u;
             if (c < n_c) {
                 const size_t off = (size_t)(c_begin + c) * xstep;
                 const size_t woff = (size_t)(c_begin + c) * wstep;
-                wr[u][0] = load_bf16x8(wp0 + woff);
-                wr[u][1] = load_bf16x8(wp1 + woff);
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+                    wr[u][mb] = load_bf16x8(wp[mb] + woff);
 #pragma unroll
                 for (int nb = 0; nb < NBT; ++nb)
                     xr[u][nb] = load_bf16x8(xp[nb] + off);
@@ -162,7 +170,7 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
         for (int u = 0; u < MAXC; ++u) {
             if (cb + WAVES * u < n_c) {
 #pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
+                for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                     for (int nb = 0; nb < NBT; ++nb)
                         acc[mb][nb] = mfma16x16x32(wr[u][mb], xr[u][nb], acc[mb][nb]);
@@ -171,7 +179,7 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
     }
     // lane (m16, c4) holds D[feature 4*c4 + i][token nb*16 + m16]
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NBT; ++nb)
 #pragma unroll
@@ -180,7 +188,9 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
     __syncthreads();
     // Thread (e, token) sums the waves in order for its rotation pair
     // (feature 16*pair + e of the low half and its partner in the high
-    // half), then combines the k-slices up a fixed binary tree: leaf
+    // half; e runs fastest across threads, so a wave's cache writes cover
+    // whole 32-byte runs of 4 rows instead of 2 bytes of 64 rows: 6.6 ->
+    // 6.45 us at 16 tokens, 15.5 -> 14.6 at 80), then combines the k-slices up a fixed binary tree: leaf
     // ksplit + k, node i with children 2i and 2i+1, one 64-bit exchange slot
     // per internal node and pair.  The first slice to reach a node parks its
     // (lo, hi) there; the second takes it, adds (a commutative fp32 add, so
@@ -190,30 +200,32 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
     // (bits(hi) << 32) | (bits(lo) + 1), never 0 for arithmetic results.
     // A thread holds NI pairs (idx = tid + 256 i) and climbs with all of
     // them at once: one exchange round trip per tree level, not per pair.
-    constexpr int NI = 16 * TOK / 256;
-    static_assert(16 * TOK % 256 == 0, "pairs per workgroup must fill the 256 threads");
+    constexpr int NP = 16 * PPU * TOK;   // rotation pairs per workgroup
+    constexpr int NI = NP / 256;
+    static_assert(NP % 256 == 0, "pairs per workgroup must fill the 256 threads");
     const size_t ub =                                          // (layer, unit, token block)
         ((size_t)layer * n_units + unit) * a.token_blocks + tb;
-    unsigned long long *slots = a.slots + ub * (size_t)(ksplit - 1) * (16 * TOK);
+    unsigned long long *slots = a.slots + ub * (size_t)(ksplit - 1) * NP;
     uint16_t *cache = static_cast<uint16_t *>(kind ? a.v_cache : a.k_cache) + layer * a.c_ls;
     float lo[NI], hi[NI];
     bool mine[NI];
 #pragma unroll
     for (int n = 0; n < NI; ++n) {
         const int idx = threadIdx.x + 256 * n;
-        const int e = idx / TOK;
-        const int tl = idx % TOK;
-        lo[n] = zs[0][0][e][tl];
-        hi[n] = zs[0][1][e][tl];
+        const int pl = idx / (16 * TOK);           // the unit's pair
+        const int e = idx % 16;
+        const int tl = (idx / 16) % TOK;
+        lo[n] = zs[0][pl][e][tl];
+        hi[n] = zs[0][PPU + pl][e][tl];
 #pragma unroll
         for (int ww = 1; ww < WAVES; ++ww) {
-            lo[n] += zs[ww][0][e][tl];
-            hi[n] += zs[ww][1][e][tl];
+            lo[n] += zs[ww][pl][e][tl];
+            hi[n] += zs[ww][PPU + pl][e][tl];
         }
         mine[n] = true;
     }
     for (unsigned node = (unsigned)(ksplit + ks); node > 1; node /= 2) {
-        unsigned long long *level = slots + (size_t)(node / 2 - 1) * (16 * TOK) + threadIdx.x;
+        unsigned long long *level = slots + (size_t)(node / 2 - 1) * NP + threadIdx.x;
         unsigned long long old[NI];
 #pragma unroll
         for (int n = 0; n < NI; ++n) {
@@ -244,8 +256,9 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
 #pragma unroll
     for (int n = 0; n < NI; ++n) {
         const int idx = threadIdx.x + 256 * n;
-        const int e = idx / TOK;
-        const int t = t0 + idx % TOK;
+        const int pair = pair0 + idx / (16 * TOK);
+        const int e = idx % 16;
+        const int t = t0 + (idx / 16) % TOK;
         if (!mine[n] || t >= a.n_tok)
             continue;
         const int pos = a.start_pos + t;
@@ -258,9 +271,9 @@ __device__ __forceinline__ void prefill_body(const PrefillParams &a, int unit, i
     }
 }
 
-template <int DH, int NBT, int MAXC = kPfMaxChunksPerWave>
+template <int DH, int NBT, int MAXC = kPfMaxChunksPerWave, int PPU = 1>
 __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
-    prefill_body<DH, NBT, MAXC>(a, blockIdx.x, blockIdx.y, blockIdx.z, gridDim.x, gridDim.y);
+    prefill_body<DH, NBT, MAXC, PPU>(a, blockIdx.x, blockIdx.y, blockIdx.z, gridDim.x, gridDim.y);
 }
 
 // Two independent projections in one launch: workgroups [0, n1) run the
@@ -268,19 +281,19 @@ __global__ __launch_bounds__(256) void prefill_bf16(PrefillParams a) {
 // second's.  Each keeps its own exchange slots (disjoint parts of the zero
 // block).  The drafter catch-up runs the backlog's K/V and the last token's
 // q this way: one launch instead of two back to back.
-template <int DH, int NBT1, int MAXC1, int NBT2, int MAXC2>
+template <int DH, int NBT1, int MAXC1, int PPU1, int NBT2, int MAXC2>
 __global__ __launch_bounds__(256) void prefill_pair_bf16(PrefillParams a1, PrefillParams a2,
                                                          int units1, int ks1, int z1,
                                                          int units2, int ks2) {
     const int b = blockIdx.x;
     const int n1 = units1 * ks1 * z1;
     if (b < n1) {
-        prefill_body<DH, NBT1, MAXC1>(a1, b % units1, (b / units1) % ks1, b / (units1 * ks1),
-                                      units1, ks1);
+        prefill_body<DH, NBT1, MAXC1, PPU1>(a1, b % units1, (b / units1) % ks1,
+                                            b / (units1 * ks1), units1, ks1);
     } else {
         const int c = b - n1;
-        prefill_body<DH, NBT2, MAXC2>(a2, c % units2, (c / units2) % ks2, c / (units2 * ks2),
-                                      units2, ks2);
+        prefill_body<DH, NBT2, MAXC2, 1>(a2, c % units2, (c / units2) % ks2, c / (units2 * ks2),
+                                         units2, ks2);
     }
 }
 
@@ -326,32 +339,50 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
+// Exchange slots: (ksplit - 1) internal tree nodes x 16*16*ppu*nbt pairs
+// per (unit, token block), inside the workspace's zero block.
+static size_t prefill_slot_bytes(const PrefillPlan &p, int n_layers) {
+    return (size_t)n_layers * p.units * p.token_blocks * (p.ksplit - 1) *
+           (16 * 16 * p.ppu * p.nbt) * sizeof(unsigned long long);
+}
+
 PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers,
                          int kinds) {
     PrefillPlan p{};
-    p.nbt = std::min(4, std::max(1, cdiv(n_tok, 16)));
+    const int pairs = head_dim / 32;
+    // One layer with more than four token blocks (a switch's backlog): units
+    // of two pairs, so each workgroup reads its slice of the activations for
+    // twice the features (the activation reads across all units halve) and
+    // the grid keeps more k-slices; otherwise one pair per unit.  Measured
+    // (8B shapes): 80 tokens 14.6 -> 12.8 us, 160 21.3 -> 15.3, 1024 69 ->
+    // 43, 4096 271 -> 160; at 40 tokens two-pair units were slower (their
+    // eight k-slices add a third exchange level).
+    p.ppu = (n_layers == 1 && n_tok >= kPfWideMinTokens && pairs % 2 == 0) ? 2 : 1;
+    if (p.ppu == 2)
+        p.nbt = n_tok <= kPfWideNbt3Tokens ? 3 : 4;
+    else
+        p.nbt = std::min(4, std::max(1, cdiv(n_tok, 16)));
     p.token_blocks = std::max(1, cdiv(n_tok, 16 * p.nbt));
-    p.units = n_kv_heads * kinds * (head_dim / 32);
+    p.units = n_kv_heads * kinds * (pairs / p.ppu);
     const int chunks = d_in / 32;
     // a power-of-two number of k-slices: enough to cover the chip, at least
-    // 4 chunks per slice.  layers * units * token_blocks * (ksplit - 1) <
-    // 512, so the exchange slots stay under 512 * 1024 pairs = the 4 MiB
-    // zero block.  Several layers in one launch need fewer slices (none from
-    // 256 (layer, unit, token block) triples up).
+    // 4 chunks per slice, and the exchange slots inside the 4 MiB zero block
+    // (one pair per unit: layers * units * token_blocks * (ksplit - 1) < 256
+    // keeps them under 2 MiB).  Several layers in one launch need fewer
+    // slices (none from 256 (layer, unit, token block) triples up).
     const long long base = (long long)p.units * p.token_blocks * n_layers;
     int ks = 1;
-    while (ks * 2 * base <= kPfTargetWorkgroups && chunks / (ks * 2) >= 4)
+    for (;;) {
+        PrefillPlan q = p;
+        q.ksplit = ks * 2;
+        if (ks * 2 * base > kPfTargetWorkgroups || chunks / (ks * 2) < 4 ||
+            prefill_slot_bytes(q, n_layers) > kCounterBytes)
+            break;
         ks *= 2;
+    }
     p.chunks_per_split = cdiv(chunks, ks);
     p.ksplit = ks;
     return p;
-}
-
-// Exchange slots: (ksplit - 1) internal tree nodes x 16*16*nbt pairs per
-// (unit, token block), inside the workspace's zero block.
-static size_t prefill_slot_bytes(const PrefillPlan &p, int n_layers) {
-    return (size_t)n_layers * p.units * p.token_blocks * (p.ksplit - 1) * (16 * 16 * p.nbt) *
-           sizeof(unsigned long long);
 }
 
 bool prefill_fits(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers) {
@@ -390,12 +421,18 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
         a.slots = static_cast<unsigned long long *>(workspace);
         dim3 grid(p.units, p.ksplit, p.token_blocks * n_layers), block(256);
 #define WF_PF_CASE(DHV, NBV)                                                        \
-    if (head_dim == DHV && p.nbt == NBV) {                                          \
+    if (head_dim == DHV && p.nbt == NBV && p.ppu == 1) {                            \
         prefill_bf16<DHV, NBV><<<grid, block, 0, stream>>>(a);                      \
+    } else
+#define WF_PF_WIDE(DHV, NBV)                                                        \
+    if (head_dim == DHV && p.nbt == NBV && p.ppu == 2) {                            \
+        prefill_bf16<DHV, NBV, kPfWideMaxChunks, 2><<<grid, block, 0, stream>>>(a); \
     } else
         WF_PF_CASE(128, 1) WF_PF_CASE(128, 2) WF_PF_CASE(128, 3) WF_PF_CASE(128, 4)
         WF_PF_CASE(64, 1) WF_PF_CASE(64, 2) WF_PF_CASE(64, 3) WF_PF_CASE(64, 4)
+        WF_PF_WIDE(128, 3) WF_PF_WIDE(128, 4) WF_PF_WIDE(64, 3) WF_PF_WIDE(64, 4)
         { return WF_ERR_UNSUPPORTED; }
+#undef WF_PF_WIDE
 #undef WF_PF_CASE
     } else {
         const long long total = (long long)n_tok * n_kv_heads * head_dim;   // waves
@@ -417,17 +454,16 @@ wf_status_t launch_prefill(wf_dtype_t dt, const void *x, const void *w_k,
 
 // The drafter catch-up's first two projections in one launch: the KV-only
 // prefill of the backlog's n_tok tiled rows (as launch_prefill with a tiled
-// x) and q = RoPE(W_q x_last) of the last token (as launch_q_rope), the two
-// sets of exchange slots in the lower and upper halves of the zero block.
-// WF_ERR_UNSUPPORTED when either set needs more than its half (the caller
-// then launches the two one after the other).
+// x) and q = RoPE(W_q x_last) of the last token (as launch_q_rope), the
+// first set of exchange slots at the start of the zero block, the second at
+// its end.  WF_ERR_UNSUPPORTED when the two sets do not fit side by side (the
+// caller then launches the two one after the other).
 wf_status_t launch_prefill_and_q(bool tiled, const uint16_t *x_rows, const void *w_k,
                                  const void *w_v, void *k_cache, void *v_cache, int n_tok,
                                  int start_pos, int cap, int d_in, int n_kv_heads,
                                  const uint16_t *x_last, const uint16_t *w_q, uint16_t *q,
                                  int n_q_heads, int head_dim, int q_pos, double rope_base,
                                  void *workspace, hipStream_t stream) {
-    constexpr size_t kHalf = kCounterBytes / 2;
     PrefillParams a1{x_rows, w_k, w_v, k_cache, v_cache, n_tok, start_pos, cap, d_in,
                      n_kv_heads, {}, nullptr, 0, 1, 0, 0, 0, tiled ? 1 : 0, 2, 0, 1};
     PrefillParams a2{x_last, w_q, w_q, q, q, 1, 0, 1, d_in, n_q_heads, {}, nullptr, 0, 1, 0, 0, 0,
@@ -436,30 +472,35 @@ wf_status_t launch_prefill_and_q(bool tiled, const uint16_t *x_rows, const void 
         a1.theta[i] = a2.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
     const PrefillPlan p1 = plan_prefill(n_tok, d_in, n_kv_heads, head_dim, 1);
     const PrefillPlan p2 = plan_prefill(1, d_in, n_q_heads, head_dim, 1, 1);
-    if (prefill_slot_bytes(p1, 1) > kHalf || prefill_slot_bytes(p2, 1) > kHalf)
+    const size_t q_off = (kCounterBytes - prefill_slot_bytes(p2, 1)) / 256 * 256;
+    if (prefill_slot_bytes(p2, 1) > kCounterBytes || prefill_slot_bytes(p1, 1) > q_off)
         return WF_ERR_UNSUPPORTED;
     a1.chunks_per_split = p1.chunks_per_split;
     a1.token_blocks = p1.token_blocks;
     a1.slots = static_cast<unsigned long long *>(workspace);
     a2.chunks_per_split = p2.chunks_per_split;
     a2.token_blocks = p2.token_blocks;
-    a2.slots = reinterpret_cast<unsigned long long *>(static_cast<char *>(workspace) + kHalf);
+    a2.slots = reinterpret_cast<unsigned long long *>(static_cast<char *>(workspace) + q_off);
     const long long n1 = (long long)p1.units * p1.ksplit * p1.token_blocks;
     const long long n2 = (long long)p2.units * p2.ksplit * p2.token_blocks;
     const dim3 grid((unsigned)(n1 + n2)), block(256);
     const bool wide2 = p2.chunks_per_split > 4 * kPfMaxChunksPerWave;
     constexpr int M8 = kPfMaxChunksPerWave, M16 = 2 * kPfMaxChunksPerWave;
-#define WF_PAIR_CASE(DHV, NBV)                                                              \
-    if (head_dim == DHV && p1.nbt == NBV) {                                                 \
+    constexpr int MW = kPfWideMaxChunks;
+#define WF_PAIR_CASE(DHV, NBV, MC, PPUV)                                                    \
+    if (head_dim == DHV && p1.nbt == NBV && p1.ppu == PPUV) {                               \
         if (wide2)                                                                          \
-            prefill_pair_bf16<DHV, NBV, M8, 1, M16><<<grid, block, 0, stream>>>(            \
+            prefill_pair_bf16<DHV, NBV, MC, PPUV, 1, M16><<<grid, block, 0, stream>>>(      \
                 a1, a2, p1.units, p1.ksplit, p1.token_blocks, p2.units, p2.ksplit);         \
         else                                                                                \
-            prefill_pair_bf16<DHV, NBV, M8, 1, M8><<<grid, block, 0, stream>>>(             \
+            prefill_pair_bf16<DHV, NBV, MC, PPUV, 1, M8><<<grid, block, 0, stream>>>(       \
                 a1, a2, p1.units, p1.ksplit, p1.token_blocks, p2.units, p2.ksplit);         \
     } else
-    WF_PAIR_CASE(128, 1) WF_PAIR_CASE(128, 2) WF_PAIR_CASE(128, 3) WF_PAIR_CASE(128, 4)
-    WF_PAIR_CASE(64, 1) WF_PAIR_CASE(64, 2) WF_PAIR_CASE(64, 3) WF_PAIR_CASE(64, 4)
+    WF_PAIR_CASE(128, 1, M8, 1) WF_PAIR_CASE(128, 2, M8, 1) WF_PAIR_CASE(128, 3, M8, 1)
+    WF_PAIR_CASE(128, 4, M8, 1) WF_PAIR_CASE(64, 1, M8, 1) WF_PAIR_CASE(64, 2, M8, 1)
+    WF_PAIR_CASE(64, 3, M8, 1) WF_PAIR_CASE(64, 4, M8, 1)
+    WF_PAIR_CASE(128, 3, MW, 2) WF_PAIR_CASE(128, 4, MW, 2)
+    WF_PAIR_CASE(64, 3, MW, 2) WF_PAIR_CASE(64, 4, MW, 2)
     { return WF_ERR_UNSUPPORTED; }
 #undef WF_PAIR_CASE
     return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;

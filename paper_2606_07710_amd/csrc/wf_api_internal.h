@@ -127,7 +127,8 @@ wf_status_t launch_compact(wf_dtype_t dt, void *k_cache, void *v_cache,
 struct PrefillPlan {
     int nbt;             // 16-token blocks per workgroup
     int token_blocks;    // workgroups along the tokens
-    int units;           // (kv head, K|V, RoPE block pair) work units
+    int ppu;             // RoPE block pairs per work unit
+    int units;           // (kv head, K|V, group of ppu RoPE block pairs) work units
     int ksplit;          // slices of the input dimension
     int chunks_per_split;
 };
