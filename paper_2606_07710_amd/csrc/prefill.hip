@@ -29,6 +29,7 @@ namespace {
 constexpr int kPfMaxChunksPerWave = 8;   // 32-wide chunks per wave per k-slice
 constexpr int kPfWideMaxChunks = 4;      // the same for two-pair units (more operand registers)
 constexpr int kPfWideMinTokens = 65;     // two-pair units from this many tokens of one layer on
+constexpr int kPfWideMinTokensBesideQ = 384;   // the same beside the catch-up's q projection
 constexpr int kPfWideNbt3Tokens = 160;   // three 16-token blocks per workgroup up to here, then four
 constexpr int kPfTargetWorkgroups = 256;
 constexpr int kMaxHalfDim = 64;          // head_dim <= 128
@@ -347,7 +348,7 @@ static size_t prefill_slot_bytes(const PrefillPlan &p, int n_layers) {
 }
 
 PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers,
-                         int kinds) {
+                         int kinds, bool beside_q) {
     PrefillPlan p{};
     const int pairs = head_dim / 32;
     // One layer with more than four token blocks (a switch's backlog): units
@@ -356,8 +357,12 @@ PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int 
     // the grid keeps more k-slices; otherwise one pair per unit.  Measured
     // (8B shapes): 80 tokens 14.6 -> 12.8 us, 160 21.3 -> 15.3, 1024 69 ->
     // 43, 4096 271 -> 160; at 40 tokens two-pair units were slower (their
-    // eight k-slices add a third exchange level).
-    p.ppu = (n_layers == 1 && n_tok >= kPfWideMinTokens && pairs % 2 == 0) ? 2 : 1;
+    // eight k-slices add a third exchange level).  Sharing a launch with the
+    // catch-up's q projection, whose workgroups take the CUs' second slots,
+    // they pay from about 384 tokens on (catch-up: 128 tokens 97.3 against
+    // 100.2 us with one-pair units, 512 tokens 108.4 against 113.7).
+    const int wide_min = beside_q ? kPfWideMinTokensBesideQ : kPfWideMinTokens;
+    p.ppu = (n_layers == 1 && n_tok >= wide_min && pairs % 2 == 0) ? 2 : 1;
     if (p.ppu == 2)
         p.nbt = n_tok <= kPfWideNbt3Tokens ? 3 : 4;
     else
@@ -470,7 +475,7 @@ wf_status_t launch_prefill_and_q(bool tiled, const uint16_t *x_rows, const void 
                      tiled ? 1 : 0, 1, q_pos, 0};
     for (int i = 0; i < head_dim / 2; ++i)
         a1.theta[i] = a2.theta[i] = std::pow(rope_base, -2.0 * (double)i / (double)head_dim);
-    const PrefillPlan p1 = plan_prefill(n_tok, d_in, n_kv_heads, head_dim, 1);
+    const PrefillPlan p1 = plan_prefill(n_tok, d_in, n_kv_heads, head_dim, 1, 2, true);
     const PrefillPlan p2 = plan_prefill(1, d_in, n_q_heads, head_dim, 1, 1);
     const size_t q_off = (kCounterBytes - prefill_slot_bytes(p2, 1)) / 256 * 256;
     if (prefill_slot_bytes(p2, 1) > kCounterBytes || prefill_slot_bytes(p1, 1) > q_off)

@@ -133,8 +133,10 @@ struct PrefillPlan {
     int chunks_per_split;
 };
 
+// beside_q: the plan of a prefill that shares its launch with the drafter
+// catch-up's q projection (prefill_pair_bf16).
 PrefillPlan plan_prefill(int n_tok, int d_in, int n_kv_heads, int head_dim, int n_layers = 1,
-                         int kinds = 2);
+                         int kinds = 2, bool beside_q = false);
 size_t prefill_workspace_bytes(wf_dtype_t dt, int n_tok, int d_in, int n_kv_heads,
                                int head_dim);
 // Whether the bf16 plan's exchange slots fit the workspace zero block (and
