@@ -94,6 +94,7 @@ CATCHUP_CASES = [
     (512, 4, 2, 64, 1024, 0, 37),
     (1024, 8, 4, 128, 2048, 513, 80),
     (4096, 32, 8, 128, 12288, 4096, 80),
+    (1024, 8, 4, 128, 2048, 100, 500),         # two-pair units beside q in one launch
     (256, 4, 2, 64, 512, 10, 4096),            # the largest single prefill batch
     (256, 4, 2, 64, 512, 3, 9000),             # three batches: 4096 + 4096 + 808
 ]

@@ -37,6 +37,9 @@ CASES = [
     ("bf16", 17, 1024, 8, 128, 1000, 1e6),
     ("bf16", 32, 5120, 8, 128, 65552, 1e6),
     ("bf16", 70, 256, 2, 64, 5, 1e4),
+    ("bf16", 80, 4096, 8, 128, 4096, 1e6),     # two-pair units, 48 + 32 tokens
+    ("bf16", 200, 2048, 4, 128, 777, 1e6),     # two-pair units, four 16-token blocks each
+    ("bf16", 100, 1024, 2, 64, 3, 1e4),        # two-pair units at head_dim 64
     ("bf16", 4096, 512, 2, 64, 100, 1e4),      # the largest catch-up a call takes
     ("f32", 4, 512, 2, 64, 252, 1e4),
     ("f32", 9, 100, 3, 128, 65000, 1e6),
