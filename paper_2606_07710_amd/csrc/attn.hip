@@ -606,20 +606,29 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
     // Two key streams whose merged rows fit a ring buffer as bf16: each
     // stream owns half the head dims (stream s: dim blocks [s*MD/2,
     // (s+1)*MD/2)) and hands the other half, rescaled, to the other stream
-    // through ring0; each adds the half it receives to its own (a + b: the
-    // same fp32 sum in either order, so the result matches one stream doing
-    // all the adds), stages its merged half as bf16 rows in ring1, and then
-    // every wave of the workgroup writes the rows out as 16-byte pieces
-    // (draft trees, 64-row workgroups: 23.35 -> 22.80 us per call at 244
-    // rows and 8K keys; with 16 or 32 rows the extra barrier is not paid
-    // back, so those keep the single hand-off below).
+    // through ring0; each adds the half it receives to its own rescaled half
+    // (the same two terms as the single hand-off, rounded once more or less
+    // where the compiler fuses the multiply into the add), stages its merged
+    // half as bf16 rows, and then every wave of the workgroup writes the
+    // rows out as 16-byte pieces (draft trees, 64-row workgroups: 23.35 ->
+    // 22.80 us per call at 244 rows and 8K keys; 32B shapes, 128-row
+    // workgroups: 60.3 -> 59.8 us at 64K keys; with 16 or 32 rows the extra
+    // barrier is not paid back, so those keep the single hand-off below).
     constexpr int SRB = DH * 2 + 16;                 // padded staged row bytes
+    // (the staged rows fill ring1, or ring1 and ring2 half and half)
+    constexpr int SHALF = ROWS_WG * SRB <= RING1_BYTES ? ROWS_WG : ROWS_WG / 2;
     constexpr bool SPLIT2 = KS == 2 && MD % 2 == 0 && ROWS_WG >= 64 &&
-                            ROWS_WG * SRB <= RING1_BYTES;
+                            SHALF * SRB <= RING1_BYTES &&
+                            (SHALF == ROWS_WG || (NBUF > 2 && SHALF * SRB <= STAGE_BYTES));
     if constexpr (SPLIT2) {
         constexpr int MH = MD / 2;
         WF_LDS(float) *reg = oreg(0);
-        WF_LDS(char) *stg = (WF_LDS(char) *)ring1;
+        auto srow = [&](int row) {                   // staged row address
+            if constexpr (SHALF == ROWS_WG)
+                return (WF_LDS(char) *)ring1 + row * SRB;
+            else
+                return (WF_LDS(char) *)(row < SHALF ? ring1 : ring2) + (row % SHALF) * SRB;
+        };
         auto give = [&](auto base_tag) __attribute__((always_inline)) {
             constexpr int B = decltype(base_tag)::value;
 #pragma unroll
@@ -641,7 +650,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                     const int md = B + mh;
                     const f32x4 v = o[md][nb] * fac[nb] +
                                     *(WF_LDS(const f32x4) *)(reg + rl * OST + md * 16 + 4 * c4);
-                    *(WF_LDS(u32x2) *)(stg + rl * SRB + (md * 16 + 4 * c4) * 2) =
+                    *(WF_LDS(u32x2) *)(srow(rl) + (md * 16 + 4 * c4) * 2) =
                         u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
                 }
             }
@@ -691,7 +700,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                 const size_t pr = (size_t)split * pairs + (size_t)(r / a.group) * a.n_q_heads +
                                   g * a.group + (r % a.group);
                 reinterpret_cast<u32x4 *>(static_cast<uint16_t *>(a.ws_o) + pr * DH)[col] =
-                    *(const WF_LDS(u32x4) *)(stg + row * SRB + col * 16);
+                    *(const WF_LDS(u32x4) *)(srow(row) + col * 16);
             }
         }
         return;
