@@ -144,3 +144,22 @@ def tree_lmhead_cases(n=20, seed=20260607):
         out.append(dict(case=case, gamma=gamma, vocab=vocab, d=d, tiled=tiled,
                         parents=parents, k=k, seed=8000 + case))
     return out
+
+
+def layer_prefill_cases(n=12, seed=20260608):
+    """All layers' KV-only prefill in one launch: 2..12 layers, 1..200
+    tokens, bf16 row-major or tiled weights."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for case in range(n):
+        n_layers = int(rng.integers(2, 13))
+        n_tok = int(rng.choice([rng.integers(1, 17), rng.integers(17, 80),
+                                rng.integers(80, 201)]))
+        d_in = 32 * int(rng.integers(1, 48))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        dh = int(rng.choice([64, 128]))
+        start = int(rng.integers(0, 5000))
+        tiled = bool(rng.random() < 0.5)
+        out.append(dict(case=case, layers=n_layers, n=n_tok, d_in=d_in, hkv=hkv, dh=dh,
+                        start=start, tiled=tiled, seed=9000 + case))
+    return out

@@ -1,14 +1,13 @@
 """Seeded random-shape GPU parity sweep against the fp64 oracle: verify
 attention (block-causal and tree masks, Sec. 3.2), KV-only prefill (Sec.
-3.4), the LM head with acceptance and entropy (Sec. 3.3.1), the drafter
+3.4; one layer, and all layers in one launch), the LM head with acceptance
+and entropy (Sec. 3.3.1) or with tree acceptance (Sec. 3.1), the drafter
 layer of the switch path (full layer and lazy catch-up, Sec. 3.4) and the
-neural routing policy (Sec. 3.3.2), and the LM head with tree acceptance
-(Sec. 3.1), over shapes
-drawn from the ranges the C ABI accepts (tests/random_cases.py: gamma 1..64,
-ragged context and vocabulary, head_dim 64 and 128, fp32 and bf16,
-row-major and tiled weights).  Each test runs a bounded number of cases
-from a fixed seed, prints every case before it runs, and stops at the first
-mismatch.
+neural routing policy (Sec. 3.3.2), over shapes drawn from the ranges the C
+ABI accepts (tests/random_cases.py: gamma 1..64, ragged context and
+vocabulary, head_dim 64 and 128, fp32 and bf16, row-major and tiled
+weights).  Each test runs a bounded number of cases from a fixed seed,
+prints every case before it runs, and stops at the first mismatch.
 """
 import dataclasses
 import math
@@ -235,3 +234,34 @@ def test_tree_lmhead_random_shapes():
         check_argmax(am, am_ref, margin, z, "bf16")
         assert entropy_rel_err(ent, ent_ref) <= TOL["bf16"], c["case"]
         check_tree_accept(am, ent, acc, path, am_ref, ent_ref, margin, tok, par, tau, 1e-2)
+
+
+def test_layer_prefill_random_shapes():
+    """All layers' KV-only prefill in one launch (Sec. 3.4): every layer's
+    written rows against the oracle, the other rows unchanged."""
+    for c in R.layer_prefill_cases():
+        print(f"random layer prefill #{c['case']}: layers={c['layers']} n={c['n']} "
+              f"d_in={c['d_in']} hkv={c['hkv']} dh={c['dh']} start={c['start']} "
+              f"tiled={c['tiled']}", flush=True)
+        L, n, d_in, hkv, dh, start, seed = (c[k] for k in ("layers", "n", "d_in", "hkv", "dh",
+                                                            "start", "seed"))
+        cap = start + n + 2
+        bf = torch.bfloat16
+        x = W.normal((L, n, d_in), 1.0, W.stream_seed(seed, "x"), bf, DEV)
+        wk = W.normal((L, hkv * dh, d_in), 0.02, W.stream_seed(seed, "w_k"), bf, DEV)
+        wv = W.normal((L, hkv * dh, d_in), 0.02, W.stream_seed(seed, "w_v"), bf, DEV)
+        kc = W.normal((L, hkv, cap, dh), 1.0, W.stream_seed(seed, "k_cache"), bf, DEV)
+        vc = W.normal((L, hkv, cap, dh), 1.0, W.stream_seed(seed, "v_cache"), bf, DEV)
+        k0, v0 = kc.clone(), vc.clone()
+        wkt, wvt = (wf.tile_weights(wk), wf.tile_weights(wv)) if c["tiled"] else (wk, wv)
+        wf.wf_kv_only_prefill_layers(x, wkt, wvt, kc, vc, start, 1e6)
+        torch.cuda.synchronize()
+        rows = slice(start, start + n)
+        for l in range(L):
+            kr, vr = oracle.kv_only_prefill(W.to_oracle(x[l]), W.to_oracle(wk[l]),
+                                            W.to_oracle(wv[l]), start, hkv, dh, 1e6)
+            assert max_vec_rel_err(host64(kc[l][:, rows]), kr) <= TOL["bf16"], (c["case"], l)
+            assert max_vec_rel_err(host64(vc[l][:, rows]), vr) <= TOL["bf16"], (c["case"], l)
+        for a, b in ((kc, k0), (vc, v0)):
+            assert torch.equal(a[:, :, :start], b[:, :, :start]), c["case"]
+            assert torch.equal(a[:, :, start + n:], b[:, :, start + n:]), c["case"]

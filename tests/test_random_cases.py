@@ -91,3 +91,13 @@ def test_tree_lmhead_cases_are_accepted():
             assert c["d"] % 512 == 0 or (c["gamma"] <= 16 and c["d"] in (4096, 5120))
         par = c["parents"]
         assert par[0] == -1 and all(0 <= par[j] < j for j in range(1, c["gamma"]))
+
+
+def test_layer_prefill_cases_are_accepted():
+    cases = R.layer_prefill_cases()
+    assert any(c["tiled"] for c in cases) and any(not c["tiled"] for c in cases)
+    for c in cases:
+        code = wf.WF_BF16_TILED if c["tiled"] else wf.WF_BF16
+        assert c["d_in"] % 32 == 0 and c["layers"] >= 2
+        assert wf.wf_kv_only_prefill_layers_workspace_bytes(
+            code, c["n"], c["d_in"], c["hkv"], c["dh"], c["layers"]) > 0, c
