@@ -22,13 +22,18 @@ constexpr int kGemvWaves = 8;
 constexpr int kGemvBatch = 8;          // 32-wide chunks per wave per load batch
 constexpr int kGemvTargetWorkgroups = 1024;
 
-template <int NBL>
+// FB 16-feature blocks per workgroup: with many rows each workgroup reads
+// its slice of x for FB blocks at once (x would otherwise be re-read by
+// every 16-feature workgroup); fewer chunks per load batch keep the
+// operands in registers.
+template <int NBL, int FB>
 __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     const uint16_t *__restrict__ x, const uint16_t *__restrict__ w_a,
     const uint16_t *__restrict__ w_b, int n_a, float *__restrict__ zpart, int rows,
     int k_in, int n_out, int chunks_per_slice, int tiled) {
-    __shared__ float zs[kGemvWaves][16][16 * NBL + 1];
-    const int f0 = 16 * blockIdx.x;
+    constexpr int BATCH = FB == 1 ? kGemvBatch : kGemvBatch / 2;
+    __shared__ float zs[kGemvWaves][16 * FB][16 * NBL + 1];
+    const int f00 = 16 * FB * blockIdx.x;
     const int ks = blockIdx.y;
     const int wave = wave_id();
     const int lane = threadIdx.x % kWave;
@@ -37,20 +42,24 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     const int c_begin = ks * chunks_per_slice;
     const int n_c = max(0, min(chunks_per_slice, k_in / 32 - c_begin));
 
-    // W operand of chunk c: row-major, 16 bytes of row f0 + m16 per lane;
-    // tiled, the 1 KB tile of the 16-feature block (n_a % 16 == 0, so a
-    // block never straddles the two matrices)
-    const uint16_t *wp;
-    int wstep;
-    if (tiled) {
-        const int blk = f0 < n_a ? f0 / 16 : (f0 - n_a) / 16;
-        wp = (f0 < n_a ? w_a : w_b) + ((size_t)blk * (k_in / 32) + c_begin) * 512 + lane * 8;
-        wstep = 512;
-    } else {
-        const int f = f0 + m16;
-        const uint16_t *wrow = f < n_a ? w_a + (size_t)f * k_in : w_b + (size_t)(f - n_a) * k_in;
-        wp = wrow + (size_t)c_begin * 32 + c4 * 8;
-        wstep = 32;
+    // W operand of chunk c for block fb: row-major, 16 bytes of row
+    // f0 + m16 per lane; tiled, the 1 KB tile of the 16-feature block
+    // (n_a % 16 == 0, so a block never straddles the two matrices)
+    const uint16_t *wp[FB];
+    const int wstep = tiled ? 512 : 32;
+#pragma unroll
+    for (int fb = 0; fb < FB; ++fb) {
+        const int f0 = f00 + 16 * fb;
+        if (tiled) {
+            const int blk = f0 < n_a ? f0 / 16 : (f0 - n_a) / 16;
+            wp[fb] = (f0 < n_a ? w_a : w_b) + ((size_t)blk * (k_in / 32) + c_begin) * 512 +
+                     lane * 8;
+        } else {
+            const int f = f0 + m16;
+            const uint16_t *wrow =
+                f < n_a ? w_a + (size_t)f * k_in : w_b + (size_t)(f - n_a) * k_in;
+            wp[fb] = wrow + (size_t)c_begin * 32 + c4 * 8;
+        }
     }
     // rows past `rows` read the last row: their columns are never used
     const uint16_t *xp[NBL];
@@ -58,45 +67,53 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     for (int nb = 0; nb < NBL; ++nb)
         xp[nb] = x + (size_t)min(16 * nb + m16, rows - 1) * k_in + (size_t)c_begin * 32 + c4 * 8;
 
-    f32x4 acc[NBL];
+    f32x4 acc[FB][NBL];
 #pragma unroll
-    for (int nb = 0; nb < NBL; ++nb)
-        acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int cb = wave; cb < n_c; cb += kGemvWaves * kGemvBatch) {
-        bf16x8 wr[kGemvBatch], xr[kGemvBatch][NBL];
+    for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
-        for (int u = 0; u < kGemvBatch; ++u) {
+        for (int nb = 0; nb < NBL; ++nb)
+            acc[fb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int cb = wave; cb < n_c; cb += kGemvWaves * BATCH) {
+        bf16x8 wr[BATCH][FB], xr[BATCH][NBL];
+#pragma unroll
+        for (int u = 0; u < BATCH; ++u) {
             const int c = cb + kGemvWaves * u;
             if (c < n_c) {
-                wr[u] = load_bf16x8(wp + (size_t)c * wstep);
+#pragma unroll
+                for (int fb = 0; fb < FB; ++fb)
+                    wr[u][fb] = load_bf16x8(wp[fb] + (size_t)c * wstep);
 #pragma unroll
                 for (int nb = 0; nb < NBL; ++nb)
                     xr[u][nb] = load_bf16x8(xp[nb] + c * 32);
             }
         }
 #pragma unroll
-        for (int u = 0; u < kGemvBatch; ++u) {
+        for (int u = 0; u < BATCH; ++u) {
             if (cb + kGemvWaves * u < n_c) {
 #pragma unroll
-                for (int nb = 0; nb < NBL; ++nb)
-                    acc[nb] = mfma16x16x32(wr[u], xr[u][nb], acc[nb]);
+                for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+                    for (int nb = 0; nb < NBL; ++nb)
+                        acc[fb][nb] = mfma16x16x32(wr[u][fb], xr[u][nb], acc[fb][nb]);
             }
         }
     }
-    // lane (m16, c4) holds features 4*c4 + i of row 16*nb + m16
+    // lane (m16, c4) holds features 16*fb + 4*c4 + i of row 16*nb + m16
 #pragma unroll
-    for (int nb = 0; nb < NBL; ++nb)
+    for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            zs[wave][4 * c4 + i][16 * nb + m16] = acc[nb][i];
+        for (int nb = 0; nb < NBL; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                zs[wave][16 * fb + 4 * c4 + i][16 * nb + m16] = acc[fb][nb][i];
     __syncthreads();
-    for (int idx = threadIdx.x; idx < 16 * rows; idx += blockDim.x) {
+    for (int idx = threadIdx.x; idx < 16 * FB * rows; idx += blockDim.x) {
         const int u = idx / rows, r = idx % rows;
         float z = zs[0][u][r];
 #pragma unroll
         for (int ww = 1; ww < kGemvWaves; ++ww)
             z += zs[ww][u][r];
-        zpart[((size_t)ks * n_out + f0 + u) * rows + r] = z;
+        zpart[((size_t)ks * n_out + f00 + u) * rows + r] = z;
     }
 }
 
@@ -304,14 +321,24 @@ wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
     const int n_out = n_a + n_b;
     const int ks = linear_slices(k_in, n_out);
     const int cps = cdiv(k_in / 32, ks);
-    const dim3 grid(n_out / 16, ks);
     const dim3 block(kGemvWaves * kWave);
-    switch (cdiv(rows, 16)) {
-    case 1: linear_partial_bf16<1><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t); break;
-    case 2: linear_partial_bf16<2><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t); break;
-    case 3: linear_partial_bf16<3><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t); break;
-    default: linear_partial_bf16<4><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t); break;
-    }
+    const int nbl = cdiv(rows, 16);
+    // from 12 rows on, four (or two) feature blocks per workgroup where the
+    // features divide evenly: x is then read once per 64 features instead of
+    // once per 16 (64 rows of a 4096-wide x weigh as much as the workgroup's
+    // weights); below that the extra workgroups of single blocks pay more
+    const int tiles = n_out / 16;
+    const int fb = rows < 12 ? 1 : (tiles % 4 == 0 ? 4 : (tiles % 2 == 0 ? 2 : 1));
+    const dim3 grid(tiles / fb, ks);
+#define WF_LIN(NBLV, FBV)                                                                 \
+    if (nbl == NBLV && fb == FBV) {                                                       \
+        linear_partial_bf16<NBLV, FBV><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart,  \
+                                                                rows, k_in, n_out, cps, t);  \
+    } else
+    WF_LIN(1, 1) WF_LIN(1, 2) WF_LIN(1, 4) WF_LIN(2, 1) WF_LIN(2, 2) WF_LIN(2, 4) WF_LIN(3, 1) WF_LIN(3, 2) WF_LIN(3, 4)
+    WF_LIN(4, 1) WF_LIN(4, 2) WF_LIN(4, 4)
+    { return WF_ERR_UNSUPPORTED; }
+#undef WF_LIN
     return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
 }
 
