@@ -65,6 +65,11 @@ FORWARD_CASES = [
     (768, 6, 3, 128, 2048, 77, 64),
     (4096, 32, 8, 128, 12288, 1024, 1),
     (4096, 32, 8, 128, 12288, 700, 16),
+    (4096, 32, 8, 128, 12288, 2000, 64),
+    # 34 feature blocks in W_o and W_down: two blocks per workgroup, with
+    # one and with two 16-row blocks; four blocks per workgroup elsewhere
+    (544, 4, 2, 64, 1056, 50, 14),
+    (544, 4, 2, 64, 1056, 50, 27),
 ]
 
 
