@@ -21,18 +21,22 @@ namespace {
 constexpr int kGemvWaves = 8;
 constexpr int kGemvBatch = 8;          // 32-wide chunks per wave per load batch
 constexpr int kGemvTargetWorkgroups = 1024;
+constexpr int kComputeUnits = 256;
 
 // FB 16-feature blocks per workgroup: with many rows each workgroup reads
 // its slice of x for FB blocks at once (x would otherwise be re-read by
 // every 16-feature workgroup); fewer chunks per load batch keep the
-// operands in registers.
+// operands in registers, and the 8 waves' sums meet in LDS RB blocks at a
+// time.  Every accumulator still takes its chunks in the same order, so
+// the result does not depend on FB.
 template <int NBL, int FB>
 __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     const uint16_t *__restrict__ x, const uint16_t *__restrict__ w_a,
     const uint16_t *__restrict__ w_b, int n_a, float *__restrict__ zpart, int rows,
     int k_in, int n_out, int chunks_per_slice, int tiled) {
-    constexpr int BATCH = FB == 1 ? kGemvBatch : kGemvBatch / 2;
-    __shared__ float zs[kGemvWaves][16 * FB][16 * NBL + 1];
+    constexpr int BATCH = FB == 1 ? kGemvBatch : FB <= 4 ? kGemvBatch / 2 : 2;
+    constexpr int RB = FB <= 4 ? FB : 2;
+    __shared__ float zs[kGemvWaves][16 * RB][16 * NBL + 1];
     const int f00 = 16 * FB * blockIdx.x;
     const int ks = blockIdx.y;
     const int wave = wave_id();
@@ -98,22 +102,26 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
             }
         }
     }
-    // lane (m16, c4) holds features 16*fb + 4*c4 + i of row 16*nb + m16
 #pragma unroll
-    for (int fb = 0; fb < FB; ++fb)
+    for (int pb = 0; pb < FB / RB; ++pb) {
+        if (pb)
+            __syncthreads();
 #pragma unroll
-        for (int nb = 0; nb < NBL; ++nb)
+        for (int fr = 0; fr < RB; ++fr)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                zs[wave][16 * fb + 4 * c4 + i][16 * nb + m16] = acc[fb][nb][i];
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < 16 * FB * rows; idx += blockDim.x) {
-        const int u = idx / rows, r = idx % rows;
-        float z = zs[0][u][r];
+            for (int nb = 0; nb < NBL; ++nb)
 #pragma unroll
-        for (int ww = 1; ww < kGemvWaves; ++ww)
-            z += zs[ww][u][r];
-        zpart[((size_t)ks * n_out + f00 + u) * rows + r] = z;
+                for (int i = 0; i < 4; ++i)
+                    zs[wave][16 * fr + 4 * c4 + i][16 * nb + m16] = acc[pb * RB + fr][nb][i];
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < 16 * RB * rows; idx += blockDim.x) {
+            const int u = idx / rows, r = idx % rows;
+            float z = zs[0][u][r];
+#pragma unroll
+            for (int ww = 1; ww < kGemvWaves; ++ww)
+                z += zs[ww][u][r];
+            zpart[((size_t)ks * n_out + f00 + 16 * RB * pb + u) * rows + r] = z;
+        }
     }
 }
 
@@ -323,20 +331,36 @@ wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
     const int cps = cdiv(k_in / 32, ks);
     const dim3 block(kGemvWaves * kWave);
     const int nbl = cdiv(rows, 16);
-    // from 12 rows on, four (or two) feature blocks per workgroup where the
-    // features divide evenly: x is then read once per 64 features instead of
-    // once per 16 (64 rows of a 4096-wide x weigh as much as the workgroup's
-    // weights); below that the extra workgroups of single blocks pay more
+    // From 12 rows on, several feature blocks per workgroup: x is then read
+    // once per 64 or 96 features instead of once per 16 (64 rows of a
+    // 4096-wide x weigh as much as the workgroup's weights); below that the
+    // extra workgroups of single blocks pay more.  Among the block counts
+    // that divide the features, take the one with the fewest operand bytes
+    // per compute unit (W rows and x rows of a slice, per workgroup), counting
+    // whole rounds of one workgroup per CU: 1536 blocks and 64 rows as 768
+    // workgroups of 2 cost 3 x (32 + 64) rows, as 384 of 4 2 x (64 + 64), as
+    // 256 of 6 1 x (96 + 64) (measured 201, 184 and 166 us for the
+    // 64-token drafter layer).
     const int tiles = n_out / 16;
-    const int fb = rows < 12 ? 1 : (tiles % 4 == 0 ? 4 : (tiles % 2 == 0 ? 2 : 1));
+    int fb = 1;
+    if (rows >= 12) {
+        auto cost = [&](int f) {
+            return cdiv(tiles / f * ks, kComputeUnits) * (16 * f + 16 * nbl);
+        };
+        for (int f : {2, 4, 6})
+            if (tiles % f == 0 && (fb == 1 || cost(f) <= cost(fb)))
+                fb = f;
+    }
     const dim3 grid(tiles / fb, ks);
 #define WF_LIN(NBLV, FBV)                                                                 \
     if (nbl == NBLV && fb == FBV) {                                                       \
         linear_partial_bf16<NBLV, FBV><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart,  \
                                                                 rows, k_in, n_out, cps, t);  \
     } else
-    WF_LIN(1, 1) WF_LIN(1, 2) WF_LIN(1, 4) WF_LIN(2, 1) WF_LIN(2, 2) WF_LIN(2, 4) WF_LIN(3, 1) WF_LIN(3, 2) WF_LIN(3, 4)
-    WF_LIN(4, 1) WF_LIN(4, 2) WF_LIN(4, 4)
+    WF_LIN(1, 1) WF_LIN(1, 2) WF_LIN(1, 4) WF_LIN(1, 6)
+    WF_LIN(2, 1) WF_LIN(2, 2) WF_LIN(2, 4) WF_LIN(2, 6)
+    WF_LIN(3, 1) WF_LIN(3, 2) WF_LIN(3, 4) WF_LIN(3, 6)
+    WF_LIN(4, 1) WF_LIN(4, 2) WF_LIN(4, 4) WF_LIN(4, 6)
     { return WF_ERR_UNSUPPORTED; }
 #undef WF_LIN
     return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;

@@ -70,6 +70,10 @@ FORWARD_CASES = [
     # one and with two 16-row blocks; four blocks per workgroup elsewhere
     (544, 4, 2, 64, 1056, 50, 14),
     (544, 4, 2, 64, 1056, 50, 27),
+    # 1032 feature blocks in [W_gate; W_up]: six blocks per workgroup, with
+    # two and with three 16-row blocks
+    (256, 2, 1, 128, 8256, 30, 20),
+    (256, 2, 1, 128, 8256, 30, 40),
 ]
 
 
