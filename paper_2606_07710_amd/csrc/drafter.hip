@@ -333,12 +333,18 @@ wf_status_t drafter_forward(const wf_decoder_layer_t &L, const uint16_t *rb, int
         zp, linear_slices(qd, d), d, M, rb, h1);
     rmsnorm_bf16<<<M, kNormThreads, 0, stream>>>(h1, W(L.mlp_norm), L.rms_eps, xn2, d, M,
                                                   nullptr);
-    // act = SiLU(Wg xn2) * (Wu xn2)
-    if ((st = launch_linear_partial(xn2, W(L.w_gate), W(L.w_up), I, I, M, d, zp, stream,
-                                    tiled)) != WF_OK)
+    // act = SiLU(Wg xn2) * (Wu xn2): in one launch where the input
+    // dimension is not split, else slices and a separate SwiGLU pass
+    st = launch_linear_swiglu(xn2, W(L.w_gate), W(L.w_up), I, M, d, act, stream, tiled);
+    if (st == WF_ERR_UNSUPPORTED) {
+        if ((st = launch_linear_partial(xn2, W(L.w_gate), W(L.w_up), I, I, M, d, zp, stream,
+                                        tiled)) != WF_OK)
+            return st;
+        reduce_swiglu_bf16<<<blocks_for((long long)M * I), 256, 0, stream>>>(
+            zp, linear_slices(d, 2 * I), I, M, act);
+    } else if (st != WF_OK) {
         return st;
-    reduce_swiglu_bf16<<<blocks_for((long long)M * I), 256, 0, stream>>>(
-        zp, linear_slices(d, 2 * I), I, M, act);
+    }
     // out = h1 + Wd act
     if ((st = launch_linear_partial(act, W(L.w_down), nullptr, d, 0, M, I, zp, stream, tiled)) != WF_OK)
         return st;

@@ -29,13 +29,22 @@ constexpr int kComputeUnits = 256;
 // operands in registers, and the 8 waves' sums meet in LDS RB blocks at a
 // time.  Every accumulator still takes its chunks in the same order, so
 // the result does not depend on FB.
-template <int NBL, int FB>
+//
+// SWI (one slice, w_a = W_gate and w_b = W_up, both n_a features): the
+// first FB/2 blocks of workgroup b are gate blocks FB/2 * b + j and the
+// rest the matching up blocks, and the epilogue stores
+// act[r][f] = bf16(SiLU(gate) * up) instead of the fp32 sums: the same
+// values, rounded the same way, as the sums followed by the separate
+// SwiGLU kernel.
+template <int NBL, int FB, bool SWI = false>
 __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     const uint16_t *__restrict__ x, const uint16_t *__restrict__ w_a,
     const uint16_t *__restrict__ w_b, int n_a, float *__restrict__ zpart, int rows,
-    int k_in, int n_out, int chunks_per_slice, int tiled) {
+    int k_in, int n_out, int chunks_per_slice, int tiled, uint16_t *__restrict__ act) {
+    static_assert(!SWI || (FB % 2 == 0), "gate and up blocks come in pairs");
     constexpr int BATCH = FB == 1 ? kGemvBatch : FB <= 4 ? kGemvBatch / 2 : 2;
-    constexpr int RB = FB <= 4 ? FB : 2;
+    constexpr int RB = (SWI || FB > 4) ? 2 : FB;
+    constexpr int HB = FB / 2;
     __shared__ float zs[kGemvWaves][16 * RB][16 * NBL + 1];
     const int f00 = 16 * FB * blockIdx.x;
     const int ks = blockIdx.y;
@@ -53,7 +62,8 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
     const int wstep = tiled ? 512 : 32;
 #pragma unroll
     for (int fb = 0; fb < FB; ++fb) {
-        const int f0 = f00 + 16 * fb;
+        const int f0 = SWI ? 16 * (HB * (int)blockIdx.x + fb % HB) + (fb < HB ? 0 : n_a)
+                           : f00 + 16 * fb;
         if (tiled) {
             const int blk = f0 < n_a ? f0 / 16 : (f0 - n_a) / 16;
             wp[fb] = (f0 < n_a ? w_a : w_b) + ((size_t)blk * (k_in / 32) + c_begin) * 512 +
@@ -112,8 +122,27 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
             for (int nb = 0; nb < NBL; ++nb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    zs[wave][16 * fr + 4 * c4 + i][16 * nb + m16] = acc[pb * RB + fr][nb][i];
+                    zs[wave][16 * fr + 4 * c4 + i][16 * nb + m16] =
+                        acc[SWI ? pb + HB * fr : pb * RB + fr][nb][i];
         __syncthreads();
+        if constexpr (SWI) {
+            // gate block pb in zs rows 0..15, its up block in 16..31; 16
+            // consecutive features per row, so the stores form 32-byte runs
+            const int g0 = 16 * (HB * (int)blockIdx.x + pb);
+            for (int idx = threadIdx.x; idx < 16 * rows; idx += blockDim.x) {
+                const int u = idx % 16, r = idx / 16;
+                float zg = zs[0][u][r], zu = zs[0][16 + u][r];
+#pragma unroll
+                for (int ww = 1; ww < kGemvWaves; ++ww) {
+                    zg += zs[ww][u][r];
+                    zu += zs[ww][16 + u][r];
+                }
+                // (0 + z: the sum over one slice, as the slice sum forms it)
+                const float gt = 0.f + zg, up = 0.f + zu;
+                act[(size_t)r * n_a + g0 + u] = f32_to_bf16(gt / (1.f + expf(-gt)) * up);
+            }
+            continue;
+        }
         for (int idx = threadIdx.x; idx < 16 * RB * rows; idx += blockDim.x) {
             const int u = idx / rows, r = idx % rows;
             float z = zs[0][u][r];
@@ -354,8 +383,8 @@ wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
     const dim3 grid(tiles / fb, ks);
 #define WF_LIN(NBLV, FBV)                                                                 \
     if (nbl == NBLV && fb == FBV) {                                                       \
-        linear_partial_bf16<NBLV, FBV><<<grid, block, 0, stream>>>(x, w_a, w_b, n_a, zpart,  \
-                                                                rows, k_in, n_out, cps, t);  \
+        linear_partial_bf16<NBLV, FBV><<<grid, block, 0, stream>>>(                       \
+            x, w_a, w_b, n_a, zpart, rows, k_in, n_out, cps, t, nullptr);                 \
     } else
     WF_LIN(1, 1) WF_LIN(1, 2) WF_LIN(1, 4) WF_LIN(1, 6)
     WF_LIN(2, 1) WF_LIN(2, 2) WF_LIN(2, 4) WF_LIN(2, 6)
@@ -363,6 +392,38 @@ wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
     WF_LIN(4, 1) WF_LIN(4, 2) WF_LIN(4, 4) WF_LIN(4, 6)
     { return WF_ERR_UNSUPPORTED; }
 #undef WF_LIN
+    return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
+}
+
+wf_status_t launch_linear_swiglu(const uint16_t *x, const uint16_t *w_gate,
+                                 const uint16_t *w_up, int inter, int rows, int k_in,
+                                 uint16_t *act, hipStream_t stream, bool tiled) {
+    const int tiles = 2 * inter / 16;
+    const int nbl = cdiv(rows, 16);
+    if (rows < 12 || rows > 64 || inter % 16 || k_in % 32 || linear_slices(k_in, 2 * inter) != 1)
+        return WF_ERR_UNSUPPORTED;
+    // the block count of the split launch's rule, among those whose gate
+    // half divides the gate blocks
+    auto cost = [&](int f) { return cdiv(tiles / f, kComputeUnits) * (16 * f + 16 * nbl); };
+    int fb = 0;
+    for (int f : {2, 4, 6})
+        if ((inter / 16) % (f / 2) == 0 && (fb == 0 || cost(f) <= cost(fb)))
+            fb = f;
+    if (fb == 0)
+        return WF_ERR_UNSUPPORTED;
+    const dim3 grid(tiles / fb, 1);
+    const dim3 block(kGemvWaves * kWave);
+    const int t = tiled ? 1 : 0;
+    const int cps = k_in / 32;
+#define WF_SWI(NBLV, FBV)                                                                 \
+    if (nbl == NBLV && fb == FBV) {                                                       \
+        linear_partial_bf16<NBLV, FBV, true><<<grid, block, 0, stream>>>(                 \
+            x, w_gate, w_up, inter, nullptr, rows, k_in, 2 * inter, cps, t, act);         \
+    } else
+    WF_SWI(1, 2) WF_SWI(1, 4) WF_SWI(1, 6) WF_SWI(2, 2) WF_SWI(2, 4) WF_SWI(2, 6)
+    WF_SWI(3, 2) WF_SWI(3, 4) WF_SWI(3, 6) WF_SWI(4, 2) WF_SWI(4, 4) WF_SWI(4, 6)
+    { return WF_ERR_UNSUPPORTED; }
+#undef WF_SWI
     return hipGetLastError() == hipSuccess ? WF_OK : WF_ERR_HIP;
 }
 

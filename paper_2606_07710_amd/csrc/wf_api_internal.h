@@ -81,6 +81,13 @@ wf_status_t launch_linear_partial(const uint16_t *x, const uint16_t *w_a,
                                   const uint16_t *w_b, int n_a, int n_b, int rows,
                                   int k_in, float *zpart, hipStream_t stream,
                                   bool tiled = false);
+// act[r][f] = bf16(SiLU(W_gate[f] . x[r]) * (W_up[f] . x[r])) in one launch,
+// for 12..64 rows where the input dimension is not split (otherwise
+// WF_ERR_UNSUPPORTED, and the caller takes launch_linear_partial and a
+// separate SwiGLU pass, which give the same bits).
+wf_status_t launch_linear_swiglu(const uint16_t *x, const uint16_t *w_gate,
+                                 const uint16_t *w_up, int inter, int rows, int k_in,
+                                 uint16_t *act, hipStream_t stream, bool tiled = false);
 
 // Single-token skinny linear layers with their epilogue in the kernel
 // (gemv.hip): y = res + W x; act = SiLU(Wg x') * (Wu x') with
