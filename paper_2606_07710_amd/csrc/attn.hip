@@ -115,16 +115,29 @@ __device__ __forceinline__ void lds_dma16(const void *src, unsigned lds) {
 
 // The same copy addressed as a wave-uniform 64-bit base (SGPRs) plus a
 // 32-bit per-lane byte offset: no per-lane address arithmetic at issue.
+// NT: with the non-temporal hint, for tiles that only this workgroup reads.
+template <bool NT = false>
 __device__ __forceinline__ void lds_dma16_so(const char *base, unsigned voff, unsigned lds) {
-    asm volatile("s_mov_b32 m0, %2\n\t"
-                 "s_nop 0\n\t"
-                 "global_load_lds_dwordx4 %0, %1"
-                 :
-                 : "v"(voff), "s"(base), "s"(lds)
-                 : "memory", "m0");
+    if constexpr (NT)
+        asm volatile("s_mov_b32 m0, %2\n\t"
+                     "s_nop 0\n\t"
+                     "global_load_lds_dwordx4 %0, %1 nt"
+                     :
+                     : "v"(voff), "s"(base), "s"(lds)
+                     : "memory", "m0");
+    else
+        asm volatile("s_mov_b32 m0, %2\n\t"
+                     "s_nop 0\n\t"
+                     "global_load_lds_dwordx4 %0, %1"
+                     :
+                     : "v"(voff), "s"(base), "s"(lds)
+                     : "memory", "m0");
 }
 
-template <int DH, int NBW, int RG, int KS, int NBUF>
+// NT: the K/V tiles are copied with the non-temporal hint; the launch sets
+// it when one row group covers each head, so a workgroup is the only reader
+// of its tiles (several row groups share them through L2).
+template <int DH, int NBW, int RG, int KS, int NBUF, bool NT>
 __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) {
     using TG = TileGeom<DH>;
     constexpr int KC = DH / 32;
@@ -249,7 +262,7 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
         const int kb = k_begin + t * kTileKeys;
         const unsigned slot = lds_addr(ring(bi)) + stream * TG::kTileBytes;
         const size_t tile_off = (size_t)kb * TG::kRowBytes;
-        auto go = [&](auto clamp_tag) __attribute__((always_inline)) {
+        auto go = [&](auto clamp_tag, auto nt_tag) __attribute__((always_inline)) {
 #pragma unroll
             for (int jr = 0; jr < LPW; ++jr) {
                 const int j = rgi + jr * RG;
@@ -262,14 +275,14 @@ __global__ __launch_bounds__(64 * KS * RG) void attn_partial_bf16(AttnParams a) 
                     off = voff[jr];
                 else
                     off = src_off(jr, kTileKeys - 1);
-                lds_dma16_so((is_v ? vg : kg) + tile_off, off,
-                             slot + (is_v ? TG::kHalfBytes : 0) + jj * 1024);
+                lds_dma16_so<decltype(nt_tag)::value>(
+                    (is_v ? vg : kg) + tile_off, off, slot + (is_v ? TG::kHalfBytes : 0) + jj * 1024);
             }
         };
         if (kb + kTileKeys - 1 <= last_key)
-            go(std::false_type{});
+            go(std::false_type{}, std::integral_constant<bool, NT>{});
         else
-            go(std::true_type{});
+            go(std::true_type{}, std::integral_constant<bool, NT>{});
     };
 
     // ---- Q^T operands and causal limits of this wave's rows ------------------
@@ -1171,7 +1184,10 @@ wf_status_t launch_attn(wf_dtype_t dt, const void *q, const void *k_cache,
 #define WF_ATTN_CASE(DHV, NBV, RGV, KSV, NBUFV)                                      \
     if (head_dim == DHV && p.nb == NBV && p.rg == RGV && p.ks == KSV &&               \
         p.nbuf == NBUFV) {                                                            \
-        attn_partial_bf16<DHV, NBV, RGV, KSV, NBUFV><<<grid, block, 0, stream>>>(a);  \
+        if (p.n_row_groups == 1)                                                      \
+            attn_partial_bf16<DHV, NBV, RGV, KSV, NBUFV, true><<<grid, block, 0, stream>>>(a);  \
+        else                                                                          \
+            attn_partial_bf16<DHV, NBV, RGV, KSV, NBUFV, false><<<grid, block, 0, stream>>>(a); \
     } else
         WF_ATTN_CASE(128, 1, 1, 2, 3) WF_ATTN_CASE(128, 1, 2, 2, 3)
         WF_ATTN_CASE(128, 1, 4, 1, 3) WF_ATTN_CASE(128, 1, 4, 2, 3)

@@ -95,7 +95,7 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_partial_bf16(
             if (c < n_c) {
 #pragma unroll
                 for (int fb = 0; fb < FB; ++fb)
-                    wr[u][fb] = load_bf16x8(wp[fb] + (size_t)c * wstep);
+                    wr[u][fb] = load_bf16x8_nt(wp[fb] + (size_t)c * wstep);
 #pragma unroll
                 for (int nb = 0; nb < NBL; ++nb)
                     xr[u][nb] = load_bf16x8(xp[nb] + c * 32);
@@ -227,7 +227,7 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void linear_epi_bf16(EpiParams 
             if (c < n_c) {
 #pragma unroll
                 for (int j = 0; j < NBLK; ++j)
-                    wr[u][j] = load_bf16x8(wp[j] + (size_t)c * wstep);
+                    wr[u][j] = load_bf16x8_nt(wp[j] + (size_t)c * wstep);
                 xr[u] = load_bf16x8(xp + c * 32);
                 if constexpr (MODE == kEpiSwiglu)
                     gr[u] = *reinterpret_cast<const u32x4 *>(gp + c * 32);

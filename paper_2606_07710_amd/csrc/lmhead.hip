@@ -245,7 +245,7 @@ __global__ __launch_bounds__(512) void lm_tiles_bf16(const uint16_t *__restrict_
         const int off = (wave + kLmWaves * u) * 32;
 #pragma unroll
         for (int mb = 0; mb < kLmMB; ++mb)
-            wr[mb] = load_bf16x8(wp[mb] + off);
+            wr[mb] = load_bf16x8_nt(wp[mb] + off);
 #pragma unroll
         for (int nb = 0; nb < NBL; ++nb)
             hr[nb] = load_bf16x8(hp[nb] + off);
@@ -380,7 +380,7 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
         for (int p = 0; p < P; ++p)
 #pragma unroll
             for (int mb = 0; mb < kLmMB; ++mb)
-                wb[p][mb] = load_bf16x8(wrow(t0, mb) + p * cs);
+                wb[p][mb] = load_bf16x8_nt(wrow(t0, mb) + p * cs);
     }
     RowState run[2] = {state_empty(), state_empty()};
 
@@ -409,11 +409,11 @@ __global__ __launch_bounds__(512) void lm_stream_bf16(const uint16_t *__restrict
             if (u + P < CPW) {
 #pragma unroll
                 for (int mb = 0; mb < kLmMB; ++mb)
-                    wb[p][mb] = load_bf16x8(cur[mb] + (u + P) * cs);
+                    wb[p][mb] = load_bf16x8_nt(cur[mb] + (u + P) * cs);
             } else if (!LAST) {
 #pragma unroll
                 for (int mb = 0; mb < kLmMB; ++mb)
-                    wb[p][mb] = load_bf16x8(nxt[mb] + (u + P - CPW) * cs);
+                    wb[p][mb] = load_bf16x8_nt(nxt[mb] + (u + P - CPW) * cs);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -550,7 +550,7 @@ __global__ __launch_bounds__(512) void lm_wide_bf16(const uint16_t *__restrict__
         for (int p = 0; p < P; ++p)
 #pragma unroll
             for (int j = 0; j < MBW; ++j)
-                wb[p][j] = load_bf16x8(wrow[j] + p * cs);
+                wb[p][j] = load_bf16x8_nt(wrow[j] + p * cs);
         __syncthreads();
     }
 
@@ -582,7 +582,7 @@ __global__ __launch_bounds__(512) void lm_wide_bf16(const uint16_t *__restrict__
             if (!LAST || u + P < CPB) {
 #pragma unroll
                 for (int j = 0; j < MBW; ++j)
-                    wb[p][j] = load_bf16x8(wrow[j] + (size_t)(cbase + u + P) * cs);
+                    wb[p][j] = load_bf16x8_nt(wrow[j] + (size_t)(cbase + u + P) * cs);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
