@@ -905,6 +905,7 @@ __global__ __launch_bounds__(64) void attn_partial_f32(AttnParams a) {
 // butterfly.  The first batch of partial loads is issued before the weights
 // are formed, so a merge over up to G*kMergeBatch splits is one round trip.
 // ---------------------------------------------------------------------------
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kMergeBatch = 16;          // float4 loads in flight per lane
 constexpr int kMaxSplits = 1024;
 
@@ -930,7 +931,9 @@ __global__ __launch_bounds__(64) void attn_merge(const void *__restrict__ ws_o,
             const size_t idx = (size_t)min(s0 + G * b, splits - 1) * sstride +
                                (size_t)pr * Q + d4;
             if constexpr (BF16) {
-                const uint2 pk = reinterpret_cast<const uint2 *>(ws_o)[idx];
+                // (each partial is read once: non-temporal)
+            const u32x2 pt = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(ws_o) + idx);
+            const uint2 pk = {pt.x, pt.y};
                 v[b] = f32x4{bf16_to_f32((uint16_t)pk.x), bf16_to_f32((uint16_t)(pk.x >> 16)),
                              bf16_to_f32((uint16_t)pk.y), bf16_to_f32((uint16_t)(pk.y >> 16))};
             } else {
@@ -1020,7 +1023,9 @@ __global__ __launch_bounds__(64 * WPB) void attn_merge_one(const void *__restric
         const int sp = min(grp + G * b, splits - 1);
         const size_t idx = (size_t)sp * sstride + (size_t)pr * Q + d4;
         if constexpr (BF16) {
-            const uint2 pk = reinterpret_cast<const uint2 *>(ws_o)[idx];
+            // (each partial is read once: non-temporal)
+            const u32x2 pt = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(ws_o) + idx);
+            const uint2 pk = {pt.x, pt.y};
             v[b] = f32x4{bf16_to_f32((uint16_t)pk.x), bf16_to_f32((uint16_t)(pk.x >> 16)),
                          bf16_to_f32((uint16_t)pk.y), bf16_to_f32((uint16_t)(pk.y >> 16))};
         } else {
